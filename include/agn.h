@@ -1,0 +1,167 @@
+/*
+ * agn.h -- C ABI of libagn, the MI355X (gfx950) implementation of the hot
+ * path of Accumulated Gradient Normalization (AGN; Hermans, Spanakis and
+ * Moeckel, ACML 2017).
+ *
+ * The library simulates n AGN workers and the parameter server on one GPU.
+ * One call to agn_round() is one round of the method: every worker runs
+ * lambda local mini-batch SGD steps on its own copy of a ReLU MLP with a
+ * softmax cross-entropy output (Algorithm 1, inner loop), normalizes its
+ * accumulated update by lambda (Algorithm 1, normalization step; Eq. 1),
+ * and the commits are added to the central variable in the caller's order
+ * (Eq. 2), each worker pulling the central variable right after its own
+ * commit (Algorithm 1, final pull; the FIFO queue of Section 1).
+ *
+ * Conventions shared by every entry point:
+ *   - Every function returns an int status: AGN_OK (0) or a negative code.
+ *     No C++ exception crosses the ABI.  On error, agn_last_error() gives
+ *     a message; the context's state is unchanged unless the code is
+ *     AGN_EHIP, after which the context is poisoned (every later call
+ *     returns AGN_ESTATE) and should be destroyed.
+ *   - "DEVICE" pointers are HIP device pointers on the device that was
+ *     current at agn_create(); "HOST" pointers are ordinary host memory.
+ *     The caller owns every buffer it passes; the library keeps no pointer
+ *     to caller memory beyond the call.
+ *   - Work is enqueued on the context's stream (agn_set_stream; default:
+ *     the null stream).  agn_round() returns without waiting; agn_central,
+ *     agn_loss, agn_worker_params and agn_debug_batch_indices wait for the
+ *     stream before returning.
+ *   - A context is not thread-safe; use one context per host thread.
+ *
+ * Parameter layout seen by callers ("packed"): W_0, b_0, W_1, b_1, ...,
+ * W_l row-major with shape [d_{l+1}][d_l], b_l of length d_{l+1};
+ * P = sum_l (d_l * d_{l+1} + d_{l+1}) floats.
+ */
+#ifndef AGN_H
+#define AGN_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* status codes */
+#define AGN_OK 0
+#define AGN_EINVAL (-1) /* bad argument, shape or commit order */
+#define AGN_ENOMEM (-2) /* device or host allocation failed */
+#define AGN_EHIP (-3)   /* HIP runtime or launch error; context poisoned */
+#define AGN_ESTATE (-4) /* poisoned context, or call out of order */
+
+/* arithmetic of the matrix products */
+#define AGN_FP32 0 /* float32 operands, float32 accumulation */
+#define AGN_BF16 1 /* bfloat16 operands (inputs, weight shadows, hidden
+                      activations, output-side gradients), float32
+                      accumulation, float32 master weights and central
+                      variable */
+
+#define AGN_MAX_LAYERS 16
+#define AGN_MAX_WORKERS 256
+
+typedef struct agn_ctx agn_ctx; /* opaque; owned by the library */
+
+/* Shapes of the model (Section 4 runs the same MLP on every worker). */
+typedef struct {
+  int32_t num_layers;   /* L, 1 <= L <= AGN_MAX_LAYERS (weight layers)       */
+  const int32_t* dims;  /* HOST, L+1 widths: dims[0] inputs, dims[L] = C >= 2
+                           classes; every width >= 1                          */
+  int32_t batch;        /* mini-batch size m >= 1 (Eq. 1)                     */
+  int32_t dtype;        /* AGN_FP32 or AGN_BF16                               */
+} agn_shapes;
+
+/* Training data of one round; worker k owns rows [k*S, (k+1)*S),
+ * S = floor(num_samples / n) (Section 1: n shards; Section 4: data equally
+ * distributed over the workers). */
+typedef struct {
+  const void* x;        /* DEVICE, [num_samples][dims[0]] row-major: float32
+                           (x_dtype 0) or bfloat16 bit patterns (x_dtype 1)  */
+  const int32_t* y;     /* DEVICE, [num_samples] labels in [0, C).  Not
+                           range-checked on the device: the caller
+                           guarantees the range.                             */
+  int64_t num_samples;  /* N >= n                                            */
+  int32_t x_dtype;      /* 0 float32, 1 bfloat16; must be 1 iff the shapes'
+                           dtype is AGN_BF16                                 */
+} agn_data;
+
+/* Create a context: validates every argument first (AGN_EINVAL, nothing
+ * allocated), allocates all device state (no allocation happens later in
+ * agn_round), draws the initial central variable from `seed` (He-normal
+ * weights N(0, 2/d_in) from a SplitMix64 stream through Box-Muller, biases
+ * zero) and gives every worker a copy of it (Algorithm 1, first pull).
+ * n in [1, AGN_MAX_WORKERS]; lambda >= 1 local steps; eta finite learning
+ * rate (constant: Section 4 applies no decay).  *out receives the context
+ * (NULL on failure). */
+int agn_create(const agn_shapes* shapes, int32_t n, int32_t lambda, float eta,
+               uint64_t seed, agn_ctx** out);
+
+/* Use `hip_stream` (a hipStream_t; NULL = null stream) for all later work. */
+int agn_set_stream(agn_ctx* ctx, void* hip_stream);
+
+/* Enqueue one AGN round.  commit_order: HOST, n entries, a permutation of
+ * 0..n-1 (checked on the host; AGN_EINVAL leaves the state unchanged).
+ * The j-th entry is the worker whose normalized delta is the j-th to be
+ * added to the central variable (Eq. 2); that worker then pulls.  Worker k
+ * at its local step t (counted from 0 over all rounds) uses the rows
+ * k*S + ((t*m + j) mod S), j = 0..m-1 (FetchNextMiniBatch of Algorithm 1).
+ * data->num_samples must be the same on every round of a context. */
+int agn_round(agn_ctx* ctx, const agn_data* data, const int32_t* commit_order);
+
+/* Copy the central variable into out (DEVICE, P floats, packed layout). */
+int agn_central(agn_ctx* ctx, float* out);
+
+/* Per-worker training loss of the last round: for worker k (indexed by
+ * worker id, not commit position), the mean over its lambda steps of the
+ * mini-batch mean softmax cross-entropy, each evaluated at the worker's
+ * parameters before that step's update.  out: DEVICE, n floats.
+ * AGN_ESTATE before the first round. */
+int agn_loss(agn_ctx* ctx, float* out);
+
+/* Number of parameters P (-1 for a NULL context). */
+int64_t agn_num_params(const agn_ctx* ctx);
+
+/* Message of the last error of ctx, or of the last failed agn_create when
+ * ctx is NULL.  Never NULL; valid until the next call on the same ctx. */
+const char* agn_last_error(const agn_ctx* ctx);
+
+/* Free everything (waits for the stream first).  NULL is a no-op. */
+void agn_destroy(agn_ctx* ctx);
+
+/* ---- test hooks (not on the timed path) ------------------------------- */
+
+/* Before the first round only (AGN_ESTATE otherwise): set the central
+ * variable and every worker's copy to `in` (DEVICE, P floats, packed). */
+int agn_set_central(agn_ctx* ctx, const float* in);
+
+/* Copy worker k's current parameters (its last pulled copy of the central
+ * variable, the start of its next round) into out (DEVICE, P floats). */
+int agn_worker_params(agn_ctx* ctx, int32_t worker, float* out);
+
+/* The m sample indices worker `worker` uses at local step `step_t`, for a
+ * data set of `num_samples` rows: out (DEVICE, m int64). */
+int agn_debug_batch_indices(agn_ctx* ctx, int32_t worker, int64_t step_t,
+                            int64_t num_samples, int64_t* out);
+
+/* ---- kernel timing ------------------------------------------------------ */
+
+/* Kernel classes, in the order a local step launches them. */
+#define AGN_K_FWD 0     /* forward product + bias + ReLU (and output logits) */
+#define AGN_K_SOFTMAX 1 /* softmax cross-entropy, loss, output gradient      */
+#define AGN_K_DX 2      /* input-gradient product + ReLU mask                */
+#define AGN_K_DW 3      /* weight-gradient product + fused SGD update        */
+#define AGN_K_COMMIT 4  /* normalize + commit + pull                         */
+#define AGN_K_NUM 5
+
+/* When enabled, every launch of the given class is bracketed by HIP events
+ * on the context's stream.  Enabling resets the counters. */
+int agn_set_kernel_timing(agn_ctx* ctx, int32_t kernel_class, int32_t enable);
+
+/* Total milliseconds and number of launches of the class since timing was
+ * enabled (waits for the stream). */
+int agn_kernel_timing(agn_ctx* ctx, int32_t kernel_class, double* total_ms,
+                      int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AGN_H */

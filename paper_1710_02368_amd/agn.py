@@ -1,0 +1,228 @@
+"""Python binding of libagn (argument marshalling only).
+
+The functions mirror the C ABI in include/agn.h one to one.  Device
+buffers are torch tensors on a ROCm device; the library receives their
+raw pointers and the current torch stream.  Every step of the AGN round
+runs in the HIP kernels of libagn: there is no Python or CPU fallback, and
+loading fails loudly when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Sequence
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libagn.so")
+
+AGN_OK, AGN_EINVAL, AGN_ENOMEM, AGN_EHIP, AGN_ESTATE = 0, -1, -2, -3, -4
+AGN_FP32, AGN_BF16 = 0, 1
+AGN_K_FWD, AGN_K_SOFTMAX, AGN_K_DX, AGN_K_DW, AGN_K_COMMIT = range(5)
+KERNEL_CLASSES = {"fwd": AGN_K_FWD, "softmax": AGN_K_SOFTMAX, "dx": AGN_K_DX,
+                  "dw": AGN_K_DW, "commit": AGN_K_COMMIT}
+
+EXPORTED = [
+    "agn_create", "agn_set_stream", "agn_round", "agn_central", "agn_loss",
+    "agn_num_params", "agn_last_error", "agn_destroy", "agn_set_central",
+    "agn_worker_params", "agn_debug_batch_indices", "agn_set_kernel_timing",
+    "agn_kernel_timing",
+]
+
+
+class agn_shapes(ctypes.Structure):
+    _fields_ = [("num_layers", ctypes.c_int32), ("dims", ctypes.POINTER(ctypes.c_int32)),
+                ("batch", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class agn_data(ctypes.Structure):
+    _fields_ = [("x", ctypes.c_void_p), ("y", ctypes.c_void_p),
+                ("num_samples", ctypes.c_int64), ("x_dtype", ctypes.c_int32)]
+
+
+class AGNError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"libagn error {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libagn.so (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with __graft_entry__.build() "
+                           "or python -m paper_1710_02368_amd.build")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    sig = {
+        "agn_create": (i32, [ctypes.POINTER(agn_shapes), i32, i32, ctypes.c_float, ctypes.c_uint64,
+                             ctypes.POINTER(vp)]),
+        "agn_set_stream": (i32, [vp, vp]),
+        "agn_round": (i32, [vp, ctypes.POINTER(agn_data), ctypes.POINTER(ctypes.c_int32)]),
+        "agn_central": (i32, [vp, vp]),
+        "agn_loss": (i32, [vp, vp]),
+        "agn_num_params": (i64, [vp]),
+        "agn_last_error": (ctypes.c_char_p, [vp]),
+        "agn_destroy": (None, [vp]),
+        "agn_set_central": (i32, [vp, vp]),
+        "agn_worker_params": (i32, [vp, i32, vp]),
+        "agn_debug_batch_indices": (i32, [vp, i32, i64, i64, vp]),
+        "agn_set_kernel_timing": (i32, [vp, i32, i32]),
+        "agn_kernel_timing": (i32, [vp, i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(lib, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(code, ctx=None):
+    if code != AGN_OK:
+        msg = load_library().agn_last_error(ctx)
+        raise AGNError(code, msg.decode() if msg else "")
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_ptr():
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+# --------------------------------------------------------------------------
+# the C ABI, one function each
+# --------------------------------------------------------------------------
+
+def agn_create(dims: Sequence[int], batch: int, n: int, lam: int, eta: float, seed: int,
+               dtype: int = AGN_FP32):
+    lib = load_library()
+    d = (ctypes.c_int32 * len(dims))(*[int(v) for v in dims])
+    shapes = agn_shapes(len(dims) - 1, d, int(batch), int(dtype))
+    ctx = ctypes.c_void_p()
+    _check(lib.agn_create(ctypes.byref(shapes), int(n), int(lam), float(eta),
+                          int(seed) & 0xFFFFFFFFFFFFFFFF, ctypes.byref(ctx)), None)
+    return ctx
+
+
+def agn_set_stream(ctx, stream_ptr=None):
+    _check(load_library().agn_set_stream(ctx, stream_ptr if stream_ptr is not None else _stream_ptr()), ctx)
+
+
+def agn_round(ctx, x, y, num_samples: int, commit_order, x_dtype: int = AGN_FP32):
+    order = np.ascontiguousarray(commit_order, dtype=np.int32)
+    data = agn_data(x.data_ptr(), y.data_ptr(), int(num_samples), int(x_dtype))
+    _check(load_library().agn_round(ctx, ctypes.byref(data),
+                                    order.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))), ctx)
+
+
+def agn_central(ctx, out):
+    _check(load_library().agn_central(ctx, ctypes.c_void_p(out.data_ptr())), ctx)
+
+
+def agn_loss(ctx, out):
+    _check(load_library().agn_loss(ctx, ctypes.c_void_p(out.data_ptr())), ctx)
+
+
+def agn_num_params(ctx) -> int:
+    return int(load_library().agn_num_params(ctx))
+
+
+def agn_last_error(ctx=None) -> str:
+    msg = load_library().agn_last_error(ctx)
+    return msg.decode() if msg else ""
+
+
+def agn_destroy(ctx):
+    load_library().agn_destroy(ctx)
+
+
+def agn_set_central(ctx, inp):
+    _check(load_library().agn_set_central(ctx, ctypes.c_void_p(inp.data_ptr())), ctx)
+
+
+def agn_worker_params(ctx, worker: int, out):
+    _check(load_library().agn_worker_params(ctx, int(worker), ctypes.c_void_p(out.data_ptr())), ctx)
+
+
+def agn_debug_batch_indices(ctx, worker: int, step_t: int, num_samples: int, out):
+    _check(load_library().agn_debug_batch_indices(ctx, int(worker), int(step_t), int(num_samples),
+                                                  ctypes.c_void_p(out.data_ptr())), ctx)
+
+
+def agn_set_kernel_timing(ctx, kernel_class: int, enable: bool):
+    _check(load_library().agn_set_kernel_timing(ctx, int(kernel_class), int(bool(enable))), ctx)
+
+
+def agn_kernel_timing(ctx, kernel_class: int):
+    ms = ctypes.c_double()
+    cnt = ctypes.c_int64()
+    _check(load_library().agn_kernel_timing(ctx, int(kernel_class), ctypes.byref(ms), ctypes.byref(cnt)), ctx)
+    return ms.value, cnt.value
+
+
+# --------------------------------------------------------------------------
+# convenience wrapper
+# --------------------------------------------------------------------------
+
+class AGN:
+    """One AGN context on the current ROCm device and stream."""
+
+    def __init__(self, dims, n, lam, eta, m, seed, dtype="fp32"):
+        self.dims = tuple(int(d) for d in dims)
+        self.n, self.lam, self.m = int(n), int(lam), int(m)
+        self.dtype = AGN_BF16 if dtype == "bf16" else AGN_FP32
+        self.ctx = agn_create(self.dims, m, n, lam, eta, seed, self.dtype)
+        agn_set_stream(self.ctx)
+        self.P = agn_num_params(self.ctx)
+
+    def close(self):
+        if self.ctx is not None:
+            agn_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def round(self, x, y, order):
+        agn_round(self.ctx, x, y, x.shape[0], order, self.dtype)
+
+    def central(self):
+        torch = _torch()
+        out = torch.empty(self.P, dtype=torch.float32, device="cuda")
+        agn_central(self.ctx, out)
+        return out
+
+    def loss(self):
+        torch = _torch()
+        out = torch.empty(self.n, dtype=torch.float32, device="cuda")
+        agn_loss(self.ctx, out)
+        return out
+
+    def worker_params(self, k):
+        torch = _torch()
+        out = torch.empty(self.P, dtype=torch.float32, device="cuda")
+        agn_worker_params(self.ctx, k, out)
+        return out
+
+    def set_central(self, vec):
+        agn_set_central(self.ctx, vec)
+
+    def batch_indices(self, worker, t, num_samples):
+        torch = _torch()
+        out = torch.empty(self.m, dtype=torch.int64, device="cuda")
+        agn_debug_batch_indices(self.ctx, worker, t, num_samples, out)
+        return out

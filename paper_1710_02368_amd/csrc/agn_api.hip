@@ -1,0 +1,498 @@
+// C ABI of libagn: context management, argument validation, the device
+// memory plan and the launch sequence of one AGN round.
+//
+// Device state of a context (float32 unless noted; P_pad = padded
+// parameter count, every tensor 256-byte aligned, weight rows padded to a
+// multiple of 8 elements):
+//   central   [P_pad]           the central variable (Eq. 2)
+//   snap      [n][P_pad]        each worker's last pulled copy (start of its round)
+//   buf[0,1]  [n][P_pad]        ping-pong parameters of the local steps; on the
+//                               last step the normalized delta (theta_lambda -
+//                               theta_0) / lambda is stored in place of theta
+//   *16       bf16 shadows of snap/buf (bf16 mode: the matrix-product operands)
+//   H[l]      [n][m][ld_l]      hidden activations after ReLU, l = 1..L-1
+//   Z         [n][m][ld_L]      logits
+//   dZ[l]     [n][m][ld_l]      gradients of the batch loss w.r.t. layer inputs, l = 1..L
+//   loss      [n][lambda][m]    per-row cross-entropy of the last round
+// Step i of a round reads its weights from src = (i == 0 ? snap : buf[(i-1)%2])
+// and writes dst = buf[i%2]; reading and writing different buffers lets the
+// input-gradient and weight-gradient products of one layer run in either
+// order.  Nothing is allocated after agn_create.
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "agn_internal.h"
+#include "../../include/agn.h"
+
+using namespace agn;
+
+struct TimingSlot {
+  int enabled = 0;
+  std::vector<hipEvent_t> ev;  // start/end pairs
+  size_t used = 0;             // pairs recorded
+  int64_t dropped = 0;
+};
+
+struct agn_ctx {
+  int L = 0, m = 0, dtype = 0, n = 0, lam = 0;
+  int dims[AGN_MAX_LAYERS + 1] = {};
+  float eta = 0.f;
+  int64_t P = 0, P_pad = 0;
+  int64_t woff[AGN_MAX_LAYERS] = {}, boff[AGN_MAX_LAYERS] = {}, ldw[AGN_MAX_LAYERS] = {};
+  int64_t lda[AGN_MAX_LAYERS + 1] = {};  // row stride of activations of width d_l
+  float* central = nullptr;
+  float* snap = nullptr;
+  float* buf[2] = {nullptr, nullptr};
+  uint16_t* snap16 = nullptr;
+  uint16_t* buf16[2] = {nullptr, nullptr};
+  void* H[AGN_MAX_LAYERS + 1] = {};
+  void* dZ[AGN_MAX_LAYERS + 1] = {};
+  float* Z = nullptr;
+  float* loss = nullptr;
+  int32_t* order = nullptr;
+  int64_t* round_dev = nullptr;
+  int64_t rounds = 0;
+  int64_t N_fixed = -1;
+  hipStream_t stream = nullptr;
+  int device = 0;
+  int poisoned = 0;
+  std::string err;
+  PackArgs pack{};
+  TimingSlot timing[AGN_K_NUM];
+  std::vector<void*> allocs;
+};
+
+static std::string g_create_err;
+
+namespace {
+
+inline int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
+
+int fail(agn_ctx* c, int code, const std::string& msg) {
+  if (c) {
+    c->err = msg;
+    if (code == AGN_EHIP) c->poisoned = 1;
+  } else {
+    g_create_err = msg;
+  }
+  return code;
+}
+
+#define HIP_CHECK(ctx, expr)                                                                \
+  do {                                                                                      \
+    hipError_t e_ = (expr);                                                                 \
+    if (e_ != hipSuccess)                                                                   \
+      return fail((ctx), AGN_EHIP, std::string(#expr) + ": " + hipGetErrorString(e_));      \
+  } while (0)
+
+void free_all(agn_ctx* c) {
+  for (void* p : c->allocs) (void)hipFree(p);
+  c->allocs.clear();
+  for (auto& t : c->timing)
+    for (hipEvent_t e : t.ev) (void)hipEventDestroy(e);
+}
+
+template <class T>
+hipError_t dalloc(agn_ctx* c, T** p, int64_t count) {
+  void* q = nullptr;
+  hipError_t e = hipMalloc(&q, (size_t)std::max<int64_t>(count, 1) * sizeof(T));
+  if (e != hipSuccess) return e;
+  c->allocs.push_back(q);
+  *p = reinterpret_cast<T*>(q);
+  return hipSuccess;
+}
+
+// Bracket a launch of class `cls` with events when timing is enabled.
+template <class F>
+hipError_t timed(agn_ctx* c, int cls, F&& launch) {
+  TimingSlot& t = c->timing[cls];
+  if (!t.enabled) return launch();
+  if (t.used >= (1u << 15)) {
+    ++t.dropped;
+    return launch();
+  }
+  if (2 * t.used + 2 > t.ev.size()) {
+    for (int i = 0; i < 2; ++i) {
+      hipEvent_t e;
+      hipError_t r = hipEventCreate(&e);
+      if (r != hipSuccess) return r;
+      t.ev.push_back(e);
+    }
+  }
+  hipError_t r = hipEventRecord(t.ev[2 * t.used], c->stream);
+  if (r != hipSuccess) return r;
+  r = launch();
+  if (r != hipSuccess) return r;
+  r = hipEventRecord(t.ev[2 * t.used + 1], c->stream);
+  ++t.used;
+  return r;
+}
+
+int check_ctx(agn_ctx* c) {
+  if (!c) return fail(nullptr, AGN_EINVAL, "null context");
+  if (c->poisoned) return fail(c, AGN_ESTATE, "context poisoned by an earlier HIP error: " + c->err);
+  return AGN_OK;
+}
+
+int set_device(agn_ctx* c) {
+  HIP_CHECK(c, hipSetDevice(c->device));
+  return AGN_OK;
+}
+
+// One local step of every worker: forward, softmax cross-entropy, backward
+// with the SGD update fused into the weight-gradient products.
+int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
+  const int L = c->L, m = c->m, n = c->n;
+  const bool bf = c->dtype == AGN_BF16;
+  const bool last = step == c->lam - 1;
+  const float* src = step == 0 ? c->snap : c->buf[(step - 1) & 1];
+  float* dst = c->buf[step & 1];
+  const uint16_t* src16 = bf ? (step == 0 ? c->snap16 : c->buf16[(step - 1) & 1]) : nullptr;
+  uint16_t* dst16 = bf ? c->buf16[step & 1] : nullptr;
+  const int64_t ps = c->P_pad;
+
+  Gather gath{c->round_dev, c->lam, step, m, S};
+  const int64_t d0 = c->dims[0];
+  const int x_vec = (d0 % (bf ? 8 : 4) == 0) && ((uintptr_t)d->x % 16 == 0);
+  Operand xop{d->x, d0, 0, 1, x_vec};
+  auto gemm = [&](int a_kc, int b_kc, const GemmArgs& g) {
+    return bf ? launch_gemm_bf16(a_kc, b_kc, g, c->stream) : launch_gemm_f32(a_kc, b_kc, g, c->stream);
+  };
+
+  // forward: hidden layers with bias + ReLU, then the logits
+  for (int l = 0; l < L; ++l) {
+    GemmArgs g{};
+    g.M = m;
+    g.N = c->dims[l + 1];
+    g.K = c->dims[l];
+    g.batch = n;
+    g.a = l == 0 ? xop : Operand{c->H[l], c->lda[l], (int64_t)m * c->lda[l], 0, 1};
+    g.b = bf ? Operand{src16 + c->woff[l], c->ldw[l], ps, 0, 1} : Operand{src + c->woff[l], c->ldw[l], ps, 0, 1};
+    g.g = gath;
+    g.epi = l < L - 1 ? EPI_FWD_RELU : EPI_FWD_LINEAR;
+    g.out = l < L - 1 ? c->H[l + 1] : (void*)c->Z;
+    g.ldo = c->lda[l + 1];
+    g.ostride = (int64_t)m * c->lda[l + 1];
+    g.bias = src + c->boff[l];
+    g.bstride = ps;
+    HIP_CHECK(c, timed(c, AGN_K_FWD, [&] { return gemm(1, 1, g); }));
+  }
+
+  // softmax cross-entropy: per-row loss and the output gradient dZ_L
+  {
+    SoftmaxArgs s{};
+    s.z = c->Z;
+    s.ldz = c->lda[L];
+    s.zstride = (int64_t)m * c->lda[L];
+    s.y = d->y;
+    s.g = gath;
+    s.n = n;
+    s.m = m;
+    s.C = c->dims[L];
+    s.dz = c->dZ[L];
+    s.ldd = c->lda[L];
+    s.dstride = (int64_t)m * c->lda[L];
+    s.dz_bf16 = bf;
+    s.loss = c->loss;
+    s.lam = c->lam;
+    s.step = step;
+    HIP_CHECK(c, timed(c, AGN_K_SOFTMAX, [&] { return launch_softmax_ce(s, c->stream); }));
+  }
+
+  // backward, last layer first
+  for (int l = L - 1; l >= 0; --l) {
+    const int64_t dz_ld = c->lda[l + 1], dz_st = (int64_t)m * c->lda[l + 1];
+    if (l >= 1) {  // dZ_l = (dZ_{l+1} W_l) * [H_l > 0]
+      GemmArgs g{};
+      g.M = m;
+      g.N = c->dims[l];
+      g.K = c->dims[l + 1];
+      g.batch = n;
+      g.a = Operand{c->dZ[l + 1], dz_ld, dz_st, 0, 1};
+      g.b = bf ? Operand{src16 + c->woff[l], c->ldw[l], ps, 0, 1} : Operand{src + c->woff[l], c->ldw[l], ps, 0, 1};
+      g.g = gath;
+      g.epi = EPI_DX_MASK;
+      g.out = c->dZ[l];
+      g.ldo = c->lda[l];
+      g.ostride = (int64_t)m * c->lda[l];
+      g.mask = c->H[l];
+      g.ldm = c->lda[l];
+      g.mstride = (int64_t)m * c->lda[l];
+      HIP_CHECK(c, timed(c, AGN_K_DX, [&] { return gemm(1, 0, g); }));
+    }
+    {  // dW_l = dZ_{l+1}^T H_l fused with the update of W_l and b_l
+      GemmArgs g{};
+      g.M = c->dims[l + 1];
+      g.N = c->dims[l];
+      g.K = m;
+      g.batch = n;
+      g.a = Operand{c->dZ[l + 1], dz_ld, dz_st, 0, 1};
+      g.b = l == 0 ? xop : Operand{c->H[l], c->lda[l], (int64_t)m * c->lda[l], 0, 1};
+      g.g = gath;
+      g.epi = EPI_DW_UPDATE;
+      g.w_src = src + c->woff[l];
+      g.w_dst = dst + c->woff[l];
+      g.w_snap = c->snap + c->woff[l];
+      g.b_src = src + c->boff[l];
+      g.b_dst = dst + c->boff[l];
+      g.b_snap = c->snap + c->boff[l];
+      g.w_dst16 = (bf && !last) ? dst16 + c->woff[l] : nullptr;
+      g.ldw = c->ldw[l];
+      g.pstride = ps;
+      g.eta = c->eta;
+      g.lam = (float)c->lam;
+      g.last = last;
+      HIP_CHECK(c, timed(c, AGN_K_DW, [&] { return gemm(0, 0, g); }));
+    }
+  }
+  (void)dst16;
+  return AGN_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int agn_create(const agn_shapes* shapes, int32_t n, int32_t lambda, float eta, uint64_t seed,
+               agn_ctx** out) {
+  if (out) *out = nullptr;
+  if (!out) return fail(nullptr, AGN_EINVAL, "out is NULL");
+  if (!shapes) return fail(nullptr, AGN_EINVAL, "shapes is NULL");
+  const int L = shapes->num_layers;
+  if (L < 1 || L > AGN_MAX_LAYERS) return fail(nullptr, AGN_EINVAL, "num_layers must be in [1, 16]");
+  if (!shapes->dims) return fail(nullptr, AGN_EINVAL, "dims is NULL");
+  for (int l = 0; l <= L; ++l)
+    if (shapes->dims[l] < 1 || shapes->dims[l] > (1 << 20))
+      return fail(nullptr, AGN_EINVAL, "every width must be in [1, 2^20]");
+  if (shapes->dims[L] < 2) return fail(nullptr, AGN_EINVAL, "need at least 2 classes");
+  if (shapes->batch < 1 || shapes->batch > (1 << 20))
+    return fail(nullptr, AGN_EINVAL, "batch must be in [1, 2^20]");
+  if (shapes->dtype != AGN_FP32 && shapes->dtype != AGN_BF16)
+    return fail(nullptr, AGN_EINVAL, "dtype must be AGN_FP32 or AGN_BF16");
+  if (n < 1 || n > AGN_MAX_WORKERS) return fail(nullptr, AGN_EINVAL, "n must be in [1, 256]");
+  if (lambda < 1) return fail(nullptr, AGN_EINVAL, "lambda must be >= 1");
+  if (!std::isfinite(eta)) return fail(nullptr, AGN_EINVAL, "eta must be finite");
+
+  agn_ctx* c = new (std::nothrow) agn_ctx();
+  if (!c) return fail(nullptr, AGN_ENOMEM, "host allocation failed");
+  c->L = L;
+  c->m = shapes->batch;
+  c->dtype = shapes->dtype;
+  c->n = n;
+  c->lam = lambda;
+  c->eta = eta;
+  for (int l = 0; l <= L; ++l) c->dims[l] = shapes->dims[l];
+
+  // parameter layout: W_l rows padded to 8 elements, tensors 64-element aligned
+  int64_t off = 0, P = 0;
+  c->pack.ntensors = 2 * L;
+  for (int l = 0; l < L; ++l) {
+    const int64_t din = c->dims[l], dout = c->dims[l + 1];
+    c->ldw[l] = round_up(din, 8);
+    c->woff[l] = off;
+    c->pack.t[2 * l] = TensorDesc{P, off, c->ldw[l], (int32_t)dout, (int32_t)din};
+    off = round_up(off + dout * c->ldw[l], 64);
+    P += din * dout;
+    c->boff[l] = off;
+    c->pack.t[2 * l + 1] = TensorDesc{P, off, dout, 1, (int32_t)dout};
+    off = round_up(off + dout, 64);
+    P += dout;
+  }
+  c->P = P;
+  c->P_pad = off;
+  c->pack.P = P;
+  for (int l = 0; l <= L; ++l) c->lda[l] = round_up(c->dims[l], 8);
+
+  auto bail = [&](int code, const std::string& msg) {
+    free_all(c);
+    delete c;
+    return fail(nullptr, code, msg);
+  };
+  if (hipGetDevice(&c->device) != hipSuccess) return bail(AGN_EHIP, "no HIP device");
+
+  const bool bf = c->dtype == AGN_BF16;
+  const int64_t nps = (int64_t)n * c->P_pad;
+  const size_t act = bf ? 2 : 4;
+  bool ok = dalloc(c, &c->central, c->P_pad) == hipSuccess && dalloc(c, &c->snap, nps) == hipSuccess &&
+            dalloc(c, &c->buf[0], nps) == hipSuccess && dalloc(c, &c->buf[1], nps) == hipSuccess &&
+            dalloc(c, &c->Z, (int64_t)n * c->m * c->lda[L]) == hipSuccess &&
+            dalloc(c, &c->loss, (int64_t)n * lambda * c->m) == hipSuccess &&
+            dalloc(c, &c->order, n) == hipSuccess && dalloc(c, &c->round_dev, 1) == hipSuccess;
+  if (ok && bf)
+    ok = dalloc(c, &c->snap16, nps) == hipSuccess && dalloc(c, &c->buf16[0], nps) == hipSuccess &&
+         dalloc(c, &c->buf16[1], nps) == hipSuccess;
+  for (int l = 1; ok && l <= L; ++l) {
+    char* p = nullptr;
+    const int64_t bytes = (int64_t)n * c->m * c->lda[l] * act;
+    if (l < L) ok = dalloc(c, &p, bytes) == hipSuccess, c->H[l] = p;
+    if (ok) ok = dalloc(c, &p, bytes) == hipSuccess, c->dZ[l] = p;
+  }
+  if (!ok) return bail(AGN_ENOMEM, "device allocation failed");
+
+  // zero everything (padding stays zero forever), then the initial parameters
+  hipError_t e = hipSuccess;
+  e = hipMemset(c->central, 0, c->P_pad * 4);
+  if (e == hipSuccess) e = hipMemset(c->snap, 0, nps * 4);
+  if (e == hipSuccess) e = hipMemset(c->buf[0], 0, nps * 4);
+  if (e == hipSuccess) e = hipMemset(c->buf[1], 0, nps * 4);
+  if (e == hipSuccess && bf) e = hipMemset(c->snap16, 0, nps * 2);
+  if (e == hipSuccess && bf) e = hipMemset(c->buf16[0], 0, nps * 2);
+  if (e == hipSuccess && bf) e = hipMemset(c->buf16[1], 0, nps * 2);
+  if (e == hipSuccess) e = hipMemset(c->round_dev, 0, 8);
+  if (e == hipSuccess) e = hipMemset(c->loss, 0, (size_t)n * lambda * c->m * 4);
+  if (e != hipSuccess) return bail(AGN_EHIP, std::string("hipMemset: ") + hipGetErrorString(e));
+
+  std::vector<float> init(P);
+  he_normal_init(c->dims, L, seed, init.data());
+  float* tmp = nullptr;
+  e = hipMalloc(&tmp, P * sizeof(float));
+  if (e != hipSuccess) return bail(AGN_ENOMEM, "device allocation failed");
+  e = hipMemcpy(tmp, init.data(), P * sizeof(float), hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = launch_unpack(c->pack, tmp, c->central, nullptr, 1, 0, nullptr);
+  if (e == hipSuccess) e = launch_unpack(c->pack, tmp, c->snap, c->snap16, n, c->P_pad, nullptr);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  (void)hipFree(tmp);
+  if (e != hipSuccess) return bail(AGN_EHIP, std::string("init: ") + hipGetErrorString(e));
+  *out = c;
+  return AGN_OK;
+}
+
+int agn_set_stream(agn_ctx* c, void* s) {
+  if (int r = check_ctx(c)) return r;
+  c->stream = reinterpret_cast<hipStream_t>(s);
+  return AGN_OK;
+}
+
+int agn_round(agn_ctx* c, const agn_data* d, const int32_t* order) {
+  if (int r = check_ctx(c)) return r;
+  if (!d || !d->x || !d->y) return fail(c, AGN_EINVAL, "data, data->x and data->y must be non-NULL");
+  if (d->x_dtype != (c->dtype == AGN_BF16 ? 1 : 0))
+    return fail(c, AGN_EINVAL, "x_dtype must be 1 for AGN_BF16 contexts and 0 otherwise");
+  if (d->num_samples < c->n) return fail(c, AGN_EINVAL, "num_samples must be >= n");
+  if (c->N_fixed >= 0 && d->num_samples != c->N_fixed)
+    return fail(c, AGN_EINVAL, "num_samples changed between rounds");
+  if (!order) return fail(c, AGN_EINVAL, "commit_order is NULL");
+  {
+    std::vector<char> seen(c->n, 0);
+    for (int j = 0; j < c->n; ++j) {
+      const int k = order[j];
+      if (k < 0 || k >= c->n || seen[k]) return fail(c, AGN_EINVAL, "commit_order is not a permutation of 0..n-1");
+      seen[k] = 1;
+    }
+  }
+  if (int r = set_device(c)) return r;
+  const int64_t S = d->num_samples / c->n;
+  HIP_CHECK(c, launch_set_order(order, c->n, c->order, c->stream));
+  for (int i = 0; i < c->lam; ++i)
+    if (int r = enqueue_step(c, d, S, i)) return r;
+  CommitArgs ca{};
+  ca.central = c->central;
+  ca.snap = c->snap;
+  ca.delta = c->buf[(c->lam - 1) & 1];
+  ca.snap16 = c->snap16;
+  ca.order = c->order;
+  ca.round = c->round_dev;
+  ca.pstride = c->P_pad;
+  ca.count = c->P_pad;
+  ca.n = c->n;
+  HIP_CHECK(c, timed(c, AGN_K_COMMIT, [&] { return launch_commit(ca, c->stream); }));
+  c->N_fixed = d->num_samples;
+  ++c->rounds;
+  return AGN_OK;
+}
+
+int agn_central(agn_ctx* c, float* out) {
+  if (int r = check_ctx(c)) return r;
+  if (!out) return fail(c, AGN_EINVAL, "out is NULL");
+  if (int r = set_device(c)) return r;
+  HIP_CHECK(c, launch_pack(c->pack, c->central, out, c->stream));
+  HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  return AGN_OK;
+}
+
+int agn_loss(agn_ctx* c, float* out) {
+  if (int r = check_ctx(c)) return r;
+  if (!out) return fail(c, AGN_EINVAL, "out is NULL");
+  if (c->rounds == 0) return fail(c, AGN_ESTATE, "no round has run yet");
+  if (int r = set_device(c)) return r;
+  HIP_CHECK(c, launch_loss_reduce(c->loss, c->n, (int64_t)c->lam * c->m, out, c->stream));
+  HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  return AGN_OK;
+}
+
+int64_t agn_num_params(const agn_ctx* c) { return c ? c->P : -1; }
+
+const char* agn_last_error(const agn_ctx* c) { return c ? c->err.c_str() : g_create_err.c_str(); }
+
+void agn_destroy(agn_ctx* c) {
+  if (!c) return;
+  (void)hipSetDevice(c->device);
+  (void)hipStreamSynchronize(c->stream);
+  free_all(c);
+  delete c;
+}
+
+int agn_set_central(agn_ctx* c, const float* in) {
+  if (int r = check_ctx(c)) return r;
+  if (!in) return fail(c, AGN_EINVAL, "in is NULL");
+  if (c->rounds != 0) return fail(c, AGN_ESTATE, "agn_set_central is allowed only before the first round");
+  if (int r = set_device(c)) return r;
+  HIP_CHECK(c, launch_unpack(c->pack, in, c->central, nullptr, 1, 0, c->stream));
+  HIP_CHECK(c, launch_unpack(c->pack, in, c->snap, c->snap16, c->n, c->P_pad, c->stream));
+  HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  return AGN_OK;
+}
+
+int agn_worker_params(agn_ctx* c, int32_t worker, float* out) {
+  if (int r = check_ctx(c)) return r;
+  if (!out) return fail(c, AGN_EINVAL, "out is NULL");
+  if (worker < 0 || worker >= c->n) return fail(c, AGN_EINVAL, "worker out of range");
+  if (int r = set_device(c)) return r;
+  HIP_CHECK(c, launch_pack(c->pack, c->snap + (int64_t)worker * c->P_pad, out, c->stream));
+  HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  return AGN_OK;
+}
+
+int agn_debug_batch_indices(agn_ctx* c, int32_t worker, int64_t step_t, int64_t num_samples, int64_t* out) {
+  if (int r = check_ctx(c)) return r;
+  if (!out) return fail(c, AGN_EINVAL, "out is NULL");
+  if (worker < 0 || worker >= c->n) return fail(c, AGN_EINVAL, "worker out of range");
+  if (step_t < 0) return fail(c, AGN_EINVAL, "step_t must be >= 0");
+  if (num_samples < c->n) return fail(c, AGN_EINVAL, "num_samples must be >= n");
+  if (int r = set_device(c)) return r;
+  HIP_CHECK(c, launch_batch_indices(worker, step_t, c->m, num_samples / c->n, out, c->stream));
+  HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  return AGN_OK;
+}
+
+int agn_set_kernel_timing(agn_ctx* c, int32_t cls, int32_t enable) {
+  if (int r = check_ctx(c)) return r;
+  if (cls < 0 || cls >= AGN_K_NUM) return fail(c, AGN_EINVAL, "kernel class out of range");
+  c->timing[cls].enabled = enable != 0;
+  c->timing[cls].used = 0;
+  c->timing[cls].dropped = 0;
+  return AGN_OK;
+}
+
+int agn_kernel_timing(agn_ctx* c, int32_t cls, double* total_ms, int64_t* launches) {
+  if (int r = check_ctx(c)) return r;
+  if (cls < 0 || cls >= AGN_K_NUM) return fail(c, AGN_EINVAL, "kernel class out of range");
+  if (!total_ms || !launches) return fail(c, AGN_EINVAL, "null output pointer");
+  if (int r = set_device(c)) return r;
+  HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  const TimingSlot& t = c->timing[cls];
+  double tot = 0.0;
+  for (size_t i = 0; i < t.used; ++i) {
+    float ms = 0.f;
+    HIP_CHECK(c, hipEventElapsedTime(&ms, t.ev[2 * i], t.ev[2 * i + 1]));
+    tot += ms;
+  }
+  *total_ms = tot;
+  *launches = (int64_t)t.used;
+  return AGN_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,116 @@
+// Internal declarations shared by the host code and the kernels of libagn.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace agn {
+
+// An operand of a batched product, as the matrix is stored in memory.
+struct Operand {
+  const void* ptr;  // element (0,0) of worker 0's matrix
+  int64_t ld;       // elements between consecutive stored rows
+  int64_t wstride;  // elements between consecutive workers' matrices (0: shared)
+  int32_t gather;   // 1: stored rows are data-set rows picked by the batch index
+  int32_t vec;      // 1: ld % 4 == 0 and ptr 16-byte aligned (vector loads allowed)
+};
+
+// Batch index of a gathered operand: worker k, local step t = round*lam + step,
+// row j -> k*S + ((t*m + j) mod S)  (FetchNextMiniBatch, Algorithm 1).
+struct Gather {
+  const int64_t* round;  // device round counter
+  int32_t lam;
+  int32_t step;
+  int32_t mb;
+  int64_t S;
+};
+
+enum Epilogue : int32_t {
+  EPI_FWD_RELU = 0,    // out = relu(acc + bias)
+  EPI_FWD_LINEAR = 1,  // out = acc + bias (logits)
+  EPI_DX_MASK = 2,     // out = acc * (mask > 0)
+  EPI_DW_UPDATE = 3,   // W_dst = W_src - eta*acc, b_dst = b_src - eta*colsum(dZ)
+                       // (last step: store (new - snapshot) / lambda instead)
+};
+
+struct GemmArgs {
+  int32_t M, N, K, batch;
+  Operand a;  // A[M][K]: stored [M][K] when a_kc, else [K][M]
+  Operand b;  // B[K][N]: stored [N][K] when b_kc, else [K][N]
+  Gather g;
+  int32_t epi;
+  // forward / input-gradient output
+  void* out;
+  int64_t ldo, ostride;
+  const void* mask;
+  int64_t ldm, mstride;
+  const float* bias;
+  int64_t bstride;
+  // weight-gradient update (one layer of every worker; stride pstride)
+  const float* w_src;
+  float* w_dst;
+  const float* w_snap;
+  const float* b_src;
+  float* b_dst;
+  const float* b_snap;
+  uint16_t* w_dst16;  // bf16 shadow of the updated weights (bf16 mode, not last step)
+  int64_t ldw, pstride;
+  float eta, lam;
+  int32_t last;
+};
+
+// launchers (return hipError_t of the launch)
+hipError_t launch_gemm_f32(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s);
+hipError_t launch_gemm_bf16(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s);
+
+struct SoftmaxArgs {
+  const float* z;      // logits [n][m][ldz]
+  int64_t ldz, zstride;
+  const int32_t* y;    // labels of the data set
+  Gather g;
+  int32_t n, m, C;
+  void* dz;            // output gradient [n][m][ldd] (float or bf16)
+  int64_t ldd, dstride;
+  int32_t dz_bf16;
+  float* loss;         // [n][lam][m] per-row losses
+  int32_t lam, step;
+};
+hipError_t launch_softmax_ce(const SoftmaxArgs& a, hipStream_t s);
+
+struct CommitArgs {
+  float* central;          // [P_pad]
+  float* snap;             // [n][P_pad] pulled copies (written)
+  const float* delta;      // [n][P_pad] normalized deltas of the round
+  uint16_t* snap16;        // bf16 shadow of the pulled copies (or null)
+  const int32_t* order;    // device, n entries
+  int64_t* round;          // device round counter (incremented)
+  int64_t pstride;         // P_pad
+  int64_t count;           // elements to process (P_pad)
+  int32_t n;
+};
+hipError_t launch_commit(const CommitArgs& a, hipStream_t s);
+
+struct TensorDesc {  // one parameter tensor: rows x cols, padded row stride ld
+  int64_t packed_off, padded_off, ld;
+  int32_t rows, cols;
+};
+struct PackArgs {
+  TensorDesc t[2 * 16];
+  int32_t ntensors;
+  int64_t P;
+};
+hipError_t launch_pack(const PackArgs& pa, const float* padded, float* packed, hipStream_t s);
+hipError_t launch_unpack(const PackArgs& pa, const float* packed, float* padded,
+                         uint16_t* padded16, int32_t copies, int64_t pstride, hipStream_t s);
+hipError_t launch_loss_reduce(const float* loss, int32_t n, int64_t per_worker, float* out,
+                              hipStream_t s);
+hipError_t launch_set_order(const int32_t* host_order, int32_t n, int32_t* dev_order,
+                            hipStream_t s);
+hipError_t launch_batch_indices(int32_t worker, int64_t t, int32_t mb, int64_t S, int64_t* out,
+                                hipStream_t s);
+hipError_t launch_copy_bf16(const float* src, uint16_t* dst, int64_t count, hipStream_t s);
+
+// host-side He-normal initial parameters (packed layout)
+void he_normal_init(const int32_t* dims, int32_t L, uint64_t seed, float* packed);
+
+}  // namespace agn

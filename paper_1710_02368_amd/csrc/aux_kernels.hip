@@ -1,0 +1,226 @@
+// Bandwidth kernels of the AGN round: softmax cross-entropy with its
+// gradient, the fused normalize/commit/pull over the parameters, and small
+// helpers (per-worker loss reduction, parameter packing, commit order,
+// batch indices).
+#include <math.h>
+
+#include "device_common.h"
+
+namespace agn {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// Softmax cross-entropy of one mini-batch row per wave (the loss of Eq. 1).
+// loss_j = logsumexp(z_j) - z_{j,y_j};  dZ_j = (softmax(z_j) - onehot(y_j)) / m,
+// the gradient of the batch-mean loss with respect to the logits.
+__global__ __launch_bounds__(256) void softmax_ce_kernel(SoftmaxArgs a) {
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t rg = (int64_t)blockIdx.x * 4 + wave;
+  if (rg >= (int64_t)a.n * a.m) return;
+  const int k = (int)(rg / a.m), j = (int)(rg % a.m);
+  const float* z = a.z + (int64_t)k * a.zstride + (int64_t)j * a.ldz;
+  const int64_t t = gather_step(a.g);
+  const int label = a.y[batch_row(k, t, a.g.mb, a.g.S, j)];
+
+  float mx = -INFINITY;
+  for (int c = lane; c < a.C; c += 64) mx = fmaxf(mx, z[c]);
+  mx = wave_max(mx);
+  float s = 0.f;
+  for (int c = lane; c < a.C; c += 64) s += expf(z[c] - mx);
+  s = wave_sum(s);
+  const float inv_s = 1.f / s;
+  const float inv_m = 1.f / (float)a.m;
+  for (int c = lane; c < a.C; c += 64) {
+    const float p = expf(z[c] - mx) * inv_s;
+    const float d = (p - (c == label ? 1.f : 0.f)) * inv_m;
+    const int64_t e = (int64_t)k * a.dstride + (int64_t)j * a.ldd + c;
+    if (a.dz_bf16)
+      reinterpret_cast<uint16_t*>(a.dz)[e] = f32_to_bf16_rne(d);
+    else
+      reinterpret_cast<float*>(a.dz)[e] = d;
+  }
+  if (lane == 0) {
+    const float lse = mx + logf(s);
+    a.loss[((int64_t)k * a.lam + a.step) * a.m + j] = lse - z[label];
+  }
+}
+
+// Normalize + commit + pull (Eq. 2; Algorithm 1, Commit and Pull).
+// Each thread owns 4 consecutive parameters.  The deltas already carry the
+// 1/lambda normalization (stored by the last local step).  In commit order
+// j = 0..n-1, worker k = order[j]:  c <- c + delta_k;  pulled_k <- c.
+// Finally central <- c.  Elements are independent, so the sequential order
+// per element is exact and needs no atomics.
+__device__ __forceinline__ void store_bf16x4(uint16_t* base, int64_t i4, f32x4 c) {
+  uint2 h;
+  h.x = (uint32_t)f32_to_bf16_rne(c.x) | ((uint32_t)f32_to_bf16_rne(c.y) << 16);
+  h.y = (uint32_t)f32_to_bf16_rne(c.z) | ((uint32_t)f32_to_bf16_rne(c.w) << 16);
+  reinterpret_cast<uint2*>(base)[i4] = h;
+}
+
+__global__ __launch_bounds__(256) void commit_kernel(CommitArgs a) {
+  const int64_t e4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t n4 = a.count / 4, ps4 = a.pstride / 4;
+  if (e4 < n4) {
+    f32x4* central = reinterpret_cast<f32x4*>(a.central);
+    f32x4* snap = reinterpret_cast<f32x4*>(a.snap);
+    const f32x4* delta = reinterpret_cast<const f32x4*>(a.delta);
+    f32x4 c = central[e4];
+    int j = 0;
+    for (; j + 8 <= a.n; j += 8) {
+      int kk[8];
+      f32x4 d[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        kk[u] = a.order[j + u];
+        d[u] = __builtin_nontemporal_load(&delta[(int64_t)kk[u] * ps4 + e4]);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        c += d[u];
+        snap[(int64_t)kk[u] * ps4 + e4] = c;
+        if (a.snap16) store_bf16x4(a.snap16, (int64_t)kk[u] * ps4 + e4, c);
+      }
+    }
+    for (; j < a.n; ++j) {
+      const int k = a.order[j];
+      c += __builtin_nontemporal_load(&delta[(int64_t)k * ps4 + e4]);
+      snap[(int64_t)k * ps4 + e4] = c;
+      if (a.snap16) store_bf16x4(a.snap16, (int64_t)k * ps4 + e4, c);
+    }
+    central[e4] = c;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) *a.round += 1;
+}
+
+// packed (W_0, b_0, W_1, ...) <-> padded internal layout
+__device__ __forceinline__ int find_tensor(const PackArgs& pa, int64_t e) {
+  int t = 0;
+  while (t + 1 < pa.ntensors && e >= pa.t[t + 1].packed_off) ++t;
+  return t;
+}
+
+__global__ void pack_kernel(PackArgs pa, const float* padded, float* packed) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= pa.P) return;
+  const TensorDesc& d = pa.t[find_tensor(pa, e)];
+  const int64_t i = e - d.packed_off;
+  const int64_t r = i / d.cols, c = i % d.cols;
+  packed[e] = padded[d.padded_off + r * d.ld + c];
+}
+
+__global__ void unpack_kernel(PackArgs pa, const float* packed, float* padded, uint16_t* padded16,
+                              int32_t copies, int64_t pstride) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= pa.P) return;
+  const TensorDesc& d = pa.t[find_tensor(pa, e)];
+  const int64_t i = e - d.packed_off;
+  const int64_t r = i / d.cols, c = i % d.cols;
+  const int64_t o = d.padded_off + r * d.ld + c;
+  const float v = packed[e];
+  for (int k = 0; k < copies; ++k) {
+    padded[(int64_t)k * pstride + o] = v;
+    if (padded16) padded16[(int64_t)k * pstride + o] = f32_to_bf16_rne(v);
+  }
+}
+
+// per-worker mean of the per-row losses, accumulated in float64 in a fixed order
+__global__ __launch_bounds__(256) void loss_reduce_kernel(const float* loss, int64_t per_worker,
+                                                          float* out) {
+  __shared__ double part[256];
+  const int k = blockIdx.x;
+  double s = 0.0;
+  for (int64_t i = threadIdx.x; i < per_worker; i += 256) s += (double)loss[(int64_t)k * per_worker + i];
+  part[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) part[threadIdx.x] += part[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) out[k] = (float)(part[0] / (double)per_worker);
+}
+
+struct OrderArg {
+  int32_t v[256];
+};
+__global__ void set_order_kernel(OrderArg o, int32_t n, int32_t* dst) {
+  const int j = threadIdx.x;
+  if (j < n) dst[j] = o.v[j];
+}
+
+__global__ void batch_indices_kernel(int32_t worker, int64_t t, int32_t mb, int64_t S, int64_t* out) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j < mb) out[j] = batch_row(worker, t, mb, S, j);
+}
+
+__global__ void copy_bf16_kernel(const float* src, uint16_t* dst, int64_t count) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e < count) dst[e] = f32_to_bf16_rne(src[e]);
+}
+
+inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
+
+}  // namespace
+
+hipError_t launch_softmax_ce(const SoftmaxArgs& a, hipStream_t s) {
+  const int64_t rows = (int64_t)a.n * a.m;
+  hipLaunchKernelGGL(softmax_ce_kernel, dim3(blocks_for(rows, 4)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_commit(const CommitArgs& a, hipStream_t s) {
+  const int64_t n4 = a.count / 4;
+  hipLaunchKernelGGL(commit_kernel, dim3(blocks_for(n4 > 0 ? n4 : 1, 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_pack(const PackArgs& pa, const float* padded, float* packed, hipStream_t s) {
+  hipLaunchKernelGGL(pack_kernel, dim3(blocks_for(pa.P, 256)), dim3(256), 0, s, pa, padded, packed);
+  return hipGetLastError();
+}
+
+hipError_t launch_unpack(const PackArgs& pa, const float* packed, float* padded, uint16_t* padded16,
+                         int32_t copies, int64_t pstride, hipStream_t s) {
+  hipLaunchKernelGGL(unpack_kernel, dim3(blocks_for(pa.P, 256)), dim3(256), 0, s, pa, packed, padded,
+                     padded16, copies, pstride);
+  return hipGetLastError();
+}
+
+hipError_t launch_loss_reduce(const float* loss, int32_t n, int64_t per_worker, float* out,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(loss_reduce_kernel, dim3(n), dim3(256), 0, s, loss, per_worker, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_set_order(const int32_t* host_order, int32_t n, int32_t* dev_order, hipStream_t s) {
+  OrderArg o;
+  for (int j = 0; j < 256; ++j) o.v[j] = j < n ? host_order[j] : 0;
+  hipLaunchKernelGGL(set_order_kernel, dim3(1), dim3(256), 0, s, o, n, dev_order);
+  return hipGetLastError();
+}
+
+hipError_t launch_batch_indices(int32_t worker, int64_t t, int32_t mb, int64_t S, int64_t* out,
+                                hipStream_t s) {
+  hipLaunchKernelGGL(batch_indices_kernel, dim3(blocks_for(mb, 256)), dim3(256), 0, s, worker, t, mb,
+                     S, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_bf16(const float* src, uint16_t* dst, int64_t count, hipStream_t s) {
+  hipLaunchKernelGGL(copy_bf16_kernel, dim3(blocks_for(count, 256)), dim3(256), 0, s, src, dst, count);
+  return hipGetLastError();
+}
+
+}  // namespace agn

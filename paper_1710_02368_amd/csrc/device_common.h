@@ -1,0 +1,40 @@
+// Device helpers shared by the kernels of libagn.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "agn_internal.h"
+
+namespace agn {
+
+constexpr int kNumXcd = 8;  // MI355X: 8 XCDs, workgroups dispatched round-robin
+
+// Workgroups are handed to the XCDs round-robin (workgroup i to XCD i % 8).
+// Map the hardware id to a logical tile id so that each XCD receives one
+// contiguous range of logical tiles: tiles that share operands (one worker's
+// weights, one row block) then share that XCD's L2.  A bijection on [0, nblk).
+__device__ __forceinline__ int xcd_remap(int pid, int nblk) {
+  const int xcd = pid % kNumXcd, local = pid / kNumXcd;
+  const int q = nblk / kNumXcd, rem = nblk % kNumXcd;
+  return xcd < rem ? xcd * (q + 1) + local : rem * (q + 1) + (xcd - rem) * q + local;
+}
+
+// Data-set row of row j of worker k's mini-batch at local step t.
+__device__ __forceinline__ int64_t batch_row(int64_t k, int64_t t, int64_t mb, int64_t S, int64_t j) {
+  return k * S + (t * mb + j) % S;
+}
+
+__device__ __forceinline__ int64_t gather_step(const Gather& g) {
+  return (*g.round) * (int64_t)g.lam + g.step;
+}
+
+// float32 -> bfloat16 bits, round to nearest even (finite inputs).
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+}  // namespace agn

@@ -1,0 +1,270 @@
+// Batched float32 products of the local SGD step on the fp32 matrix cores
+// of gfx950 (v_mfma_f32_32x32x2_f32), one launch per layer for all workers.
+//
+// A workgroup of 4 waves owns a 64x64 output tile of one worker; each wave
+// owns a 32x32 quarter held in 16 accumulator registers per lane.  K is
+// consumed in steps of 32 through double-buffered LDS tiles, with the next
+// step's global loads in flight while the current step's 16 MFMAs run.
+//
+// Operands are read as stored, with no transposition pass:
+//   forward          H_{l+1} = relu(H_l W_l^T + b_l)   A = H_l [m][d_l]      (K-contiguous)
+//                                                      B = W_l [d_{l+1}][d_l] (K-contiguous)
+//   input gradient   dZ_l = (dZ_{l+1} W_l) * [H_l > 0]  A = dZ  (K-contiguous)
+//                                                      B = W_l (N-contiguous)
+//   weight gradient  dW_l = dZ_{l+1}^T H_l             A = dZ  (M-contiguous)
+//                                                      B = H_l (N-contiguous)
+// For the first layer the rows of H_0 are gathered straight from the data
+// set by the mini-batch index (no copy of the batch is made).  The weight-
+// gradient product carries the SGD update of Algorithm 1 in its epilogue,
+// so gradients are never written to memory: W <- W - eta*dW (and the bias
+// from the column sums of dZ, which the row-block's first tile forms from
+// the same LDS tiles).  On a round's last step the epilogue stores the
+// normalized displacement (W_new - W_pulled) / lambda, which equals the
+// accumulated update a / lambda of Algorithm 1.
+#include "device_common.h"
+
+namespace agn {
+namespace {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int BM = 64, BN = 64, BK = 32, NT = 256;
+constexpr int KC_LD = BK + 4;            // LDS row stride of a K-contiguous tile
+constexpr int KS_LD = 64 + 4;            // LDS row stride of a K-strided tile
+constexpr int KC_TILE = 64 * KC_LD;
+constexpr int KS_TILE = BK * KS_LD;
+
+__device__ __forceinline__ float4 load4(const float* p, int valid, int vec) {
+  if (valid >= 4 && vec) return *reinterpret_cast<const float4*>(p);
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (valid > 0) v.x = p[0];
+  if (valid > 1) v.y = p[1];
+  if (valid > 2) v.z = p[2];
+  if (valid > 3) v.w = p[3];
+  return v;
+}
+
+// Global->register staging of one operand tile.
+// K-contiguous tile: 64 outer rows x 32 k; thread loads rows tid/8 and
+// tid/8+32 at k offset 4*(tid%8).  K-strided tile: 32 k rows x 64 outer;
+// thread loads k rows tid/16 and tid/16+16 at outer offset 4*(tid%16).
+template <bool KC>
+struct TileLoader {
+  const float* rowp[2];  // KC: fixed row pointers (null past the edge)
+  const float* base;     // KS: worker base
+  int64_t ld;
+  int outer0, outer_n, K;
+  int vec, gather;
+  int64_t worker, t, mb, S;
+
+  __device__ void init(const Operand& op, const Gather& g, int64_t w, int o0, int on, int k, int tid) {
+    base = reinterpret_cast<const float*>(op.ptr) + w * op.wstride;
+    ld = op.ld;
+    outer0 = o0;
+    outer_n = on;
+    K = k;
+    vec = op.vec;
+    gather = op.gather;
+    worker = w;
+    mb = g.mb;
+    S = g.S;
+    t = gather ? gather_step(g) : 0;
+    if (KC) {
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        const int o = o0 + tid / 8 + 32 * p;
+        int64_t r = o;
+        if (gather && o < on) r = batch_row(worker, t, mb, S, o);
+        rowp[p] = o < on ? base + r * ld : nullptr;
+      }
+    }
+  }
+
+  __device__ void load(int k0, int tid, float4 (&v)[2]) const {
+    if (KC) {
+      const int kk = k0 + 4 * (tid % 8);
+#pragma unroll
+      for (int p = 0; p < 2; ++p)
+        v[p] = rowp[p] ? load4(rowp[p] + kk, K - kk, vec) : make_float4(0.f, 0.f, 0.f, 0.f);
+    } else {
+      const int cc = outer0 + 4 * (tid % 16);
+#pragma unroll
+      for (int p = 0; p < 2; ++p) {
+        const int kr = k0 + tid / 16 + 16 * p;
+        if (kr < K) {
+          int64_t r = gather ? batch_row(worker, t, mb, S, kr) : kr;
+          v[p] = load4(base + r * ld + cc, outer_n - cc, vec);
+        } else {
+          v[p] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+      }
+    }
+  }
+
+  __device__ static void store(float* lds, int tid, const float4 (&v)[2]) {
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      if (KC) {
+        *reinterpret_cast<float4*>(lds + (tid / 8 + 32 * p) * KC_LD + 4 * (tid % 8)) = v[p];
+      } else {
+        *reinterpret_cast<float4*>(lds + (tid / 16 + 16 * p) * KS_LD + 4 * (tid % 16)) = v[p];
+      }
+    }
+  }
+};
+
+// Fragment of one wave for 16 MFMAs: lane (i = lane%32, h = lane/32)
+// supplies element k = 16h + s of its row/column i for MFMA number s, so
+// that MFMA s contracts over k in {s, 16+s}.
+template <bool KC>
+__device__ __forceinline__ void read_frag(const float* lds, int outer_off, int li, int lh, float (&f)[16]) {
+  if (KC) {
+    const float* p = lds + (outer_off + li) * KC_LD + lh * 16;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      float4 v = *reinterpret_cast<const float4*>(p + 4 * q);
+      f[4 * q] = v.x;
+      f[4 * q + 1] = v.y;
+      f[4 * q + 2] = v.z;
+      f[4 * q + 3] = v.w;
+    }
+  } else {
+#pragma unroll
+    for (int s = 0; s < 16; ++s) f[s] = lds[(lh * 16 + s) * KS_LD + outer_off + li];
+  }
+}
+
+template <bool A_KC, bool B_KC, int EPI>
+__global__ __launch_bounds__(NT) void gemm_f32_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) float lds_a[2][A_KC ? KC_TILE : KS_TILE];
+  __shared__ __attribute__((aligned(16))) float lds_b[2][B_KC ? KC_TILE : KS_TILE];
+
+  const int tid = threadIdx.x;
+  const int tm = (g.M + BM - 1) / BM, tn = (g.N + BN - 1) / BN;
+  const int nblk = tm * tn * g.batch;
+  const int logical = xcd_remap(blockIdx.x, nblk);
+  const int worker = logical / (tm * tn);
+  const int rem = logical % (tm * tn);
+  const int tile_n = rem / tm, tile_m = rem % tm;
+  const int m0 = tile_m * BM, n0 = tile_n * BN;
+
+  TileLoader<A_KC> la;
+  TileLoader<B_KC> lb;
+  la.init(g.a, g.g, worker, m0, g.M, g.K, tid);
+  lb.init(g.b, g.g, worker, n0, g.N, g.K, tid);
+
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int li = lane & 31, lh = lane >> 5;
+
+  // bias gradient (weight-gradient epilogue): the first column tile of each
+  // row block sums its dZ tile columns (A is dZ^T, stored K-strided)
+  const bool do_bias = (EPI == EPI_DW_UPDATE) && tile_n == 0 && tid < 64;
+  float bsum = 0.f;
+
+  f32x16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+
+  const int nk = (g.K + BK - 1) / BK;
+  float4 va[2], vb[2];
+  la.load(0, tid, va);
+  lb.load(0, tid, vb);
+  TileLoader<A_KC>::store(lds_a[0], tid, va);
+  TileLoader<B_KC>::store(lds_b[0], tid, vb);
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < nk) {
+      la.load((kt + 1) * BK, tid, va);
+      lb.load((kt + 1) * BK, tid, vb);
+    }
+    float af[16], bf[16];
+    read_frag<A_KC>(lds_a[cur], wm * 32, li, lh, af);
+    read_frag<B_KC>(lds_b[cur], wn * 32, li, lh, bf);
+#pragma unroll
+    for (int s = 0; s < 16; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af[s], bf[s], acc, 0, 0, 0);
+    if (do_bias) {
+#pragma unroll 8
+      for (int k = 0; k < BK; ++k) bsum += lds_a[cur][k * KS_LD + tid];
+    }
+    if (kt + 1 < nk) {
+      TileLoader<A_KC>::store(lds_a[cur ^ 1], tid, va);
+      TileLoader<B_KC>::store(lds_b[cur ^ 1], tid, vb);
+    }
+    __syncthreads();
+  }
+
+  // epilogue: lane holds D[i][j], j = lane%32, i = 8*(r/4) + 4*(lane/32) + r%4
+  const int col = n0 + wn * 32 + li;
+  if (EPI == EPI_FWD_RELU || EPI == EPI_FWD_LINEAR) {
+    if (col < g.N) {
+      float* out = reinterpret_cast<float*>(g.out) + (int64_t)worker * g.ostride;
+      const float bcol = g.bias[(int64_t)worker * g.bstride + col];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wm * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+        if (row < g.M) {
+          float v = acc[r] + bcol;
+          if (EPI == EPI_FWD_RELU) v = v > 0.f ? v : 0.f;
+          out[(int64_t)row * g.ldo + col] = v;
+        }
+      }
+    }
+  } else if (EPI == EPI_DX_MASK) {
+    if (col < g.N) {
+      float* out = reinterpret_cast<float*>(g.out) + (int64_t)worker * g.ostride;
+      const float* mk = reinterpret_cast<const float*>(g.mask) + (int64_t)worker * g.mstride;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wm * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+        if (row < g.M) {
+          const int64_t e = (int64_t)row * g.ldo + col;
+          out[e] = mk[(int64_t)row * g.ldm + col] > 0.f ? acc[r] : 0.f;
+        }
+      }
+    }
+  } else {  // EPI_DW_UPDATE: rows are output units o, columns input units i
+    const int64_t wo = (int64_t)worker * g.pstride;
+    if (col < g.N) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = m0 + wm * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+        if (row < g.M) {
+          const int64_t e = wo + (int64_t)row * g.ldw + col;
+          const float nw = g.w_src[e] - g.eta * acc[r];
+          g.w_dst[e] = g.last ? (nw - g.w_snap[e]) / g.lam : nw;
+        }
+      }
+    }
+    if (do_bias) {
+      const int o = m0 + tid;
+      if (o < g.M) {
+        const int64_t e = wo + o;
+        const float nb = g.b_src[e] - g.eta * bsum;
+        g.b_dst[e] = g.last ? (nb - g.b_snap[e]) / g.lam : nb;
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_gemm_f32(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s) {
+  const int tm = (g.M + BM - 1) / BM, tn = (g.N + BN - 1) / BN;
+  const dim3 grid(tm * tn * g.batch), block(NT);
+  if (a_kc && b_kc && g.epi == EPI_FWD_RELU)
+    hipLaunchKernelGGL((gemm_f32_kernel<true, true, EPI_FWD_RELU>), grid, block, 0, s, g);
+  else if (a_kc && b_kc && g.epi == EPI_FWD_LINEAR)
+    hipLaunchKernelGGL((gemm_f32_kernel<true, true, EPI_FWD_LINEAR>), grid, block, 0, s, g);
+  else if (a_kc && !b_kc && g.epi == EPI_DX_MASK)
+    hipLaunchKernelGGL((gemm_f32_kernel<true, false, EPI_DX_MASK>), grid, block, 0, s, g);
+  else if (!a_kc && !b_kc && g.epi == EPI_DW_UPDATE)
+    hipLaunchKernelGGL((gemm_f32_kernel<false, false, EPI_DW_UPDATE>), grid, block, 0, s, g);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+}  // namespace agn

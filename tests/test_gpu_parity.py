@@ -1,0 +1,163 @@
+"""GPU path (libagn on gfx950) against the CPU oracle, element by element,
+on the same seeded inputs and commit orders.
+
+Tolerances (normwise per parameter tensor, maximum over tensors): float32
+<= 1e-4 after one round and <= 1e-3 after several; bf16 <= 2e-2.  Integer
+work (batch indices) is bit-exact.  Shapes are chosen to span several
+64x64 tiles with ragged tails, unaligned input widths (scalar load path),
+mini-batches that straddle the end of a shard, shards with an unused
+remainder, a single layer, one worker, lambda = 1 and m = 1.
+"""
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import AGNOracle, he_normal_init, flat_params, batch_indices
+from tests.helpers import rel_err, to_device, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+FP32_TOL_1 = 1e-4
+FP32_TOL_N = 1e-3
+BF16_TOL = 2e-2
+
+
+def _agn():
+    require_gpu()
+    import paper_1710_02368_amd as agn
+    return agn
+
+
+SMALL = [
+    # name, dims, n, lam, m, eta, rounds, N, data, order, dtype
+    ("ragged_deep", (200, 130, 70, 10), 3, 3, 40, 0.05, 3, 650, "gauss_linear", "permutation", "fp32"),
+    ("unaligned_d0", (37, 29, 5), 4, 2, 9, 0.1, 4, 101, "sparse_teacher2", "permutation", "fp32"),
+    ("single_layer", (64, 3), 2, 5, 16, 0.1, 2, 200, "gauss_linear", "sequential", "fp32"),
+    ("sgd_n1_lam1", (50, 70, 4), 1, 1, 130, 0.05, 3, 300, "gauss_linear", "sequential", "fp32"),
+    ("wide_tiles", (96, 300, 300, 12), 5, 2, 70, 0.05, 2, 1000, "sparse_teacher2", "permutation", "fp32"),
+    ("batch_of_one", (16, 8, 2), 2, 3, 1, 0.1, 3, 10, "gauss_linear", "permutation", "fp32"),
+]
+
+
+def run_parity(wl, tol1, tolN, check_workers=True):
+    agn = _agn()
+    import torch
+    X, y = W.make_data(wl)
+    orders = W.commit_orders(wl)
+    xd, yd = to_device(X, y)
+    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, dtype=wl.dtype)
+    o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, bf16=wl.dtype == "bf16")
+    # the initial central variable (same generator on both sides)
+    init_err, _ = rel_err(g.central().cpu().numpy(), o.central_flat(), wl.dims)
+    assert init_err <= 1e-7, f"init mismatch {init_err}"
+    for r, order in enumerate(orders, start=1):
+        g.round(xd, yd, order)
+        o.round(X, y, order)
+        tol = tol1 if r == 1 else tolN
+        err, where = rel_err(g.central().cpu().numpy(), o.central_flat(), wl.dims)
+        print(f"{wl.name} round {r}: central rel err {err:.3e} ({where})", flush=True)
+        assert err <= tol, (r, where, err)
+        gl = g.loss().cpu().numpy()
+        np.testing.assert_allclose(gl, o.last_loss, rtol=max(tol, 1e-5), atol=1e-6)
+        if check_workers:
+            for k in range(wl.n):
+                e, w = rel_err(g.worker_params(k).cpu().numpy(), o.worker_flat(k), wl.dims)
+                assert e <= tol, (r, k, w, e)
+    torch.cuda.synchronize()
+    g.close()
+
+
+@pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
+def test_small_shapes(case):
+    name, dims, n, lam, m, eta, R, N, data, order, dtype = case
+    wl = W.small_workload(name, dims, n, lam, m, eta, R, N, data=data, order=order, dtype=dtype)
+    tol1, tolN = (FP32_TOL_1, FP32_TOL_N) if dtype == "fp32" else (BF16_TOL, BF16_TOL)
+    run_parity(wl, tol1, tolN)
+
+
+def test_tiny_workload_full_size():
+    run_parity(W.workload("tiny"), FP32_TOL_1, FP32_TOL_1)
+
+
+def test_batch_indices_bit_exact():
+    agn = _agn()
+    for (N, n, m) in [(4096, 2, 32), (60000, 8, 128), (60000, 20, 128), (120000, 40, 128),
+                      (262144, 32, 256), (101, 4, 9), (10, 2, 1)]:
+        g = agn.AGN((8, 2), n, 1, 0.1, m, seed=1)
+        S = N // n
+        for k in sorted({0, n // 2, n - 1}):
+            for t in (0, 1, 7, 58, 449, 10 ** 7 + 3):
+                got = g.batch_indices(k, t, N).cpu().numpy()
+                np.testing.assert_array_equal(got, batch_indices(k, t, m, S))
+        g.close()
+
+
+def test_init_matches_oracle_generator():
+    agn = _agn()
+    for dims, seed in [((784, 1000, 1000, 10), 20171002), ((3072, 2048, 100), 5), ((7, 3, 2), 2 ** 63 + 11)]:
+        g = agn.AGN(dims, 2, 1, 0.1, 4, seed=seed)
+        got = g.central().cpu().numpy()
+        ref = flat_params(he_normal_init(dims, seed))
+        diff = got.view(np.int32).astype(np.int64) - ref.view(np.int32).astype(np.int64)
+        assert np.max(np.abs(diff)) <= 1, "more than 1 ulp apart"
+        assert np.mean(diff == 0) > 0.999
+        g.close()
+
+
+def test_determinism_bitwise():
+    agn = _agn()
+    wl = W.small_workload("det", (96, 300, 300, 12), 5, 3, 70, 0.05, 2, 1000)
+    X, y = W.make_data(wl)
+    xd, yd = to_device(X, y)
+    res = []
+    for _ in range(2):
+        g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed)
+        for order in W.commit_orders(wl):
+            g.round(xd, yd, order)
+        res.append((g.central().cpu().numpy(), g.loss().cpu().numpy()))
+        g.close()
+    np.testing.assert_array_equal(res[0][0], res[1][0])
+    np.testing.assert_array_equal(res[0][1], res[1][1])
+
+
+def test_set_central_and_eta_zero_fixed_point():
+    agn = _agn()
+    import torch
+    wl = W.small_workload("fix", (40, 24, 6), 3, 2, 8, 0.0, 2, 120)
+    X, y = W.make_data(wl)
+    xd, yd = to_device(X, y)
+    g = agn.AGN(wl.dims, wl.n, wl.lam, 0.0, wl.m, seed=3)
+    v = torch.linspace(-1, 1, g.P, device="cuda", dtype=torch.float32)
+    g.set_central(v)
+    g.round(xd, yd, [2, 0, 1])
+    assert torch.equal(g.central(), v)
+    for k in range(wl.n):
+        assert torch.equal(g.worker_params(k), v)
+    with pytest.raises(agn.AGNError):          # only before the first round
+        g.set_central(v)
+    g.close()
+
+
+def test_errors_leave_state_unchanged():
+    agn = _agn()
+    wl = W.small_workload("err", (20, 12, 4), 3, 2, 5, 0.1, 1, 60)
+    X, y = W.make_data(wl)
+    xd, yd = to_device(X, y)
+    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=4)
+    c0 = g.central().cpu().numpy()
+    for bad in ([0, 0, 1], [0, 1, 3], [2, 2, 2], [-1, 0, 1]):
+        with pytest.raises(agn.AGNError) as ei:
+            agn.agn_round(g.ctx, xd, yd, X.shape[0], bad)
+        assert ei.value.code == -1
+    with pytest.raises(agn.AGNError):
+        agn.agn_round(g.ctx, xd, yd, X.shape[0], [0, 1, 2], x_dtype=1)
+    with pytest.raises(agn.AGNError):
+        agn.agn_round(g.ctx, xd, yd, 2, [0, 1, 2])       # fewer samples than workers
+    with pytest.raises(agn.AGNError) as ei:
+        g.loss()                                          # no round yet
+    assert ei.value.code == -4
+    np.testing.assert_array_equal(g.central().cpu().numpy(), c0)
+    g.round(xd, yd, [1, 2, 0])
+    with pytest.raises(agn.AGNError):
+        agn.agn_round(g.ctx, xd, yd, X.shape[0] - 1, [0, 1, 2])   # N changed
+    g.close()

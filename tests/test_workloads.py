@@ -38,7 +38,7 @@ def test_sparse_data_and_two_layer_teacher():
     assert X.min() >= 0 and X.max() < 1
     counts = np.bincount(y, minlength=10)
     print("class histogram", counts)
-    assert (counts > 0).sum() >= 5
+    assert (counts > 0).sum() == 10 and counts.min() > 0.3 * counts.mean()
 
 
 def test_config3_shares_config2_data():

@@ -44,7 +44,7 @@ class Workload:
     N         number of samples; worker k owns rows [k*S, (k+1)*S), S = N // n
     data      "gauss_linear" (x ~ N(0,1), labels = argmax of a linear teacher)
               or "sparse_teacher2" (x = Bernoulli(0.2) * U[0,1), labels =
-              argmax of a two-layer ReLU teacher)
+              argmax of a two-layer ReLU teacher with per-class centred logits)
     seed      base seed; data, teacher and orders use independent streams
     dtype     "fp32" or "bf16" (bf16 GEMM inputs, fp32 master weights)
     data_seed seed of the data/teacher streams (config 3 shares config 2's data)
@@ -153,10 +153,13 @@ def _teacher_labels(wl: Workload, X_chunks: Sequence[np.ndarray], rng_t) -> np.n
         T = rng_t.standard_normal((d0, C))
         ys = [np.argmax(xc.astype(np.float64) @ T, axis=1) for xc in X_chunks]
     else:
+        # two-layer ReLU teacher; its logits are centred per class over the
+        # data set so that the classes come out roughly balanced
         A = rng_t.standard_normal((d0, TEACHER_HIDDEN)) / np.sqrt(d0)
         B = rng_t.standard_normal((TEACHER_HIDDEN, C)) / np.sqrt(TEACHER_HIDDEN)
-        ys = [np.argmax(np.maximum(xc.astype(np.float64) @ A, 0.0) @ B, axis=1)
-              for xc in X_chunks]
+        z = np.concatenate([np.maximum(xc.astype(np.float64) @ A, 0.0) @ B for xc in X_chunks])
+        z -= z.mean(axis=0)
+        ys = [np.argmax(z, axis=1)]
     return np.concatenate(ys).astype(np.int32)
 
 
