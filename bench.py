@@ -1,0 +1,189 @@
+"""Benchmark of the AGN hot path on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+One step is one AGN round: lambda local SGD steps of all n workers
+(forward, softmax cross-entropy, backward with the fused update) and the
+normalize/commit/pull of the n deltas in the round's commit order.  The
+value is whole-job throughput in worker-samples per second
+(n * lambda * m per round) with inputs resident in HBM.
+
+Printed: one JSON line with the metric, the per-kernel-class breakdown,
+the roofline of the dominant kernel class and the CPU oracle timed on a
+bounded sample on the host cores.  The timed region replays the captured
+round graph; the dominant class's average launch duration comes from HIP
+events around each of its launches in an eager pass of the same kernels on
+the same stream right after the timed region.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "worker-samples/sec per AGN round on 1 MI355X; MFMA util % + commit HBM GB/s"
+PEAK_HBM_GBS = 8000.0
+PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2516.6}   # dense MFMA peaks of MI355X
+CLASSES = ["fwd", "softmax", "dx", "dw", "commit"]
+
+
+def class_work(agn, g):
+    """Algorithmic work per round of each kernel class as the library
+    launches it: ("flop", FLOPs) for classes of matrix products, ("byte",
+    bytes) for the bandwidth classes."""
+    out = {}
+    for c in CLASSES:
+        f, b = agn.agn_kernel_class_work(g.ctx, agn.KERNEL_CLASSES[c])
+        out[c] = ("flop", f) if f > 0 else ("byte", b)
+    return out
+
+
+def cpu_baseline(wl, X, y, orders, budget_s=12.0):
+    """The oracle as it stands, on the host cores, over whole rounds until
+    about budget_s seconds have passed (at least one round)."""
+    from oracle import AGNOracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, bf16=wl.dtype == "bf16")
+    t0 = time.perf_counter()
+    rounds = 0
+    while True:
+        o.round(X, y, orders[rounds % len(orders)])
+        rounds += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": rounds * wl.worker_samples_per_round / dt, "unit": "worker-samples/s",
+            "cores": int(threads), "kind": "oracle",
+            "sample": f"{rounds} full round(s) of {wl.name} ({rounds * wl.worker_samples_per_round} "
+                      f"worker-samples) in {dt:.1f} s, float32 storage / float64 accumulation"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="mlp1000_n8")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the multi-GPU "
+              "sharding of the commit is a design, not a build", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_1710_02368_amd as agn
+    import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a ROCm GPU"
+    wl = W.workload(args.workload)
+    X, y = W.make_data(wl)
+    orders = W.commit_orders(wl, rounds=max(wl.rounds, 1))
+    xd = torch.from_numpy(X.view(np.int16) if X.dtype == np.uint16 else X).cuda()
+    yd = torch.from_numpy(y).cuda()
+    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, dtype=wl.dtype)
+    order_at = lambda i: orders[i % len(orders)]
+
+    for i in range(args.warmup):
+        g.round(xd, yd, order_at(i))
+    torch.cuda.synchronize()
+
+    # per-class breakdown (untimed pass, every class bracketed by events)
+    for c in CLASSES:
+        agn.agn_set_kernel_timing(g.ctx, agn.KERNEL_CLASSES[c], True)
+    prof_rounds = 2
+    for i in range(prof_rounds):
+        g.round(xd, yd, order_at(i))
+    work = class_work(agn, g)
+    breakdown = {}
+    for c in CLASSES:
+        ms, cnt = agn.agn_kernel_timing(g.ctx, agn.KERNEL_CLASSES[c])
+        agn.agn_set_kernel_timing(g.ctx, agn.KERNEL_CLASSES[c], False)
+        kind, amount = work[c]
+        per_round_ms = ms / prof_rounds
+        rate = amount / (per_round_ms * 1e-3) if per_round_ms > 0 else 0.0
+        breakdown[c] = {"ms_per_round": round(per_round_ms, 4), "launches_per_round": cnt // prof_rounds,
+                        ("TFLOP/s" if kind == "flop" else "GB/s"): round(rate / (1e12 if kind == "flop" else 1e9), 2)}
+    dominant = max(CLASSES, key=lambda c: breakdown[c]["ms_per_round"])
+
+    # timed region: K rounds, replaying the captured round graph (the product path)
+    for i in range(2):
+        g.round(xd, yd, order_at(i))     # (re)capture outside the timed region
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        g.round(xd, yd, order_at(args.warmup + i))
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+
+    # kernel timing pass right after it: the same kernels launched eagerly on
+    # the same stream, each launch of the dominant class between HIP events
+    kt_rounds = max(1, min(args.steps, 10))
+    agn.agn_set_kernel_timing(g.ctx, agn.KERNEL_CLASSES[dominant], True)
+    for i in range(kt_rounds):
+        g.round(xd, yd, order_at(i))
+    dom_ms, dom_cnt = agn.agn_kernel_timing(g.ctx, agn.KERNEL_CLASSES[dominant])
+    agn.agn_set_kernel_timing(g.ctx, agn.KERNEL_CLASSES[dominant], False)
+
+    # commit kernel alone (HBM roofline of the normalize/commit/pull)
+    agn.agn_set_kernel_timing(g.ctx, agn.KERNEL_CLASSES["commit"], True)
+    for i in range(5):
+        g.round(xd, yd, order_at(i))
+    c_ms, c_cnt = agn.agn_kernel_timing(g.ctx, agn.KERNEL_CLASSES["commit"])
+    agn.agn_set_kernel_timing(g.ctx, agn.KERNEL_CLASSES["commit"], False)
+    torch.cuda.synchronize()
+
+    value = args.steps * wl.worker_samples_per_round / dt
+    kind, amount = work[dominant]
+    per_launch = amount * kt_rounds / max(dom_cnt, 1)
+    avg_s = dom_ms * 1e-3 / max(dom_cnt, 1)
+    if kind == "flop":
+        achieved = per_launch / avg_s / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_TFLOPS[wl.dtype],
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS[wl.dtype], 4), "traffic": None,
+                "kernel_class": dominant, "avg_launch_us": round(avg_s * 1e6, 2),
+                "algorithmic_per_launch": per_launch, "launches": dom_cnt}
+    else:
+        achieved = per_launch / avg_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None, "kernel_class": dominant,
+                "avg_launch_us": round(avg_s * 1e6, 2), "algorithmic_per_launch": per_launch,
+                "launches": dom_cnt}
+    c_avg = c_ms * 1e-3 / max(c_cnt, 1)
+    commit_gbs = work["commit"][1] / c_avg / 1e9
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "worker-samples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(dt * 1e3 / args.steps, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32" if wl.dtype == "fp32" else "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "dims": list(wl.dims), "n": wl.n, "lambda": wl.lam, "m": wl.m,
+                   "eta": wl.eta, "commit_order": wl.order, "num_samples": wl.N,
+                   "worker_samples_per_round": wl.worker_samples_per_round},
+        "roofline": roof,
+        "commit_roofline": {"bound": "hbm", "achieved": round(commit_gbs, 1), "peak": PEAK_HBM_GBS,
+                            "unit": "GB/s", "frac": round(commit_gbs / PEAK_HBM_GBS, 4),
+                            "avg_launch_us": round(c_avg * 1e6, 2),
+                            "algorithmic_per_launch": work["commit"][1]},
+        "round_mfma_util": round(wl.flops_per_round / (dt / args.steps) / 1e12 / PEAK_TFLOPS[wl.dtype], 4),
+        "kernels": breakdown,
+    }
+    g.close()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, X, y, orders, budget_s=args.cpu_budget)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -145,11 +145,22 @@ int agn_debug_batch_indices(agn_ctx* ctx, int32_t worker, int64_t step_t,
 
 /* Kernel classes, in the order a local step launches them. */
 #define AGN_K_FWD 0     /* forward product + bias + ReLU (and output logits) */
-#define AGN_K_SOFTMAX 1 /* softmax cross-entropy, loss, output gradient      */
+#define AGN_K_SOFTMAX 1 /* output layer: softmax cross-entropy, loss, output
+                           gradient (with few classes also the logits and the
+                           output layer's input gradient, fused)             */
 #define AGN_K_DX 2      /* input-gradient product + ReLU mask                */
 #define AGN_K_DW 3      /* weight-gradient product + fused SGD update        */
 #define AGN_K_COMMIT 4  /* normalize + commit + pull                         */
 #define AGN_K_NUM 5
+
+/* Algorithmic work of one round attributed to a kernel class, as this
+ * context launches it: flops = 2 * multiply-adds of the class's matrix
+ * products; bytes = the memory traffic the class cannot avoid (for the
+ * commit: central + n deltas read, n pulled copies + central written;
+ * for the weight-gradient class: every parameter read and written once per
+ * local step).  HOST outputs. */
+int agn_kernel_class_work(agn_ctx* ctx, int32_t kernel_class, double* flops,
+                          double* bytes);
 
 /* When enabled, every launch of the given class is bracketed by HIP events
  * on the context's stream.  Enabling resets the counters. */

@@ -27,7 +27,7 @@ EXPORTED = [
     "agn_create", "agn_set_stream", "agn_round", "agn_central", "agn_loss",
     "agn_num_params", "agn_last_error", "agn_destroy", "agn_set_central",
     "agn_worker_params", "agn_debug_batch_indices", "agn_set_kernel_timing",
-    "agn_kernel_timing",
+    "agn_kernel_timing", "agn_kernel_class_work",
 ]
 
 
@@ -75,6 +75,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "agn_debug_batch_indices": (i32, [vp, i32, i64, i64, vp]),
         "agn_set_kernel_timing": (i32, [vp, i32, i32]),
         "agn_kernel_timing": (i32, [vp, i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]),
+        "agn_kernel_class_work": (i32, [vp, i32, ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -169,6 +171,13 @@ def agn_kernel_timing(ctx, kernel_class: int):
     cnt = ctypes.c_int64()
     _check(load_library().agn_kernel_timing(ctx, int(kernel_class), ctypes.byref(ms), ctypes.byref(cnt)), ctx)
     return ms.value, cnt.value
+
+
+def agn_kernel_class_work(ctx, kernel_class: int):
+    f = ctypes.c_double()
+    b = ctypes.c_double()
+    _check(load_library().agn_kernel_class_work(ctx, int(kernel_class), ctypes.byref(f), ctypes.byref(b)), ctx)
+    return f.value, b.value
 
 
 # --------------------------------------------------------------------------

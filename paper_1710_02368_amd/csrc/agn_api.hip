@@ -56,8 +56,17 @@ struct agn_ctx {
   int64_t* round_dev = nullptr;
   int64_t rounds = 0;
   int64_t N_fixed = -1;
-  hipStream_t stream = nullptr;
+  hipStream_t stream = nullptr;       // caller's stream (all work is ordered on it)
+  hipStream_t cap_stream = nullptr;   // private stream used only to capture the round graph
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t graph_exec = nullptr;
+  const void* graph_x = nullptr;      // data the captured graph was recorded with
+  const void* graph_y = nullptr;
+  int64_t graph_n = -1;
   int device = 0;
+  int use_head = 0;  // fused output-layer kernels (few classes)
+  int capturing = 0;
+  hipStream_t ls = nullptr;           // stream the launch sequence is enqueued on
   int poisoned = 0;
   std::string err;
   PackArgs pack{};
@@ -88,7 +97,19 @@ int fail(agn_ctx* c, int code, const std::string& msg) {
       return fail((ctx), AGN_EHIP, std::string(#expr) + ": " + hipGetErrorString(e_));      \
   } while (0)
 
+void drop_graph(agn_ctx* c) {
+  if (c->graph_exec) (void)hipGraphExecDestroy(c->graph_exec);
+  if (c->graph) (void)hipGraphDestroy(c->graph);
+  c->graph_exec = nullptr;
+  c->graph = nullptr;
+  c->graph_x = c->graph_y = nullptr;
+  c->graph_n = -1;
+}
+
 void free_all(agn_ctx* c) {
+  drop_graph(c);
+  if (c->cap_stream) (void)hipStreamDestroy(c->cap_stream);
+  c->cap_stream = nullptr;
   for (void* p : c->allocs) (void)hipFree(p);
   c->allocs.clear();
   for (auto& t : c->timing)
@@ -109,7 +130,7 @@ hipError_t dalloc(agn_ctx* c, T** p, int64_t count) {
 template <class F>
 hipError_t timed(agn_ctx* c, int cls, F&& launch) {
   TimingSlot& t = c->timing[cls];
-  if (!t.enabled) return launch();
+  if (!t.enabled || c->capturing) return launch();
   if (t.used >= (1u << 15)) {
     ++t.dropped;
     return launch();
@@ -159,11 +180,13 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
   const int x_vec = (d0 % (bf ? 8 : 4) == 0) && ((uintptr_t)d->x % 16 == 0);
   Operand xop{d->x, d0, 0, 1, x_vec};
   auto gemm = [&](int a_kc, int b_kc, const GemmArgs& g) {
-    return bf ? launch_gemm_bf16(a_kc, b_kc, g, c->stream) : launch_gemm_f32(a_kc, b_kc, g, c->stream);
+    return bf ? launch_gemm_bf16(a_kc, b_kc, g, c->ls) : launch_gemm_f32(a_kc, b_kc, g, c->ls);
   };
 
-  // forward: hidden layers with bias + ReLU, then the logits
-  for (int l = 0; l < L; ++l) {
+  // forward: hidden layers with bias + ReLU, then the logits (unless the
+  // fused output-layer kernel computes them)
+  const int fwd_layers = c->use_head ? L - 1 : L;
+  for (int l = 0; l < fwd_layers; ++l) {
     GemmArgs g{};
     g.M = m;
     g.N = c->dims[l + 1];
@@ -181,8 +204,62 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     HIP_CHECK(c, timed(c, AGN_K_FWD, [&] { return gemm(1, 1, g); }));
   }
 
-  // softmax cross-entropy: per-row loss and the output gradient dZ_L
-  {
+  if (c->use_head) {
+    // logits + softmax cross-entropy + dZ_L + dZ_{L-1}, then dW_{L-1} + update
+    const bool first = L == 1;
+    const float* hin = first ? (const float*)d->x : (const float*)c->H[L - 1];
+    const int64_t ldh = first ? d0 : c->lda[L - 1];
+    const int64_t hst = first ? 0 : (int64_t)m * c->lda[L - 1];
+    HeadArgs h{};
+    h.h = hin;
+    h.ldh = ldh;
+    h.hstride = hst;
+    h.gather = first;
+    h.w = src + c->woff[L - 1];
+    h.b = src + c->boff[L - 1];
+    h.ldw = c->ldw[L - 1];
+    h.pstride = ps;
+    h.y = d->y;
+    h.g = gath;
+    h.n = n;
+    h.m = m;
+    h.d = c->dims[L - 1];
+    h.C = c->dims[L];
+    h.dz = (float*)c->dZ[L];
+    h.lddz = c->lda[L];
+    h.dzstride = (int64_t)m * c->lda[L];
+    h.dprev = first ? nullptr : (float*)c->dZ[L - 1];
+    h.loss = c->loss;
+    h.lam = c->lam;
+    h.step = step;
+    HIP_CHECK(c, timed(c, AGN_K_SOFTMAX, [&] { return launch_head(h, c->ls); }));
+    HeadDwArgs w{};
+    w.h = hin;
+    w.ldh = ldh;
+    w.hstride = hst;
+    w.gather = first;
+    w.g = gath;
+    w.dz = (const float*)c->dZ[L];
+    w.lddz = c->lda[L];
+    w.dzstride = (int64_t)m * c->lda[L];
+    w.n = n;
+    w.m = m;
+    w.d = c->dims[L - 1];
+    w.C = c->dims[L];
+    w.w_src = src + c->woff[L - 1];
+    w.w_dst = dst + c->woff[L - 1];
+    w.w_snap = c->snap + c->woff[L - 1];
+    w.b_src = src + c->boff[L - 1];
+    w.b_dst = dst + c->boff[L - 1];
+    w.b_snap = c->snap + c->boff[L - 1];
+    w.ldw = c->ldw[L - 1];
+    w.pstride = ps;
+    w.eta = c->eta;
+    w.lam = (float)c->lam;
+    w.last = last;
+    HIP_CHECK(c, timed(c, AGN_K_DW, [&] { return launch_head_dw(w, c->ls); }));
+  } else {
+    // softmax cross-entropy: per-row loss and the output gradient dZ_L
     SoftmaxArgs s{};
     s.z = c->Z;
     s.ldz = c->lda[L];
@@ -199,11 +276,11 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     s.loss = c->loss;
     s.lam = c->lam;
     s.step = step;
-    HIP_CHECK(c, timed(c, AGN_K_SOFTMAX, [&] { return launch_softmax_ce(s, c->stream); }));
+    HIP_CHECK(c, timed(c, AGN_K_SOFTMAX, [&] { return launch_softmax_ce(s, c->ls); }));
   }
 
-  // backward, last layer first
-  for (int l = L - 1; l >= 0; --l) {
+  // backward, last layer first (the fused output layer already did layer L-1)
+  for (int l = c->use_head ? L - 2 : L - 1; l >= 0; --l) {
     const int64_t dz_ld = c->lda[l + 1], dz_st = (int64_t)m * c->lda[l + 1];
     if (l >= 1) {  // dZ_l = (dZ_{l+1} W_l) * [H_l > 0]
       GemmArgs g{};
@@ -249,6 +326,25 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     }
   }
   (void)dst16;
+  return AGN_OK;
+}
+
+// lambda local steps of every worker, then normalize + commit + pull
+int enqueue_round(agn_ctx* c, const agn_data* d) {
+  const int64_t S = d->num_samples / c->n;
+  for (int i = 0; i < c->lam; ++i)
+    if (int r = enqueue_step(c, d, S, i)) return r;
+  CommitArgs ca{};
+  ca.central = c->central;
+  ca.snap = c->snap;
+  ca.delta = c->buf[(c->lam - 1) & 1];
+  ca.snap16 = c->snap16;
+  ca.order = c->order;
+  ca.round = c->round_dev;
+  ca.pstride = c->P_pad;
+  ca.count = c->P_pad;
+  ca.n = c->n;
+  HIP_CHECK(c, timed(c, AGN_K_COMMIT, [&] { return launch_commit(ca, c->ls); }));
   return AGN_OK;
 }
 
@@ -312,6 +408,9 @@ int agn_create(const agn_shapes* shapes, int32_t n, int32_t lambda, float eta, u
     return fail(nullptr, code, msg);
   };
   if (hipGetDevice(&c->device) != hipSuccess) return bail(AGN_EHIP, "no HIP device");
+  c->use_head = c->dtype == AGN_FP32 && head_prepare(c->dims[L], c->dims[L - 1]);
+  if (hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking) != hipSuccess)
+    return bail(AGN_EHIP, "hipStreamCreate failed");
 
   const bool bf = c->dtype == AGN_BF16;
   const int64_t nps = (int64_t)n * c->P_pad;
@@ -384,21 +483,37 @@ int agn_round(agn_ctx* c, const agn_data* d, const int32_t* order) {
     }
   }
   if (int r = set_device(c)) return r;
-  const int64_t S = d->num_samples / c->n;
+  // the commit order of this round (read by the commit kernel)
   HIP_CHECK(c, launch_set_order(order, c->n, c->order, c->stream));
-  for (int i = 0; i < c->lam; ++i)
-    if (int r = enqueue_step(c, d, S, i)) return r;
-  CommitArgs ca{};
-  ca.central = c->central;
-  ca.snap = c->snap;
-  ca.delta = c->buf[(c->lam - 1) & 1];
-  ca.snap16 = c->snap16;
-  ca.order = c->order;
-  ca.round = c->round_dev;
-  ca.pstride = c->P_pad;
-  ca.count = c->P_pad;
-  ca.n = c->n;
-  HIP_CHECK(c, timed(c, AGN_K_COMMIT, [&] { return launch_commit(ca, c->stream); }));
+  bool timing = false;
+  for (const auto& t : c->timing) timing = timing || t.enabled;
+  if (timing) {  // eager launches, each timed class bracketed by events
+    c->ls = c->stream;
+    if (int r = enqueue_round(c, d)) return r;
+  } else {       // replay the captured round
+    if (!c->graph_exec || c->graph_x != d->x || c->graph_y != d->y || c->graph_n != d->num_samples) {
+      drop_graph(c);
+      c->ls = c->cap_stream;
+      c->capturing = 1;
+      hipError_t e = hipStreamBeginCapture(c->cap_stream, hipStreamCaptureModeRelaxed);
+      int r = e == hipSuccess ? enqueue_round(c, d) : AGN_OK;
+      hipGraph_t gr = nullptr;
+      hipError_t e2 = hipStreamEndCapture(c->cap_stream, &gr);
+      c->capturing = 0;
+      if (r) {
+        if (gr) (void)hipGraphDestroy(gr);
+        return r;
+      }
+      HIP_CHECK(c, e);
+      HIP_CHECK(c, e2);
+      c->graph = gr;
+      HIP_CHECK(c, hipGraphInstantiate(&c->graph_exec, c->graph, nullptr, nullptr, 0));
+      c->graph_x = d->x;
+      c->graph_y = d->y;
+      c->graph_n = d->num_samples;
+    }
+    HIP_CHECK(c, hipGraphLaunch(c->graph_exec, c->stream));
+  }
   c->N_fixed = d->num_samples;
   ++c->rounds;
   return AGN_OK;
@@ -465,6 +580,44 @@ int agn_debug_batch_indices(agn_ctx* c, int32_t worker, int64_t step_t, int64_t 
   if (int r = set_device(c)) return r;
   HIP_CHECK(c, launch_batch_indices(worker, step_t, c->m, num_samples / c->n, out, c->stream));
   HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  return AGN_OK;
+}
+
+int agn_kernel_class_work(agn_ctx* c, int32_t cls, double* flops, double* bytes) {
+  if (int r = check_ctx(c)) return r;
+  if (cls < 0 || cls >= AGN_K_NUM) return fail(c, AGN_EINVAL, "kernel class out of range");
+  if (!flops || !bytes) return fail(c, AGN_EINVAL, "null output pointer");
+  const int L = c->L;
+  const double rows = (double)c->n * c->lam * c->m;  // worker-samples per round
+  auto mac = [&](int l) { return (double)c->dims[l] * c->dims[l + 1]; };
+  const double C = c->dims[L];
+  const double xb = c->dtype == AGN_BF16 ? 2.0 : 4.0;
+  double f = 0.0, b = 0.0;
+  switch (cls) {
+    case AGN_K_FWD:
+      for (int l = 0; l < (c->use_head ? L - 1 : L); ++l) f += 2.0 * mac(l) * rows;
+      break;
+    case AGN_K_SOFTMAX:
+      if (c->use_head) {
+        f = 2.0 * mac(L - 1) * rows * (L >= 2 ? 2.0 : 1.0);
+        b = rows * (4.0 * c->dims[L - 1] * (L >= 2 ? 2.0 : 1.0) + 4.0 * C + 8.0);
+      } else {
+        b = rows * (4.0 * C + xb * C + 4.0);
+      }
+      break;
+    case AGN_K_DX:
+      for (int l = 1; l < (c->use_head ? L - 1 : L); ++l) f += 2.0 * mac(l) * rows;
+      break;
+    case AGN_K_DW:
+      for (int l = 0; l < L; ++l) f += 2.0 * mac(l) * rows;
+      b = 8.0 * (double)c->n * c->P * c->lam;  // read + write every parameter each step
+      break;
+    case AGN_K_COMMIT:
+      b = 8.0 * (double)(c->n + 1) * c->P;    // central + n deltas in, n pulls + central out
+      break;
+  }
+  *flops = f;
+  *bytes = b;
   return AGN_OK;
 }
 

@@ -77,6 +77,46 @@ struct SoftmaxArgs {
 };
 hipError_t launch_softmax_ce(const SoftmaxArgs& a, hipStream_t s);
 
+// Fused output layer (C <= 32): logits, softmax cross-entropy, output
+// gradient dZ_L and the previous layer's input gradient dZ_{L-1}.
+struct HeadArgs {
+  const float* h;          // H_{L-1} [n][m][ldh] (or the data set, gathered, when L == 1)
+  int64_t ldh, hstride;
+  int32_t gather;
+  const float* w;          // W_{L-1} of worker 0 in the step's source parameters
+  const float* b;          // b_{L-1}
+  int64_t ldw, pstride;
+  const int32_t* y;
+  Gather g;
+  int32_t n, m, d, C;
+  float* dz;               // dZ_L [n][m][lddz]
+  int64_t lddz, dzstride;
+  float* dprev;            // dZ_{L-1}, same layout as h (null when L == 1)
+  float* loss;             // [n][lam][m]
+  int32_t lam, step;
+};
+struct HeadDwArgs {        // output-layer weight gradient + update (M = C <= 32)
+  const float* h;
+  int64_t ldh, hstride;
+  int32_t gather;
+  Gather g;
+  const float* dz;
+  int64_t lddz, dzstride;
+  int32_t n, m, d, C;
+  const float* w_src;
+  float* w_dst;
+  const float* w_snap;
+  const float* b_src;
+  float* b_dst;
+  const float* b_snap;
+  int64_t ldw, pstride;
+  float eta, lam;
+  int32_t last;
+};
+bool head_prepare(int C, int d);
+hipError_t launch_head(const HeadArgs& a, hipStream_t s);
+hipError_t launch_head_dw(const HeadDwArgs& a, hipStream_t s);
+
 struct CommitArgs {
   float* central;          // [P_pad]
   float* snap;             // [n][P_pad] pulled copies (written)

@@ -31,8 +31,14 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 constexpr int BM = 64, BN = 64, BK = 32, NT = 256;
 constexpr int KC_LD = BK + 4;            // LDS row stride of a K-contiguous tile
 constexpr int KS_LD = 64 + 4;            // LDS row stride of a K-strided tile
+constexpr int KS_SKEW = 32;              // extra offset of K-strided rows 16..31
 constexpr int KC_TILE = 64 * KC_LD;
-constexpr int KS_TILE = BK * KS_LD;
+constexpr int KS_TILE = BK * KS_LD + KS_SKEW;
+
+// LDS offset of element (k, outer) of a K-strided tile.  Rows k and k+16 are
+// read by the two halves of a wave in the same instruction; the skew puts
+// them 32 banks apart.
+__device__ __forceinline__ int ks_off(int k, int o) { return k * KS_LD + o + (k >> 4) * KS_SKEW; }
 
 __device__ __forceinline__ float4 load4(const float* p, int valid, int vec) {
   if (valid >= 4 && vec) return *reinterpret_cast<const float4*>(p);
@@ -107,7 +113,7 @@ struct TileLoader {
       if (KC) {
         *reinterpret_cast<float4*>(lds + (tid / 8 + 32 * p) * KC_LD + 4 * (tid % 8)) = v[p];
       } else {
-        *reinterpret_cast<float4*>(lds + (tid / 16 + 16 * p) * KS_LD + 4 * (tid % 16)) = v[p];
+        *reinterpret_cast<float4*>(lds + ks_off(tid / 16 + 16 * p, 4 * (tid % 16))) = v[p];
       }
     }
   }
@@ -130,7 +136,7 @@ __device__ __forceinline__ void read_frag(const float* lds, int outer_off, int l
     }
   } else {
 #pragma unroll
-    for (int s = 0; s < 16; ++s) f[s] = lds[(lh * 16 + s) * KS_LD + outer_off + li];
+    for (int s = 0; s < 16; ++s) f[s] = lds[ks_off(lh * 16 + s, outer_off + li)];
   }
 }
 
@@ -162,10 +168,16 @@ __global__ __launch_bounds__(NT) void gemm_f32_kernel(GemmArgs g) {
   const bool do_bias = (EPI == EPI_DW_UPDATE) && tile_n == 0 && tid < 64;
   float bsum = 0.f;
 
-  f32x16 acc;
+  // two independent accumulation chains (even / odd MFMA of each step)
+  f32x16 acc0, acc1;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  for (int r = 0; r < 16; ++r) {
+    acc0[r] = 0.f;
+    acc1[r] = 0.f;
+  }
 
+  // K loop: the next tile's global loads are in flight while the current
+  // tile's 16 MFMAs run; LDS is double-buffered, one barrier per step.
   const int nk = (g.K + BK - 1) / BK;
   float4 va[2], vb[2];
   la.load(0, tid, va);
@@ -184,10 +196,13 @@ __global__ __launch_bounds__(NT) void gemm_f32_kernel(GemmArgs g) {
     read_frag<A_KC>(lds_a[cur], wm * 32, li, lh, af);
     read_frag<B_KC>(lds_b[cur], wn * 32, li, lh, bf);
 #pragma unroll
-    for (int s = 0; s < 16; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(af[s], bf[s], acc, 0, 0, 0);
+    for (int s = 0; s < 16; s += 2) {
+      acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(af[s], bf[s], acc0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_f32_32x32x2f32(af[s + 1], bf[s + 1], acc1, 0, 0, 0);
+    }
     if (do_bias) {
 #pragma unroll 8
-      for (int k = 0; k < BK; ++k) bsum += lds_a[cur][k * KS_LD + tid];
+      for (int k = 0; k < BK; ++k) bsum += lds_a[cur][ks_off(k, tid)];
     }
     if (kt + 1 < nk) {
       TileLoader<A_KC>::store(lds_a[cur ^ 1], tid, va);
@@ -195,6 +210,7 @@ __global__ __launch_bounds__(NT) void gemm_f32_kernel(GemmArgs g) {
     }
     __syncthreads();
   }
+  f32x16 acc = acc0 + acc1;
 
   // epilogue: lane holds D[i][j], j = lane%32, i = 8*(r/4) + 4*(lane/32) + r%4
   const int col = n0 + wn * 32 + li;
@@ -251,20 +267,19 @@ __global__ __launch_bounds__(NT) void gemm_f32_kernel(GemmArgs g) {
 
 }  // namespace
 
-hipError_t launch_gemm_f32(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s) {
+template <bool A_KC, bool B_KC, int EPI>
+static hipError_t go(const GemmArgs& g, hipStream_t s) {
   const int tm = (g.M + BM - 1) / BM, tn = (g.N + BN - 1) / BN;
-  const dim3 grid(tm * tn * g.batch), block(NT);
-  if (a_kc && b_kc && g.epi == EPI_FWD_RELU)
-    hipLaunchKernelGGL((gemm_f32_kernel<true, true, EPI_FWD_RELU>), grid, block, 0, s, g);
-  else if (a_kc && b_kc && g.epi == EPI_FWD_LINEAR)
-    hipLaunchKernelGGL((gemm_f32_kernel<true, true, EPI_FWD_LINEAR>), grid, block, 0, s, g);
-  else if (a_kc && !b_kc && g.epi == EPI_DX_MASK)
-    hipLaunchKernelGGL((gemm_f32_kernel<true, false, EPI_DX_MASK>), grid, block, 0, s, g);
-  else if (!a_kc && !b_kc && g.epi == EPI_DW_UPDATE)
-    hipLaunchKernelGGL((gemm_f32_kernel<false, false, EPI_DW_UPDATE>), grid, block, 0, s, g);
-  else
-    return hipErrorInvalidValue;
+  hipLaunchKernelGGL((gemm_f32_kernel<A_KC, B_KC, EPI>), dim3(tm * tn * g.batch), dim3(NT), 0, s, g);
   return hipGetLastError();
+}
+
+hipError_t launch_gemm_f32(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s) {
+  if (a_kc && b_kc && g.epi == EPI_FWD_RELU) return go<true, true, EPI_FWD_RELU>(g, s);
+  if (a_kc && b_kc && g.epi == EPI_FWD_LINEAR) return go<true, true, EPI_FWD_LINEAR>(g, s);
+  if (a_kc && !b_kc && g.epi == EPI_DX_MASK) return go<true, false, EPI_DX_MASK>(g, s);
+  if (!a_kc && !b_kc && g.epi == EPI_DW_UPDATE) return go<false, false, EPI_DW_UPDATE>(g, s);
+  return hipErrorInvalidValue;
 }
 
 }  // namespace agn

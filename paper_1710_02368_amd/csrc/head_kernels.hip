@@ -1,0 +1,303 @@
+// Output layer of the local step for few classes (C <= 32): one fused
+// kernel for the logits, the softmax cross-entropy with its gradient and
+// the output layer's input gradient, and one kernel for the output layer's
+// weight gradient with the SGD update.  These layers are skinny (C rows or
+// C columns), so tile products leave most of a matrix-core tile empty; the
+// work is vector FMAs from LDS-resident weights.
+//
+// Per row j of a worker's mini-batch (softmax cross-entropy, Eq. 1's loss):
+//   z_c = b_c + sum_i H[j][i] W[c][i]
+//   loss_j = logsumexp(z) - z_{y_j};   dZ[j][c] = (softmax(z)_c - [c == y_j]) / m
+//   dZ_prev[j][i] = (sum_c dZ[j][c] W[c][i]) * [H[j][i] > 0]
+// Weight gradient (summed over the m rows) fused with the update:
+//   W[c][i] <- W[c][i] - eta * sum_j dZ[j][c] H[j][i];  b[c] <- b[c] - eta * sum_j dZ[j][c]
+#include <math.h>
+
+#include "device_common.h"
+
+namespace agn {
+namespace {
+
+constexpr int HEAD_WAVE_ROWS = 2;                  // rows a wave processes together
+constexpr int HEAD_ROWS = 4 * HEAD_WAVE_ROWS;       // rows per workgroup
+constexpr int HEAD_DMAX = 2048;                     // hidden width limit
+
+__device__ __forceinline__ float wsum(float v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+// LDS: W padded to CMAX rows x 64*QMAX columns (zeros outside C x d), then b.
+// Each wave keeps its rows of H in registers (QMAX per lane per row, all
+// loaded at once); padding rows and columns are zero, so the loops are
+// static and branch-free.
+template <int CMAX, int QMAX>
+__global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
+  extern __shared__ float smem[];
+  constexpr int LW = 64 * QMAX;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int blocks_per_worker = (a.m + HEAD_ROWS - 1) / HEAD_ROWS;
+  const int k = blockIdx.x / blocks_per_worker;
+  const int r0 = (blockIdx.x % blocks_per_worker) * HEAD_ROWS;
+  const int d = a.d, C = a.C;
+  const float* W = a.w + (int64_t)k * a.pstride;
+  const float* bias = a.b + (int64_t)k * a.pstride;
+  float* Ws = smem;
+  float* bs = smem + CMAX * LW;
+  const int64_t t = gather_step(a.g);
+
+  // rows of this wave: issue every load of H before anything waits
+  int jr[HEAD_WAVE_ROWS];
+  const float* hp[HEAD_WAVE_ROWS];
+  float hv[HEAD_WAVE_ROWS][QMAX];
+#pragma unroll
+  for (int r = 0; r < HEAD_WAVE_ROWS; ++r) {
+    jr[r] = r0 + wave * HEAD_WAVE_ROWS + r;
+    const int j = jr[r] < a.m ? jr[r] : a.m - 1;   // rows past m compute a copy, store nothing
+    hp[r] = a.gather ? a.h + batch_row(k, t, a.g.mb, a.g.S, j) * a.ldh
+                     : a.h + (int64_t)k * a.hstride + (int64_t)j * a.ldh;
+#pragma unroll
+    for (int q = 0; q < QMAX; ++q) {
+      const int i = lane + 64 * q;
+      hv[r][q] = hp[r][i < d ? i : d - 1];
+    }
+  }
+  // W and b into LDS, float4 at a time (W rows are 16-byte aligned)
+  constexpr int NW4 = CMAX * LW / 4;
+#pragma unroll
+  for (int it = 0; it < (NW4 + 255) / 256; ++it) {
+    const int e4 = tid + 256 * it;
+    if (NW4 % 256 != 0 && e4 >= NW4) break;
+    const int c = e4 / (LW / 4), i = 4 * (e4 % (LW / 4));
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (c < C && i < d) {
+      v = *reinterpret_cast<const float4*>(W + (int64_t)c * a.ldw + i);
+      if (i + 1 >= d) v.y = 0.f;
+      if (i + 2 >= d) v.z = 0.f;
+      if (i + 3 >= d) v.w = 0.f;
+    }
+    *reinterpret_cast<float4*>(Ws + c * LW + i) = v;
+  }
+  if (tid < CMAX) bs[tid] = tid < C ? bias[tid] : 0.f;
+#pragma unroll
+  for (int r = 0; r < HEAD_WAVE_ROWS; ++r)
+#pragma unroll
+    for (int q = 0; q < QMAX; ++q) hv[r][q] = lane + 64 * q < d ? hv[r][q] : 0.f;
+  __syncthreads();
+
+  // logits: lane-partial dot products, then one wave reduction per (row, class)
+  float p[HEAD_WAVE_ROWS][CMAX];
+#pragma unroll
+  for (int r = 0; r < HEAD_WAVE_ROWS; ++r)
+#pragma unroll
+    for (int c = 0; c < CMAX; ++c) p[r][c] = 0.f;
+#pragma unroll
+  for (int q = 0; q < QMAX; ++q) {
+#pragma unroll
+    for (int c = 0; c < CMAX; ++c) {
+      const float w = Ws[c * LW + lane + 64 * q];
+#pragma unroll
+      for (int r = 0; r < HEAD_WAVE_ROWS; ++r) p[r][c] += hv[r][q] * w;
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < HEAD_WAVE_ROWS; ++r)
+#pragma unroll
+    for (int c = 0; c < CMAX; ++c) p[r][c] = wsum(p[r][c]) + bs[c];
+
+  // softmax cross-entropy per row; p becomes dZ
+  const float inv_m = 1.f / (float)a.m;
+#pragma unroll
+  for (int r = 0; r < HEAD_WAVE_ROWS; ++r) {
+    const int j = jr[r] < a.m ? jr[r] : a.m - 1;
+    const int label = a.y[batch_row(k, t, a.g.mb, a.g.S, j)];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int c = 0; c < CMAX; ++c) mx = c < C ? fmaxf(mx, p[r][c]) : mx;
+    float s = 0.f, zy = 0.f;
+#pragma unroll
+    for (int c = 0; c < CMAX; ++c) {
+      const float e = c < C ? expf(p[r][c] - mx) : 0.f;
+      zy = c == label ? p[r][c] : zy;
+      s += e;
+      p[r][c] = e;
+    }
+    const float inv_s = 1.f / s;
+#pragma unroll
+    for (int c = 0; c < CMAX; ++c)
+      p[r][c] = c < C ? (p[r][c] * inv_s - (c == label ? 1.f : 0.f)) * inv_m : 0.f;
+    if (jr[r] < a.m) {
+      float* dzo = a.dz + (int64_t)k * a.dzstride + (int64_t)jr[r] * a.lddz;
+      float mine = 0.f;
+#pragma unroll
+      for (int c = 0; c < CMAX; ++c) mine = lane == c ? p[r][c] : mine;
+      if (lane < C) dzo[lane] = mine;
+      if (lane == 0) a.loss[((int64_t)k * a.lam + a.step) * a.m + jr[r]] = mx + logf(s) - zy;
+    }
+  }
+
+  // input gradient of the output layer, masked by the ReLU of H_{L-1}
+  if (a.dprev) {
+#pragma unroll
+    for (int q = 0; q < QMAX; ++q) {
+      const int i = lane + 64 * q;
+      float acc[HEAD_WAVE_ROWS];
+#pragma unroll
+      for (int r = 0; r < HEAD_WAVE_ROWS; ++r) acc[r] = 0.f;
+#pragma unroll
+      for (int c = 0; c < CMAX; ++c) {
+        const float w = Ws[c * LW + i];
+#pragma unroll
+        for (int r = 0; r < HEAD_WAVE_ROWS; ++r) acc[r] += p[r][c] * w;
+      }
+#pragma unroll
+      for (int r = 0; r < HEAD_WAVE_ROWS; ++r) {
+        if (jr[r] < a.m && i < d) {
+          float* dp = a.dprev + (int64_t)k * a.hstride + (int64_t)jr[r] * a.ldh;
+          dp[i] = hv[r][q] > 0.f ? acc[r] : 0.f;
+        }
+      }
+    }
+  }
+}
+
+// Output-layer weight gradient + update.  Workgroup = (worker, 64 input
+// units); lane owns input unit i, the 4 waves split the m rows (row j goes
+// to wave j % 4) and their partial sums are added in wave order.
+constexpr int HDW_CHUNK = 128;  // rows of dZ staged in LDS at a time
+template <int CMAX>
+__global__ __launch_bounds__(256) void head_dw_kernel(HeadDwArgs a) {
+  __shared__ float dzs[HDW_CHUNK * CMAX];
+  __shared__ float part[4][CMAX][64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int blocks_per_worker = (a.d + 63) / 64;
+  const int k = blockIdx.x / blocks_per_worker;
+  const int ib = blockIdx.x % blocks_per_worker;
+  const int i = ib * 64 + lane;
+  const int ic = i < a.d ? i : a.d - 1;
+  const int C = a.C;
+  const int64_t t = a.gather ? gather_step(a.g) : 0;
+  const float* hb = a.h + (int64_t)k * a.hstride;
+  const float* dzb = a.dz + (int64_t)k * a.dzstride;
+  float acc[CMAX];
+#pragma unroll
+  for (int c = 0; c < CMAX; ++c) acc[c] = 0.f;
+  float bsum = 0.f;
+  for (int j0 = 0; j0 < a.m; j0 += HDW_CHUNK) {
+    const int rows = min(HDW_CHUNK, a.m - j0);
+    __syncthreads();
+    for (int e = tid; e < rows * CMAX; e += 256) {
+      const int r = e / CMAX, c = e - r * CMAX;
+      dzs[e] = c < C ? dzb[(int64_t)(j0 + r) * a.lddz + c] : 0.f;
+    }
+    __syncthreads();
+    if (ib == 0 && tid < C)
+      for (int r = 0; r < rows; ++r) bsum += dzs[r * CMAX + tid];
+    int r = wave;
+    for (; r + 28 < rows; r += 32) {   // 8 rows per wave in flight
+      float hv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int j = j0 + r + 4 * u;
+        const int64_t row = a.gather ? batch_row(k, t, a.g.mb, a.g.S, j) : j;
+        hv[u] = hb[row * a.ldh + ic];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+#pragma unroll
+        for (int c = 0; c < CMAX; ++c) acc[c] += dzs[(r + 4 * u) * CMAX + c] * hv[u];
+    }
+    for (; r < rows; r += 4) {
+      const int j = j0 + r;
+      const int64_t row = a.gather ? batch_row(k, t, a.g.mb, a.g.S, j) : j;
+      const float hv = hb[row * a.ldh + ic];
+#pragma unroll
+      for (int c = 0; c < CMAX; ++c) acc[c] += dzs[r * CMAX + c] * hv;
+    }
+  }
+#pragma unroll
+  for (int c = 0; c < CMAX; ++c) part[wave][c][lane] = acc[c];
+  __syncthreads();
+  const int64_t wo = (int64_t)k * a.pstride;
+  for (int c = wave; c < C; c += 4) {
+    const float g = ((part[0][c][lane] + part[1][c][lane]) + part[2][c][lane]) + part[3][c][lane];
+    if (i < a.d) {
+      const int64_t e = wo + (int64_t)c * a.ldw + i;
+      const float nw = a.w_src[e] - a.eta * g;
+      a.w_dst[e] = a.last ? (nw - a.w_snap[e]) / a.lam : nw;
+    }
+  }
+  if (ib == 0 && tid < C) {
+    const int64_t e = wo + tid;
+    const float nb = a.b_src[e] - a.eta * bsum;
+    a.b_dst[e] = a.last ? (nb - a.b_snap[e]) / a.lam : nb;
+  }
+}
+
+}  // namespace
+
+static int head_cmax(int C) { return C <= 10 ? 10 : C <= 16 ? 16 : 32; }
+static int head_qmax(int d) { return d <= 128 ? 2 : d <= 512 ? 8 : d <= 1024 ? 16 : 32; }
+
+size_t head_lds_bytes(int C, int d) {
+  const int cm = head_cmax(C);
+  return ((size_t)cm * 64 * head_qmax(d) + cm) * sizeof(float);
+}
+
+template <int CM, int QM>
+static hipError_t head_go(const HeadArgs& a, hipStream_t s, bool prepare) {
+  const size_t lds = head_lds_bytes(a.C, a.d);
+  if (prepare) {
+    if (lds <= 64 * 1024) return hipSuccess;
+    return hipFuncSetAttribute((const void*)head_kernel<CM, QM>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                               (int)lds);
+  }
+  const int blocks = a.n * ((a.m + HEAD_ROWS - 1) / HEAD_ROWS);
+  hipLaunchKernelGGL((head_kernel<CM, QM>), dim3(blocks), dim3(256), lds, s, a);
+  return hipGetLastError();
+}
+
+template <int CM>
+static hipError_t head_dispatch_q(const HeadArgs& a, hipStream_t s, bool prepare) {
+  switch (head_qmax(a.d)) {
+    case 2: return head_go<CM, 2>(a, s, prepare);
+    case 8: return head_go<CM, 8>(a, s, prepare);
+    case 16: return head_go<CM, 16>(a, s, prepare);
+    default: return head_go<CM, 32>(a, s, prepare);
+  }
+}
+
+static hipError_t head_dispatch(const HeadArgs& a, hipStream_t s, bool prepare) {
+  switch (head_cmax(a.C)) {
+    case 10: return head_dispatch_q<10>(a, s, prepare);
+    case 16: return head_dispatch_q<16>(a, s, prepare);
+    default: return head_dispatch_q<32>(a, s, prepare);
+  }
+}
+
+// The fused output layer applies when C <= 32, the hidden width is at most
+// 2048 and the padded W fits in the LDS a workgroup may use (160 KB per CU
+// on gfx950; beyond 64 KB the kernel's dynamic-LDS limit is raised first).
+bool head_prepare(int C, int d) {
+  if (C > 32 || d > HEAD_DMAX) return false;
+  if (head_lds_bytes(C, d) > 160 * 1024 - 1024) return false;
+  HeadArgs a{};
+  a.C = C;
+  a.d = d;
+  return head_dispatch(a, nullptr, true) == hipSuccess;
+}
+
+hipError_t launch_head(const HeadArgs& a, hipStream_t s) { return head_dispatch(a, s, false); }
+
+hipError_t launch_head_dw(const HeadDwArgs& a, hipStream_t s) {
+  const int blocks = a.n * ((a.d + 63) / 64);
+  switch (head_cmax(a.C)) {
+    case 10: hipLaunchKernelGGL(head_dw_kernel<10>, dim3(blocks), dim3(256), 0, s, a); break;
+    case 16: hipLaunchKernelGGL(head_dw_kernel<16>, dim3(blocks), dim3(256), 0, s, a); break;
+    default: hipLaunchKernelGGL(head_dw_kernel<32>, dim3(blocks), dim3(256), 0, s, a); break;
+  }
+  return hipGetLastError();
+}
+
+}  // namespace agn

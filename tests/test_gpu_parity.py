@@ -36,6 +36,12 @@ SMALL = [
     ("sgd_n1_lam1", (50, 70, 4), 1, 1, 130, 0.05, 3, 300, "gauss_linear", "sequential", "fp32"),
     ("wide_tiles", (96, 300, 300, 12), 5, 2, 70, 0.05, 2, 1000, "sparse_teacher2", "permutation", "fp32"),
     ("batch_of_one", (16, 8, 2), 2, 3, 1, 0.1, 3, 10, "gauss_linear", "permutation", "fp32"),
+    # output-layer paths: many classes (separate logits product + softmax kernel),
+    # a hidden width beyond the fused kernel's reach, and a fused kernel whose
+    # LDS-resident output weights exceed 64 KB
+    ("many_classes", (60, 50, 40), 3, 2, 24, 0.1, 2, 300, "gauss_linear", "permutation", "fp32"),
+    ("wide_hidden", (30, 2100, 10), 2, 2, 8, 0.02, 2, 64, "gauss_linear", "permutation", "fp32"),
+    ("big_head_lds", (50, 2000, 12), 2, 2, 16, 0.02, 2, 96, "gauss_linear", "permutation", "fp32"),
 ]
 
 
