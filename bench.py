@@ -31,7 +31,7 @@ sys.path.insert(0, ROOT)
 METRIC = "worker-samples/sec per AGN round on 1 MI355X; MFMA util % + commit HBM GB/s"
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2516.6}   # dense MFMA peaks of MI355X
-CLASSES = ["fwd", "softmax", "dx", "dw", "commit"]
+CLASSES = ["fwd", "output", "bwd", "commit"]
 
 
 def class_work(agn, g):

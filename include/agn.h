@@ -136,6 +136,11 @@ int agn_set_central(agn_ctx* ctx, const float* in);
  * variable, the start of its next round) into out (DEVICE, P floats). */
 int agn_worker_params(agn_ctx* ctx, int32_t worker, float* out);
 
+/* Copy the normalized delta worker k committed in the last round (Eq. 1:
+ * its accumulated update divided by lambda) into out (DEVICE, P floats,
+ * packed).  AGN_ESTATE before the first round. */
+int agn_debug_delta(agn_ctx* ctx, int32_t worker, float* out);
+
 /* The m sample indices worker `worker` uses at local step `step_t`, for a
  * data set of `num_samples` rows: out (DEVICE, m int64). */
 int agn_debug_batch_indices(agn_ctx* ctx, int32_t worker, int64_t step_t,
@@ -144,21 +149,23 @@ int agn_debug_batch_indices(agn_ctx* ctx, int32_t worker, int64_t step_t,
 /* ---- kernel timing ------------------------------------------------------ */
 
 /* Kernel classes, in the order a local step launches them. */
-#define AGN_K_FWD 0     /* forward product + bias + ReLU (and output logits) */
-#define AGN_K_SOFTMAX 1 /* output layer: softmax cross-entropy, loss, output
-                           gradient (with few classes also the logits and the
-                           output layer's input gradient, fused)             */
-#define AGN_K_DX 2      /* input-gradient product + ReLU mask                */
-#define AGN_K_DW 3      /* weight-gradient product + fused SGD update        */
-#define AGN_K_COMMIT 4  /* normalize + commit + pull                         */
-#define AGN_K_NUM 5
+#define AGN_K_FWD 0    /* forward products + bias + ReLU (and the logits when
+                          the output layer is not fused)                     */
+#define AGN_K_OUTPUT 1 /* output layer: softmax cross-entropy, loss, output
+                          gradient; with few classes also the logits and the
+                          output layer's input gradient, fused               */
+#define AGN_K_BWD 2    /* backward products: per layer the input-gradient
+                          product and the weight-gradient product fused with
+                          the SGD update, launched together                  */
+#define AGN_K_COMMIT 3 /* normalize + commit + pull                          */
+#define AGN_K_NUM 4
 
 /* Algorithmic work of one round attributed to a kernel class, as this
  * context launches it: flops = 2 * multiply-adds of the class's matrix
  * products; bytes = the memory traffic the class cannot avoid (for the
  * commit: central + n deltas read, n pulled copies + central written;
- * for the weight-gradient class: every parameter read and written once per
- * local step).  HOST outputs. */
+ * for the backward class: every parameter read and written once per local
+ * step, plus its bf16 shadow written in bf16 mode).  HOST outputs. */
 int agn_kernel_class_work(agn_ctx* ctx, int32_t kernel_class, double* flops,
                           double* bytes);
 

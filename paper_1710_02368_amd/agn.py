@@ -19,15 +19,14 @@ LIB_PATH = os.path.join(_PKG, "libagn.so")
 
 AGN_OK, AGN_EINVAL, AGN_ENOMEM, AGN_EHIP, AGN_ESTATE = 0, -1, -2, -3, -4
 AGN_FP32, AGN_BF16 = 0, 1
-AGN_K_FWD, AGN_K_SOFTMAX, AGN_K_DX, AGN_K_DW, AGN_K_COMMIT = range(5)
-KERNEL_CLASSES = {"fwd": AGN_K_FWD, "softmax": AGN_K_SOFTMAX, "dx": AGN_K_DX,
-                  "dw": AGN_K_DW, "commit": AGN_K_COMMIT}
+AGN_K_FWD, AGN_K_OUTPUT, AGN_K_BWD, AGN_K_COMMIT = range(4)
+KERNEL_CLASSES = {"fwd": AGN_K_FWD, "output": AGN_K_OUTPUT, "bwd": AGN_K_BWD, "commit": AGN_K_COMMIT}
 
 EXPORTED = [
     "agn_create", "agn_set_stream", "agn_round", "agn_central", "agn_loss",
     "agn_num_params", "agn_last_error", "agn_destroy", "agn_set_central",
     "agn_worker_params", "agn_debug_batch_indices", "agn_set_kernel_timing",
-    "agn_kernel_timing", "agn_kernel_class_work",
+    "agn_kernel_timing", "agn_kernel_class_work", "agn_debug_delta",
 ]
 
 
@@ -73,6 +72,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "agn_set_central": (i32, [vp, vp]),
         "agn_worker_params": (i32, [vp, i32, vp]),
         "agn_debug_batch_indices": (i32, [vp, i32, i64, i64, vp]),
+        "agn_debug_delta": (i32, [vp, i32, vp]),
         "agn_set_kernel_timing": (i32, [vp, i32, i32]),
         "agn_kernel_timing": (i32, [vp, i32, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64)]),
         "agn_kernel_class_work": (i32, [vp, i32, ctypes.POINTER(ctypes.c_double),
@@ -157,6 +157,10 @@ def agn_worker_params(ctx, worker: int, out):
     _check(load_library().agn_worker_params(ctx, int(worker), ctypes.c_void_p(out.data_ptr())), ctx)
 
 
+def agn_debug_delta(ctx, worker: int, out):
+    _check(load_library().agn_debug_delta(ctx, int(worker), ctypes.c_void_p(out.data_ptr())), ctx)
+
+
 def agn_debug_batch_indices(ctx, worker: int, step_t: int, num_samples: int, out):
     _check(load_library().agn_debug_batch_indices(ctx, int(worker), int(step_t), int(num_samples),
                                                   ctypes.c_void_p(out.data_ptr())), ctx)
@@ -225,6 +229,12 @@ class AGN:
         torch = _torch()
         out = torch.empty(self.P, dtype=torch.float32, device="cuda")
         agn_worker_params(self.ctx, k, out)
+        return out
+
+    def delta(self, k):
+        torch = _torch()
+        out = torch.empty(self.P, dtype=torch.float32, device="cuda")
+        agn_debug_delta(self.ctx, k, out)
         return out
 
     def set_central(self, vec):

@@ -232,7 +232,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     h.loss = c->loss;
     h.lam = c->lam;
     h.step = step;
-    HIP_CHECK(c, timed(c, AGN_K_SOFTMAX, [&] { return launch_head(h, c->ls); }));
+    HIP_CHECK(c, timed(c, AGN_K_OUTPUT, [&] { return launch_head(h, c->ls); }));
     HeadDwArgs w{};
     w.h = hin;
     w.ldh = ldh;
@@ -257,7 +257,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     w.eta = c->eta;
     w.lam = (float)c->lam;
     w.last = last;
-    HIP_CHECK(c, timed(c, AGN_K_DW, [&] { return launch_head_dw(w, c->ls); }));
+    HIP_CHECK(c, timed(c, AGN_K_BWD, [&] { return launch_head_dw(w, c->ls); }));
   } else {
     // softmax cross-entropy: per-row loss and the output gradient dZ_L
     SoftmaxArgs s{};
@@ -276,53 +276,56 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     s.loss = c->loss;
     s.lam = c->lam;
     s.step = step;
-    HIP_CHECK(c, timed(c, AGN_K_SOFTMAX, [&] { return launch_softmax_ce(s, c->ls); }));
+    HIP_CHECK(c, timed(c, AGN_K_OUTPUT, [&] { return launch_softmax_ce(s, c->ls); }));
   }
 
-  // backward, last layer first (the fused output layer already did layer L-1)
+  // backward, last layer first (the fused output layer already did layer L-1):
+  // per layer one launch with the input-gradient product (l >= 1) and the
+  // weight-gradient product fused with the update
   for (int l = c->use_head ? L - 2 : L - 1; l >= 0; --l) {
     const int64_t dz_ld = c->lda[l + 1], dz_st = (int64_t)m * c->lda[l + 1];
+    GemmArgs w{};  // dW_l = dZ_{l+1}^T H_l fused with the update of W_l and b_l
+    w.M = c->dims[l + 1];
+    w.N = c->dims[l];
+    w.K = m;
+    w.batch = n;
+    w.a = Operand{c->dZ[l + 1], dz_ld, dz_st, 0, 1};
+    w.b = l == 0 ? xop : Operand{c->H[l], c->lda[l], (int64_t)m * c->lda[l], 0, 1};
+    w.g = gath;
+    w.epi = EPI_DW_UPDATE;
+    w.w_src = src + c->woff[l];
+    w.w_dst = dst + c->woff[l];
+    w.w_snap = c->snap + c->woff[l];
+    w.b_src = src + c->boff[l];
+    w.b_dst = dst + c->boff[l];
+    w.b_snap = c->snap + c->boff[l];
+    w.w_dst16 = (bf && !last) ? dst16 + c->woff[l] : nullptr;
+    w.ldw = c->ldw[l];
+    w.pstride = ps;
+    w.eta = c->eta;
+    w.lam = (float)c->lam;
+    w.last = last;
     if (l >= 1) {  // dZ_l = (dZ_{l+1} W_l) * [H_l > 0]
-      GemmArgs g{};
-      g.M = m;
-      g.N = c->dims[l];
-      g.K = c->dims[l + 1];
-      g.batch = n;
-      g.a = Operand{c->dZ[l + 1], dz_ld, dz_st, 0, 1};
-      g.b = bf ? Operand{src16 + c->woff[l], c->ldw[l], ps, 0, 1} : Operand{src + c->woff[l], c->ldw[l], ps, 0, 1};
-      g.g = gath;
-      g.epi = EPI_DX_MASK;
-      g.out = c->dZ[l];
-      g.ldo = c->lda[l];
-      g.ostride = (int64_t)m * c->lda[l];
-      g.mask = c->H[l];
-      g.ldm = c->lda[l];
-      g.mstride = (int64_t)m * c->lda[l];
-      HIP_CHECK(c, timed(c, AGN_K_DX, [&] { return gemm(1, 0, g); }));
-    }
-    {  // dW_l = dZ_{l+1}^T H_l fused with the update of W_l and b_l
-      GemmArgs g{};
-      g.M = c->dims[l + 1];
-      g.N = c->dims[l];
-      g.K = m;
-      g.batch = n;
-      g.a = Operand{c->dZ[l + 1], dz_ld, dz_st, 0, 1};
-      g.b = l == 0 ? xop : Operand{c->H[l], c->lda[l], (int64_t)m * c->lda[l], 0, 1};
-      g.g = gath;
-      g.epi = EPI_DW_UPDATE;
-      g.w_src = src + c->woff[l];
-      g.w_dst = dst + c->woff[l];
-      g.w_snap = c->snap + c->woff[l];
-      g.b_src = src + c->boff[l];
-      g.b_dst = dst + c->boff[l];
-      g.b_snap = c->snap + c->boff[l];
-      g.w_dst16 = (bf && !last) ? dst16 + c->woff[l] : nullptr;
-      g.ldw = c->ldw[l];
-      g.pstride = ps;
-      g.eta = c->eta;
-      g.lam = (float)c->lam;
-      g.last = last;
-      HIP_CHECK(c, timed(c, AGN_K_DW, [&] { return gemm(0, 0, g); }));
+      GemmArgs x{};
+      x.M = m;
+      x.N = c->dims[l];
+      x.K = c->dims[l + 1];
+      x.batch = n;
+      x.a = Operand{c->dZ[l + 1], dz_ld, dz_st, 0, 1};
+      x.b = bf ? Operand{src16 + c->woff[l], c->ldw[l], ps, 0, 1} : Operand{src + c->woff[l], c->ldw[l], ps, 0, 1};
+      x.g = gath;
+      x.epi = EPI_DX_MASK;
+      x.out = c->dZ[l];
+      x.ldo = c->lda[l];
+      x.ostride = (int64_t)m * c->lda[l];
+      x.mask = c->H[l];
+      x.ldm = c->lda[l];
+      x.mstride = (int64_t)m * c->lda[l];
+      HIP_CHECK(c, timed(c, AGN_K_BWD, [&] {
+        return bf ? launch_gemm_bf16_bwd(x, w, c->ls) : launch_gemm_f32_bwd(x, w, c->ls);
+      }));
+    } else {
+      HIP_CHECK(c, timed(c, AGN_K_BWD, [&] { return gemm(0, 0, w); }));
     }
   }
   (void)dst16;
@@ -571,6 +574,18 @@ int agn_worker_params(agn_ctx* c, int32_t worker, float* out) {
   return AGN_OK;
 }
 
+int agn_debug_delta(agn_ctx* c, int32_t worker, float* out) {
+  if (int r = check_ctx(c)) return r;
+  if (!out) return fail(c, AGN_EINVAL, "out is NULL");
+  if (worker < 0 || worker >= c->n) return fail(c, AGN_EINVAL, "worker out of range");
+  if (c->rounds == 0) return fail(c, AGN_ESTATE, "no round has run yet");
+  if (int r = set_device(c)) return r;
+  const float* delta = c->buf[(c->lam - 1) & 1] + (int64_t)worker * c->P_pad;
+  HIP_CHECK(c, launch_pack(c->pack, delta, out, c->stream));
+  HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  return AGN_OK;
+}
+
 int agn_debug_batch_indices(agn_ctx* c, int32_t worker, int64_t step_t, int64_t num_samples, int64_t* out) {
   if (int r = check_ctx(c)) return r;
   if (!out) return fail(c, AGN_EINVAL, "out is NULL");
@@ -597,7 +612,7 @@ int agn_kernel_class_work(agn_ctx* c, int32_t cls, double* flops, double* bytes)
     case AGN_K_FWD:
       for (int l = 0; l < (c->use_head ? L - 1 : L); ++l) f += 2.0 * mac(l) * rows;
       break;
-    case AGN_K_SOFTMAX:
+    case AGN_K_OUTPUT:
       if (c->use_head) {
         f = 2.0 * mac(L - 1) * rows * (L >= 2 ? 2.0 : 1.0);
         b = rows * (4.0 * c->dims[L - 1] * (L >= 2 ? 2.0 : 1.0) + 4.0 * C + 8.0);
@@ -605,15 +620,13 @@ int agn_kernel_class_work(agn_ctx* c, int32_t cls, double* flops, double* bytes)
         b = rows * (4.0 * C + xb * C + 4.0);
       }
       break;
-    case AGN_K_DX:
-      for (int l = 1; l < (c->use_head ? L - 1 : L); ++l) f += 2.0 * mac(l) * rows;
-      break;
-    case AGN_K_DW:
+    case AGN_K_BWD:  // weight gradients of every layer, input gradients not done in the output kernel
       for (int l = 0; l < L; ++l) f += 2.0 * mac(l) * rows;
-      b = 8.0 * (double)c->n * c->P * c->lam;  // read + write every parameter each step
+      for (int l = 1; l < (c->use_head ? L - 1 : L); ++l) f += 2.0 * mac(l) * rows;
+      b = (c->dtype == AGN_BF16 ? 10.0 : 8.0) * (double)c->n * c->P * c->lam;
       break;
     case AGN_K_COMMIT:
-      b = 8.0 * (double)(c->n + 1) * c->P;    // central + n deltas in, n pulls + central out
+      b = 8.0 * (double)(c->n + 1) * c->P;  // central + n deltas in, n pulls + central out
       break;
   }
   *flops = f;

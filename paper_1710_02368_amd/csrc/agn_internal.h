@@ -62,6 +62,10 @@ struct GemmArgs {
 // launchers (return hipError_t of the launch)
 hipError_t launch_gemm_f32(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s);
 hipError_t launch_gemm_bf16(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s);
+// input-gradient (EPI_DX_MASK) and weight-gradient (EPI_DW_UPDATE) products of
+// one layer in one launch
+hipError_t launch_gemm_f32_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s);
+hipError_t launch_gemm_bf16_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s);
 
 struct SoftmaxArgs {
   const float* z;      // logits [n][m][ldz]

@@ -140,15 +140,20 @@ __device__ __forceinline__ void read_frag(const float* lds, int outer_off, int l
   }
 }
 
+constexpr int LDS_FLOATS = 2 * (KC_TILE > KS_TILE ? KC_TILE : KS_TILE);
+
+// One 64x64 output tile (logical tile id `logical`) of one product.
+// lds_a / lds_b: LDS_FLOATS each (two buffers of one operand tile).
 template <bool A_KC, bool B_KC, int EPI>
-__global__ __launch_bounds__(NT) void gemm_f32_kernel(GemmArgs g) {
-  __shared__ __attribute__((aligned(16))) float lds_a[2][A_KC ? KC_TILE : KS_TILE];
-  __shared__ __attribute__((aligned(16))) float lds_b[2][B_KC ? KC_TILE : KS_TILE];
+__device__ __forceinline__ void gemm_tile(const GemmArgs& g, const int logical, float* lds_a_base,
+                                          float* lds_b_base) {
+  constexpr int TA = A_KC ? KC_TILE : KS_TILE;
+  constexpr int TB_ = B_KC ? KC_TILE : KS_TILE;
+#define LDS_A(i) (lds_a_base + (i) * TA)
+#define LDS_B(i) (lds_b_base + (i) * TB_)
 
   const int tid = threadIdx.x;
   const int tm = (g.M + BM - 1) / BM, tn = (g.N + BN - 1) / BN;
-  const int nblk = tm * tn * g.batch;
-  const int logical = xcd_remap(blockIdx.x, nblk);
   const int worker = logical / (tm * tn);
   const int rem = logical % (tm * tn);
   const int tile_n = rem / tm, tile_m = rem % tm;
@@ -182,8 +187,8 @@ __global__ __launch_bounds__(NT) void gemm_f32_kernel(GemmArgs g) {
   float4 va[2], vb[2];
   la.load(0, tid, va);
   lb.load(0, tid, vb);
-  TileLoader<A_KC>::store(lds_a[0], tid, va);
-  TileLoader<B_KC>::store(lds_b[0], tid, vb);
+  TileLoader<A_KC>::store(LDS_A(0), tid, va);
+  TileLoader<B_KC>::store(LDS_B(0), tid, vb);
   __syncthreads();
 
   for (int kt = 0; kt < nk; ++kt) {
@@ -193,8 +198,8 @@ __global__ __launch_bounds__(NT) void gemm_f32_kernel(GemmArgs g) {
       lb.load((kt + 1) * BK, tid, vb);
     }
     float af[16], bf[16];
-    read_frag<A_KC>(lds_a[cur], wm * 32, li, lh, af);
-    read_frag<B_KC>(lds_b[cur], wn * 32, li, lh, bf);
+    read_frag<A_KC>(LDS_A(cur), wm * 32, li, lh, af);
+    read_frag<B_KC>(LDS_B(cur), wn * 32, li, lh, bf);
 #pragma unroll
     for (int s = 0; s < 16; s += 2) {
       acc0 = __builtin_amdgcn_mfma_f32_32x32x2f32(af[s], bf[s], acc0, 0, 0, 0);
@@ -202,11 +207,11 @@ __global__ __launch_bounds__(NT) void gemm_f32_kernel(GemmArgs g) {
     }
     if (do_bias) {
 #pragma unroll 8
-      for (int k = 0; k < BK; ++k) bsum += lds_a[cur][ks_off(k, tid)];
+      for (int k = 0; k < BK; ++k) bsum += LDS_A(cur)[ks_off(k, tid)];
     }
     if (kt + 1 < nk) {
-      TileLoader<A_KC>::store(lds_a[cur ^ 1], tid, va);
-      TileLoader<B_KC>::store(lds_b[cur ^ 1], tid, vb);
+      TileLoader<A_KC>::store(LDS_A(cur ^ 1), tid, va);
+      TileLoader<B_KC>::store(LDS_B(cur ^ 1), tid, vb);
     }
     __syncthreads();
   }
@@ -265,12 +270,48 @@ __global__ __launch_bounds__(NT) void gemm_f32_kernel(GemmArgs g) {
   }
 }
 
+#undef LDS_A
+#undef LDS_B
+
+__host__ __device__ inline int tiles_of(const GemmArgs& g) { return ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN) * g.batch; }
+
+template <bool A_KC, bool B_KC, int EPI>
+__global__ __launch_bounds__(NT) void gemm_f32_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) float lds_a[LDS_FLOATS];
+  __shared__ __attribute__((aligned(16))) float lds_b[LDS_FLOATS];
+  gemm_tile<A_KC, B_KC, EPI>(g, xcd_remap(blockIdx.x, tiles_of(g)), lds_a, lds_b);
+}
+
+// The backward products of one layer in one launch: the input-gradient tiles
+// (long K) first, then the weight-gradient tiles.  Both read dZ_{l+1}; the
+// first reads W_l from the step's source parameters, the second writes the
+// destination parameters, so they are independent.  Each range is laid out
+// over the XCDs on its own (the first range is padded to a multiple of 8
+// workgroups, the pad workgroups exit at once).
+__global__ __launch_bounds__(NT) void gemm_f32_bwd_kernel(GemmArgs dx, GemmArgs dw, int n1, int n1pad) {
+  __shared__ __attribute__((aligned(16))) float lds_a[LDS_FLOATS];
+  __shared__ __attribute__((aligned(16))) float lds_b[LDS_FLOATS];
+  const int pid = blockIdx.x;
+  if (pid < n1pad) {
+    if (pid < n1) gemm_tile<true, false, EPI_DX_MASK>(dx, xcd_remap(pid, n1), lds_a, lds_b);
+  } else {
+    const int p2 = pid - n1pad;
+    gemm_tile<false, false, EPI_DW_UPDATE>(dw, xcd_remap(p2, tiles_of(dw)), lds_a, lds_b);
+  }
+}
+
 }  // namespace
 
 template <bool A_KC, bool B_KC, int EPI>
 static hipError_t go(const GemmArgs& g, hipStream_t s) {
-  const int tm = (g.M + BM - 1) / BM, tn = (g.N + BN - 1) / BN;
-  hipLaunchKernelGGL((gemm_f32_kernel<A_KC, B_KC, EPI>), dim3(tm * tn * g.batch), dim3(NT), 0, s, g);
+  hipLaunchKernelGGL((gemm_f32_kernel<A_KC, B_KC, EPI>), dim3(tiles_of(g)), dim3(NT), 0, s, g);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_f32_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s) {
+  if (dx.epi != EPI_DX_MASK || dw.epi != EPI_DW_UPDATE) return hipErrorInvalidValue;
+  const int n1 = tiles_of(dx), n1pad = (n1 + kNumXcd - 1) / kNumXcd * kNumXcd;
+  hipLaunchKernelGGL(gemm_f32_bwd_kernel, dim3(n1pad + tiles_of(dw)), dim3(NT), 0, s, dx, dw, n1, n1pad);
   return hipGetLastError();
 }
 

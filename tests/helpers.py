@@ -41,3 +41,37 @@ def to_device(X, y):
 def require_gpu():
     import torch
     assert torch.cuda.is_available(), "a ROCm GPU is required for this test"
+
+
+def rel_fro(got, ref, dims):
+    """Per parameter tensor ||got - ref||_2 / ||ref||_2 (Frobenius), maximum
+    over the tensors.  Unlike the max-norm metric it is not dominated by the
+    localized change one flipped ReLU derivative makes."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    worst, where = 0.0, None
+    for name, a, b in tensor_slices(dims):
+        den = np.linalg.norm(ref[a:b])
+        err = np.linalg.norm(got[a:b] - ref[a:b]) / (den if den > 0 else 1.0)
+        if err > worst:
+            worst, where = err, name
+    return worst, where
+
+
+def parity_report(got, ref, dims):
+    """The full-size parity metrics of the central variable:
+    vec   ||got - ref||_inf / ||ref||_inf over the whole parameter vector
+    W     max over weight tensors of the per-tensor max-norm relative error
+    b     max over bias tensors of the per-tensor Frobenius relative error
+    """
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    vec = np.max(np.abs(got - ref)) / np.max(np.abs(ref))
+    w = b = 0.0
+    for name, a0, a1 in tensor_slices(dims):
+        d = got[a0:a1] - ref[a0:a1]
+        if name[0] == "W":
+            w = max(w, np.max(np.abs(d)) / max(np.max(np.abs(ref[a0:a1])), 1e-300))
+        else:
+            b = max(b, np.linalg.norm(d) / max(np.linalg.norm(ref[a0:a1]), 1e-300))
+    return {"vec": vec, "W": w, "b": b}
