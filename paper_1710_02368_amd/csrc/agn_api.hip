@@ -54,6 +54,7 @@ struct agn_ctx {
   float* loss = nullptr;
   int32_t* order = nullptr;
   int64_t* round_dev = nullptr;
+  float* zero = nullptr;  // 4 KB of zeros
   int64_t rounds = 0;
   int64_t N_fixed = -1;
   hipStream_t stream = nullptr;       // caller's stream (all work is ordered on it)
@@ -201,6 +202,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     g.ostride = (int64_t)m * c->lda[l + 1];
     g.bias = src + c->boff[l];
     g.bstride = ps;
+    g.zero = c->zero;
     HIP_CHECK(c, timed(c, AGN_K_FWD, [&] { return gemm(1, 1, g); }));
   }
 
@@ -305,6 +307,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     w.eta = c->eta;
     w.lam = (float)c->lam;
     w.last = last;
+    w.zero = c->zero;
     if (l >= 1) {  // dZ_l = (dZ_{l+1} W_l) * [H_l > 0]
       GemmArgs x{};
       x.M = m;
@@ -321,6 +324,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
       x.mask = c->H[l];
       x.ldm = c->lda[l];
       x.mstride = (int64_t)m * c->lda[l];
+      x.zero = c->zero;
       HIP_CHECK(c, timed(c, AGN_K_BWD, [&] {
         return bf ? launch_gemm_bf16_bwd(x, w, c->ls) : launch_gemm_f32_bwd(x, w, c->ls);
       }));
@@ -422,7 +426,8 @@ int agn_create(const agn_shapes* shapes, int32_t n, int32_t lambda, float eta, u
             dalloc(c, &c->buf[0], nps) == hipSuccess && dalloc(c, &c->buf[1], nps) == hipSuccess &&
             dalloc(c, &c->Z, (int64_t)n * c->m * c->lda[L]) == hipSuccess &&
             dalloc(c, &c->loss, (int64_t)n * lambda * c->m) == hipSuccess &&
-            dalloc(c, &c->order, n) == hipSuccess && dalloc(c, &c->round_dev, 1) == hipSuccess;
+            dalloc(c, &c->order, n) == hipSuccess && dalloc(c, &c->round_dev, 1) == hipSuccess &&
+            dalloc(c, &c->zero, 1024) == hipSuccess;
   if (ok && bf)
     ok = dalloc(c, &c->snap16, nps) == hipSuccess && dalloc(c, &c->buf16[0], nps) == hipSuccess &&
          dalloc(c, &c->buf16[1], nps) == hipSuccess;
@@ -444,6 +449,7 @@ int agn_create(const agn_shapes* shapes, int32_t n, int32_t lambda, float eta, u
   if (e == hipSuccess && bf) e = hipMemset(c->buf16[0], 0, nps * 2);
   if (e == hipSuccess && bf) e = hipMemset(c->buf16[1], 0, nps * 2);
   if (e == hipSuccess) e = hipMemset(c->round_dev, 0, 8);
+  if (e == hipSuccess) e = hipMemset(c->zero, 0, 1024 * sizeof(float));
   if (e == hipSuccess) e = hipMemset(c->loss, 0, (size_t)n * lambda * c->m * 4);
   if (e != hipSuccess) return bail(AGN_EHIP, std::string("hipMemset: ") + hipGetErrorString(e));
 

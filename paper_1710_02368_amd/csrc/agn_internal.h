@@ -57,6 +57,7 @@ struct GemmArgs {
   int64_t ldw, pstride;
   float eta, lam;
   int32_t last;
+  const float* zero;  // a zeroed page (operand reads past an edge)
 };
 
 // launchers (return hipError_t of the launch)
@@ -66,6 +67,11 @@ hipError_t launch_gemm_bf16(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s
 // one layer in one launch
 hipError_t launch_gemm_f32_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s);
 hipError_t launch_gemm_bf16_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s);
+// direct global->LDS variants of the float32 products (used when both
+// operands qualify, see gemm_f32_dl_ok)
+bool gemm_f32_dl_ok(int a_kc, int b_kc, const GemmArgs& g);
+hipError_t launch_gemm_f32_dl(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s);
+hipError_t launch_gemm_f32_dl_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s);
 
 struct SoftmaxArgs {
   const float* z;      // logits [n][m][ldz]

@@ -173,6 +173,29 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, const int logical, 
   const bool do_bias = (EPI == EPI_DW_UPDATE) && tile_n == 0 && tid < 64;
   float bsum = 0.f;
 
+  // operands of the epilogue, loaded before the K loop so that their latency
+  // hides behind it: lane holds D[i][j], j = lane%32,
+  // i = 8*(r/4) + 4*(lane/32) + r%4
+  const int col = n0 + wn * 32 + li;
+  const int64_t wo = (int64_t)worker * g.pstride;
+  float pre[16], pre2[16];
+  if (EPI == EPI_DX_MASK || EPI == EPI_DW_UPDATE) {
+    const float* mk = EPI == EPI_DX_MASK ? reinterpret_cast<const float*>(g.mask) + (int64_t)worker * g.mstride
+                                         : nullptr;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = m0 + wm * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
+      const bool ok = row < g.M && col < g.N;
+      if (EPI == EPI_DX_MASK) {
+        pre[r] = ok ? mk[(int64_t)row * g.ldm + col] : 0.f;
+      } else {
+        const int64_t e = wo + (int64_t)row * g.ldw + col;
+        pre[r] = ok ? g.w_src[e] : 0.f;
+        pre2[r] = (ok && g.last) ? g.w_snap[e] : 0.f;
+      }
+    }
+  }
+
   // two independent accumulation chains (even / odd MFMA of each step)
   f32x16 acc0, acc1;
 #pragma unroll
@@ -217,8 +240,6 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, const int logical, 
   }
   f32x16 acc = acc0 + acc1;
 
-  // epilogue: lane holds D[i][j], j = lane%32, i = 8*(r/4) + 4*(lane/32) + r%4
-  const int col = n0 + wn * 32 + li;
   if (EPI == EPI_FWD_RELU || EPI == EPI_FWD_LINEAR) {
     if (col < g.N) {
       float* out = reinterpret_cast<float*>(g.out) + (int64_t)worker * g.ostride;
@@ -236,26 +257,21 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, const int logical, 
   } else if (EPI == EPI_DX_MASK) {
     if (col < g.N) {
       float* out = reinterpret_cast<float*>(g.out) + (int64_t)worker * g.ostride;
-      const float* mk = reinterpret_cast<const float*>(g.mask) + (int64_t)worker * g.mstride;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = m0 + wm * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
-        if (row < g.M) {
-          const int64_t e = (int64_t)row * g.ldo + col;
-          out[e] = mk[(int64_t)row * g.ldm + col] > 0.f ? acc[r] : 0.f;
-        }
+        if (row < g.M) out[(int64_t)row * g.ldo + col] = pre[r] > 0.f ? acc[r] : 0.f;
       }
     }
   } else {  // EPI_DW_UPDATE: rows are output units o, columns input units i
-    const int64_t wo = (int64_t)worker * g.pstride;
     if (col < g.N) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = m0 + wm * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
         if (row < g.M) {
           const int64_t e = wo + (int64_t)row * g.ldw + col;
-          const float nw = g.w_src[e] - g.eta * acc[r];
-          g.w_dst[e] = g.last ? (nw - g.w_snap[e]) / g.lam : nw;
+          const float nw = pre[r] - g.eta * acc[r];
+          g.w_dst[e] = g.last ? (nw - pre2[r]) / g.lam : nw;
         }
       }
     }
@@ -316,6 +332,7 @@ hipError_t launch_gemm_f32_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream
 }
 
 hipError_t launch_gemm_f32(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s) {
+  if (a_kc && b_kc && gemm_f32_dl_ok(a_kc, b_kc, g)) return launch_gemm_f32_dl(a_kc, b_kc, g, s);
   if (a_kc && b_kc && g.epi == EPI_FWD_RELU) return go<true, true, EPI_FWD_RELU>(g, s);
   if (a_kc && b_kc && g.epi == EPI_FWD_LINEAR) return go<true, true, EPI_FWD_LINEAR>(g, s);
   if (a_kc && !b_kc && g.epi == EPI_DX_MASK) return go<true, false, EPI_DX_MASK>(g, s);
