@@ -1,8 +1,8 @@
 // Batched float32 products with direct global->LDS operand loads
 // (global_load_lds_dwordx4 on gfx950): operand tiles travel from memory into
-// LDS without passing through registers, two K steps ahead of their use, and
-// the fragments of the next K step are read from LDS while the MFMAs of the
-// current one run.
+// LDS without passing through registers, three K steps ahead of their use,
+// and the fragments of the next K step are read from LDS while the MFMAs of
+// the current one run.
 //
 // Tile: 64x64 outputs per workgroup of 4 waves; wave (wm, wn) owns a 32x32
 // block as 2x2 blocks of v_mfma_f32_16x16x4_f32; K in steps of 32.  In one
@@ -22,36 +22,87 @@
 // LDS layout of one operand tile (64 x 32 floats = 512 chunks of 16 bytes;
 // a wave's load instruction fills 64 consecutive chunks, lane l chunk l):
 //   K-contiguous (rows = outer index, 8 chunks of 4 k per row):
-//     chunk (r, q) at r*8 + (q ^ ((r>>1)&7)), so the 16 rows that one
-//     16-byte read touches per cycle cover all 64 banks once;
+//     chunk (r, q) at r*8 + (q ^ key(r)), key(r) = (r&7) ^ ((r>>3)&1): the
+//     rows of 8 consecutive lanes of a 16-byte read fall in 8 distinct
+//     16-byte bank groups modulo 128 bytes, and those of 16 consecutive
+//     lanes in 16 distinct groups modulo 256 bytes;
 //   K-strided (rows = k, 16 chunks of 4 outer per row):
 //     chunk (k, c) at k*16 + (c ^ (8*((k>>3)&1))), so rows k and k+8, read
 //     together by lane groups 0 and 1, land in opposite halves of the banks.
 // Each lane loads the global 16 bytes that belong in its slot; lanes past an
 // edge read a zero page, so edge tiles hold exact zeros.
+//
+// Two schedules:
+//   * forward and input-gradient products (K = layer width, tens of K
+//     steps): one output tile per workgroup;
+//   * weight-gradient products (K = mini-batch, a few K steps per tile):
+//     persistent workgroups walk a list of tiles and the operand loads run
+//     on across tile boundaries, so a tile's first steps load while the
+//     previous tile computes and stores.  The weight (and, on a round's last
+//     step, snapshot) tile of the epilogue is loaded into LDS by the same
+//     direct loads, so that every wait on the load counter has a known
+//     count.
 #include "device_common.h"
 
 namespace agn {
 namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
-constexpr int NT = 256, TM = 64, BKD = 32;
-constexpr int TILE_F = TM * BKD;                 // floats per operand tile
-constexpr int STAGE_F = 2 * TILE_F;              // A and B
-constexpr int GTAB = 1024;                       // gathered K-strided rows: offset table
+constexpr int NT = 256, TM = 64, BKD = 32, NS = 4;  // NS: LDS stages
+constexpr int TILE_F = TM * BKD;                     // floats per operand tile
+constexpr int STAGE_F = 2 * TILE_F;                  // A and B
+constexpr int EPI_F = TM * TM;                       // floats of one epilogue operand tile
+constexpr int NWG_DW = 512;                          // persistent weight-gradient workgroups (2 per CU)
 
-__device__ __forceinline__ int kc_slot(int r, int q) { return r * 8 + (q ^ ((r >> 1) & 7)); }
+__device__ __forceinline__ int kc_key(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+__device__ __forceinline__ int kc_slot(int r, int q) { return r * 8 + (q ^ kc_key(r)); }
 __device__ __forceinline__ int ks_slot(int k, int c) { return k * 16 + (c ^ (((k >> 3) & 1) << 3)); }
 
-// vmcnt(n) without waiting on the other counters (gfx9 encoding)
-#define WAIT_VM(n) __builtin_amdgcn_s_waitcnt(((n) & 0xF) | ((((n) >> 4) & 3) << 14) | (0x7 << 4) | (0xF << 8))
-// lgkmcnt(0) alone
-#define WAIT_LGKM0() __builtin_amdgcn_s_waitcnt(0xC07F)
+// The direct loads, the barrier and the waits on their counter are written
+// as inline assembly with a memory clobber: the compiler neither moves LDS
+// reads across them nor adds waits of its own for the loads (it cannot tell
+// which LDS stage a load writes, and would wait for all of them); the waits
+// below count the load instructions exactly.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
 
-// One operand's tile loads: this wave issues slots [64j, 64j+64) for
-// j = 2*wave and 2*wave+1 (two load instructions per operand per K step).
+// LDS byte offset of a pointer into a __shared__ array
+__device__ __forceinline__ uint32_t lds_off(const float* p) {
+  return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) float*)p);
+}
+
+// one 64-lane direct load: lane l's 16 bytes from src to LDS byte offset
+// lds + 16*l (lds wave-uniform, in M0; one wait state between the M0 write
+// and the load that reads it)
+__device__ __forceinline__ void fire(const float* src, uint32_t lds) {
+  const uint32_t m0 = __builtin_amdgcn_readfirstlane(lds);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(m0), "v"(src)
+               : "memory", "m0");
+}
+
+// at most N of this wave's vector memory loads still in flight
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+__device__ __forceinline__ void wait_lgkm0() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ void barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+#pragma clang diagnostic pop
+
+// Slot of lane `lane` in load instruction j of a K-strided tile: k row and
+// 16-byte column chunk.
+__device__ __forceinline__ int ks_row(int j, int lane) { return 4 * j + lane / 16; }
+__device__ __forceinline__ int ks_chunk(int j, int lane) {
+  return (lane % 16) ^ (((ks_row(j, lane) >> 3) & 1) << 3);
+}
+
+// One-tile schedule: one operand's tile loads.  This wave fills slots
+// [64j, 64j+64) for j = 2*wave and 2*wave+1 (two load instructions per
+// operand per K step).  K-contiguous operands may be gathered (data-set rows
+// of the first layer); K-strided ones are not.
 template <bool KC>
 struct DirectLoader {
   const float* base;
@@ -59,58 +110,41 @@ struct DirectLoader {
   int64_t ld;
   int outer0, outer_n, K;
   const float* rowp[2];      // KC: the lane's two rows (null past the edge)
-  const int64_t* tab;        // KS gathered: row offsets (elements) in LDS, or null
-  int gather;
-  int64_t worker, t, mb, S;
 
   __device__ void init(const Operand& op, const Gather& g, const float* zp, int64_t w, int o0, int on, int k,
-                       int wave, int lane, const int64_t* table) {
+                       int wave, int lane) {
     base = reinterpret_cast<const float*>(op.ptr) + w * op.wstride;
     zero = zp;
     ld = op.ld;
     outer0 = o0;
     outer_n = on;
     K = k;
-    gather = op.gather;
-    worker = w;
-    mb = g.mb;
-    S = g.S;
-    t = gather ? gather_step(g) : 0;
-    tab = table;
     if (KC) {
+      const int64_t t = op.gather ? gather_step(g) : 0;
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int r = 8 * (2 * wave + u) + lane / 8;
         const int o = o0 + r;
         int64_t ri = o;
-        if (gather && o < on) ri = batch_row(worker, t, mb, S, o);
+        if (op.gather && o < on) ri = batch_row(w, t, g.mb, g.S, o);
         rowp[u] = o < on ? base + ri * ld : nullptr;
       }
     }
   }
 
-  __device__ void issue(int k0, float* stage_tile, int wave, int lane) const {
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      const int j = 2 * wave + u;
-      const float* src;
-      if (KC) {
-        const int r = 8 * j + lane / 8;
-        const int q = (lane % 8) ^ ((r >> 1) & 7);
-        const int k = k0 + 4 * q;
-        src = (rowp[u] && k < K) ? rowp[u] + k : zero;
-      } else {
-        const int kl = 4 * j + lane / 16;
-        const int c = (lane % 16) ^ (((kl >> 3) & 1) << 3);
-        const int kk = k0 + kl, o = outer0 + 4 * c;
-        if (kk < K && o < outer_n) {
-          const int64_t roff = gather ? (tab ? tab[kk] : batch_row(worker, t, mb, S, kk) * ld) : (int64_t)kk * ld;
-          src = base + roff + o;
-        } else {
-          src = zero;
-        }
-      }
-      __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)(stage_tile + 256 * j), 16, 0, 0);
+  // source of this lane's 16 bytes in load instruction u (0, 1) of the K
+  // step starting at k0; the zero page past an edge (also for k0 >= K)
+  __device__ const float* src(int k0, int u, int wave, int lane) const {
+    const int j = 2 * wave + u;
+    if (KC) {
+      const int r = 8 * j + lane / 8;
+      const int q = (lane % 8) ^ kc_key(r);
+      const int k = k0 + 4 * q;
+      return (rowp[u] && k < K) ? rowp[u] + k : zero;
+    } else {
+      const int kk = k0 + ks_row(j, lane), o = outer0 + 4 * ks_chunk(j, lane);
+      if (kk >= K || o >= outer_n) return zero;
+      return base + (int64_t)kk * ld + o;
     }
   }
 };
@@ -151,53 +185,50 @@ __device__ __forceinline__ void read_frags(const float* stage, int wm, int wn, i
   frag<B_KC>(stage + TILE_F, wn * 32, li, lg, f.b);
 }
 
-__device__ __forceinline__ void mfmas(const Frags& f, f32x4 (&acc)[2][2]) {
+struct Lanes {
+  int wave, lane, wm, wn, li, lg;
+};
+
+// K step: the fragments of this step are in `cur`; the loads of the next
+// NS-1 steps are in flight.  Wait until every wave has read `cur` and the
+// next step's loads have landed (VM: load instructions this wave may leave
+// in flight, those issued after the next step's), then, interleaved with the
+// 32 MFMAs, read the next step's fragments from `rd` into `nxt` and start the
+// loads `src` of the step NS ahead into `wr` (the stage this step came from).
+// Loads past the end of K read the zero page, so every step has the same
+// shape and the MFMAs, LDS reads and loads form one basic block.
+template <bool A_KC, bool B_KC, int VM>
+__device__ __forceinline__ void k_step(const Lanes& q, const Frags& cur, Frags& nxt, const float* rd, float* wr,
+                                       const float* const (&src)[4], f32x4 (&acc)[2][2], float (&bsum)[2]) {
+  wait_lgkm0();
+  wait_vm<VM>();
+  barrier();
+  read_frags<A_KC, B_KC>(rd, q.wm, q.wn, q.li, q.lg, nxt);
+  const uint32_t wa = lds_off(wr) + 4 * 256 * (2 * q.wave);
+  fire(src[0], wa);
+  fire(src[1], wa + 4 * 256);
+  fire(src[2], wa + 4 * TILE_F);
+  fire(src[3], wa + 4 * (TILE_F + 256));
 #pragma unroll
   for (int s = 0; s < 8; ++s)
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
       for (int bj = 0; bj < 2; ++bj)
-        acc[bi][bj] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.a[bi][s], f.b[bj][s], acc[bi][bj], 0, 0, 0);
-}
-
-template <bool A_KC, bool B_KC>
-struct Pipe {
-  const DirectLoader<A_KC>* la;
-  const DirectLoader<B_KC>* lb;
-  int nk, wave, lane, wm, wn, li, lg;
-  bool do_bias;
-};
-
-// K step kt: the fragments of step kt are in `cur`.  Wait until every wave
-// has read them and the loads of step kt+1 have landed, read step kt+1's
-// fragments from `rd` into `nxt`, start the loads of step kt+3 into `wr`
-// (the stage step kt came from), then run step kt's MFMAs.
-template <bool A_KC, bool B_KC>
-__device__ __forceinline__ void k_step(const Pipe<A_KC, B_KC>& p, int kt, const Frags& cur, Frags& nxt,
-                                       const float* rd, float* wr, f32x4 (&acc)[2][2], float (&bsum)[2]) {
-  // (unconditional, so that `cur` counts as landed on every path into the
-  // MFMAs and the compiler adds no wait of its own there)
-  WAIT_LGKM0();
-  if (kt + 1 < p.nk) {
-    if (kt + 2 < p.nk)
-      WAIT_VM(4);
-    else
-      WAIT_VM(0);
-    __builtin_amdgcn_s_barrier();
-    read_frags<A_KC, B_KC>(rd, p.wm, p.wn, p.li, p.lg, nxt);
-    if (kt + 3 < p.nk) {
-      p.la->issue((kt + 3) * BKD, wr, p.wave, p.lane);
-      p.lb->issue((kt + 3) * BKD, wr + TILE_F, p.wave, p.lane);
-    }
-  }
-  mfmas(cur, acc);
-  if (p.do_bias) {  // A is dZ^T (K-strided): this lane's two columns over its 8 k
+        acc[bi][bj] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.a[bi][s], cur.b[bj][s], acc[bi][bj], 0, 0, 0);
+  // bias gradient (used by the weight-gradient product, where A = dZ^T is
+  // K-strided): this lane's two columns over its 8 k
 #pragma unroll
-    for (int s = 0; s < 8; ++s) {
-      bsum[0] += cur.a[0][s];
-      bsum[1] += cur.a[1][s];
-    }
+  for (int s = 0; s < 8; ++s) {
+    bsum[0] += cur.a[0][s];
+    bsum[1] += cur.a[1][s];
+  }
+  // issue order: the LDS reads spread between the MFMAs
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // LDS read
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
   }
 }
 
@@ -205,65 +236,60 @@ __device__ __forceinline__ void k_step(const Pipe<A_KC, B_KC>& p, int kt, const 
 template <bool KC>
 __device__ __forceinline__ int tile_idx(int b, int x) { return KC ? 16 * b + x : 2 * x + b; }
 
+__host__ __device__ inline int tiles_dl(const GemmArgs& g) { return ((g.M + TM - 1) / TM) * ((g.N + TM - 1) / TM) * g.batch; }
+
+struct TileCoord {
+  int worker, m0, n0, tile_n;
+};
+
+__device__ __forceinline__ TileCoord coord_of(const GemmArgs& g, int logical) {
+  const int tm = (g.M + TM - 1) / TM, tn = (g.N + TM - 1) / TM;
+  TileCoord c;
+  c.worker = logical / (tm * tn);
+  const int rem = logical % (tm * tn);
+  c.tile_n = rem / tm;
+  c.m0 = (rem % tm) * TM;
+  c.n0 = c.tile_n * TM;
+  return c;
+}
+
+// ---------------------------------------------------------------------------
+// One-tile schedule: forward (A = H or gathered data rows, B = W, both
+// K-contiguous) and input-gradient (A = dZ K-contiguous, B = W K-strided).
+
 template <bool A_KC, bool B_KC, int EPI>
 __device__ __forceinline__ void tile_dl(const GemmArgs& g, const int logical, float* st0, float* st1, float* st2,
-                                        int64_t* tab) {
+                                        float* st3) {
+  static_assert(EPI != EPI_DW_UPDATE, "weight-gradient tiles use the persistent schedule");
   const int tid = threadIdx.x;
-  const int tm = (g.M + TM - 1) / TM, tn = (g.N + TM - 1) / TM;
-  const int worker = logical / (tm * tn);
-  const int rem = logical % (tm * tn);
-  const int tile_n = rem / tm, tile_m = rem % tm;
-  const int m0 = tile_m * TM, n0 = tile_n * TM;
-  const int lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
-  const int li = lane & 15, lg = lane >> 4;
-  const int64_t wo = (int64_t)worker * g.pstride;
-  const int rbase = m0 + wm * 32, cbase = n0 + wn * 32;
+  const TileCoord c = coord_of(g, logical);
+  const int worker = c.worker, m0 = c.m0, n0 = c.n0;
+  const Lanes q{tid >> 6, tid & 63, (tid >> 6) >> 1, (tid >> 6) & 1, tid & 15, (tid & 63) >> 4};
+  const int rbase = m0 + q.wm * 32, cbase = n0 + q.wn * 32;
   // accumulator (bi, bj, r) sits at row rbase + tile_idx<A_KC>(bi, 4*lg + r),
   // column cbase + tile_idx<B_KC>(bj, li)
 
-  // operands of the epilogue first (oldest in the memory queue), so the K
-  // loop's counted waits cover them
-  float pre[2][2][4], pre2[2][2][4];
-  if (EPI == EPI_DX_MASK || EPI == EPI_DW_UPDATE) {
-    const float* mk = EPI == EPI_DX_MASK ? reinterpret_cast<const float*>(g.mask) + (int64_t)worker * g.mstride
-                                         : nullptr;
+  // mask of the input-gradient epilogue first (oldest in the memory queue),
+  // so the K loop's counted waits cover it
+  float pre[2][2][4];
+  if (EPI == EPI_DX_MASK) {
+    const float* mk = reinterpret_cast<const float*>(g.mask) + (int64_t)worker * g.mstride;
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
 #pragma unroll
         for (int bj = 0; bj < 2; ++bj) {
-          const int row = rbase + tile_idx<A_KC>(bi, 4 * lg + r), col = cbase + tile_idx<B_KC>(bj, li);
-          const bool ok = row < g.M && col < g.N;
-          if (EPI == EPI_DX_MASK) {
-            pre[bi][bj][r] = ok ? mk[(int64_t)row * g.ldm + col] : 0.f;
-          } else {
-            const int64_t e = wo + (int64_t)row * g.ldw + col;
-            pre[bi][bj][r] = ok ? g.w_src[e] : 0.f;
-            pre2[bi][bj][r] = (ok && g.last) ? g.w_snap[e] : 0.f;
-          }
+          const int row = rbase + tile_idx<A_KC>(bi, 4 * q.lg + r), col = cbase + tile_idx<B_KC>(bj, q.li);
+          pre[bi][bj][r] = (row < g.M && col < g.N) ? mk[(int64_t)row * g.ldm + col] : 0.f;
         }
-  }
-
-  // gathered K-strided operand (data rows of the first layer's weight
-  // gradient): row offsets once per workgroup
-  const bool tabA = !A_KC && g.a.gather && g.K <= GTAB, tabB = !B_KC && g.b.gather && g.K <= GTAB;
-  if (tabA || tabB) {
-    const Operand& op = tabA ? g.a : g.b;
-    const int64_t ts = gather_step(g.g);
-    for (int k = tid; k < g.K; k += NT) tab[k] = batch_row(worker, ts, g.g.mb, g.g.S, k) * op.ld;
-    __syncthreads();
   }
 
   DirectLoader<A_KC> la;
   DirectLoader<B_KC> lb;
-  la.init(g.a, g.g, g.zero, worker, m0, g.M, g.K, wave, lane, tabA ? tab : nullptr);
-  lb.init(g.b, g.g, g.zero, worker, n0, g.N, g.K, wave, lane, tabB ? tab : nullptr);
+  la.init(g.a, g.g, g.zero, worker, m0, g.M, g.K, q.wave, q.lane);
+  lb.init(g.b, g.g, g.zero, worker, n0, g.N, g.K, q.wave, q.lane);
 
-  // bias gradient of the weight-gradient product: the waves of the first
-  // column tile with wn = 0 sum their A fragments (A = dZ^T)
-  const bool do_bias = (EPI == EPI_DW_UPDATE) && tile_n == 0 && wn == 0;
   float bsum[2] = {0.f, 0.f};
   f32x4 acc[2][2];
 #pragma unroll
@@ -272,59 +298,43 @@ __device__ __forceinline__ void tile_dl(const GemmArgs& g, const int logical, fl
     for (int bj = 0; bj < 2; ++bj) acc[bi][bj] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int nk = (g.K + BKD - 1) / BKD;
-  // steps 0..2 in flight (4 load instructions per wave per step), then the
+  // steps 0..3 in flight (4 load instructions per wave per step), then the
   // fragments of step 0
-  la.issue(0, st0, wave, lane);
-  lb.issue(0, st0 + TILE_F, wave, lane);
-  if (nk > 1) {
-    la.issue(BKD, st1, wave, lane);
-    lb.issue(BKD, st1 + TILE_F, wave, lane);
+  {
+    float* stg[NS] = {st0, st1, st2, st3};
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const uint32_t wa = lds_off(stg[s]) + 4 * 256 * (2 * q.wave);
+      fire(la.src(s * BKD, 0, q.wave, q.lane), wa);
+      fire(la.src(s * BKD, 1, q.wave, q.lane), wa + 4 * 256);
+      fire(lb.src(s * BKD, 0, q.wave, q.lane), wa + 4 * TILE_F);
+      fire(lb.src(s * BKD, 1, q.wave, q.lane), wa + 4 * (TILE_F + 256));
+    }
   }
-  if (nk > 2) {
-    la.issue(2 * BKD, st2, wave, lane);
-    lb.issue(2 * BKD, st2 + TILE_F, wave, lane);
-    WAIT_VM(8);
-  } else if (nk > 1) {
-    WAIT_VM(4);
-  } else {
-    WAIT_VM(0);
-  }
-  __builtin_amdgcn_s_barrier();
+  wait_vm<4 * (NS - 1)>();
+  barrier();
   Frags f0, f1;
-  read_frags<A_KC, B_KC>(st0, wm, wn, li, lg, f0);
+  read_frags<A_KC, B_KC>(st0, q.wm, q.wn, q.li, q.lg, f0);
 
-  // stage of step kt: kt % 3; fragment set: kt % 2
-  const Pipe<A_KC, B_KC> p{&la, &lb, nk, wave, lane, wm, wn, li, lg, do_bias};
-  for (int kt = 0; kt < nk; kt += 6) {
-    k_step(p, kt, f0, f1, st1, st0, acc, bsum);
-    if (kt + 1 < nk) k_step(p, kt + 1, f1, f0, st2, st1, acc, bsum);
-    if (kt + 2 < nk) k_step(p, kt + 2, f0, f1, st0, st2, acc, bsum);
-    if (kt + 3 < nk) k_step(p, kt + 3, f1, f0, st1, st0, acc, bsum);
-    if (kt + 4 < nk) k_step(p, kt + 4, f0, f1, st2, st1, acc, bsum);
-    if (kt + 5 < nk) k_step(p, kt + 5, f1, f0, st0, st2, acc, bsum);
+  auto step = [&](int kt, const Frags& cur, Frags& nxt, const float* rd, float* wr) {
+    const int k0 = (kt + NS) * BKD;
+    const float* const src[4] = {la.src(k0, 0, q.wave, q.lane), la.src(k0, 1, q.wave, q.lane),
+                                 lb.src(k0, 0, q.wave, q.lane), lb.src(k0, 1, q.wave, q.lane)};
+    k_step<A_KC, B_KC, 4 * (NS - 2)>(q, cur, nxt, rd, wr, src, acc, bsum);
+  };
+  // stage of step kt: kt % 4; fragment set: kt % 2
+  const int nk4 = nk & ~3;
+  for (int kt = 0; kt < nk4; kt += 4) {
+    step(kt, f0, f1, st1, st0);
+    step(kt + 1, f1, f0, st2, st1);
+    step(kt + 2, f0, f1, st3, st2);
+    step(kt + 3, f1, f0, st0, st3);
   }
-
-  if (EPI == EPI_DW_UPDATE && do_bias) {
-    // lane groups 1..3 hold partial sums of the same columns as group 0:
-    // add them in a fixed order
-    float tot[2];
-#pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const float p1 = __shfl(bsum[b], li + 16), p2 = __shfl(bsum[b], li + 32), p3 = __shfl(bsum[b], li + 48);
-      tot[b] = ((bsum[b] + p1) + p2) + p3;
-    }
-    if (lg == 0) {
-#pragma unroll
-      for (int b = 0; b < 2; ++b) {
-        const int o = rbase + 2 * li + b;
-        if (o < g.M) {
-          const int64_t e = wo + o;
-          const float nb = g.b_src[e] - g.eta * tot[b];
-          g.b_dst[e] = g.last ? (nb - g.b_snap[e]) / g.lam : nb;
-        }
-      }
-    }
-  }
+  if (nk4 < nk) step(nk4, f0, f1, st1, st0);
+  if (nk4 + 1 < nk) step(nk4 + 1, f1, f0, st2, st1);
+  if (nk4 + 2 < nk) step(nk4 + 2, f0, f1, st3, st2);
+  // loads of the steps past the end (zero page) still write LDS
+  wait_vm<0>();
 
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi)
@@ -332,50 +342,306 @@ __device__ __forceinline__ void tile_dl(const GemmArgs& g, const int logical, fl
     for (int r = 0; r < 4; ++r)
 #pragma unroll
       for (int bj = 0; bj < 2; ++bj) {
-        const int row = rbase + tile_idx<A_KC>(bi, 4 * lg + r), col = cbase + tile_idx<B_KC>(bj, li);
+        const int row = rbase + tile_idx<A_KC>(bi, 4 * q.lg + r), col = cbase + tile_idx<B_KC>(bj, q.li);
         if (row >= g.M || col >= g.N) continue;
         const float v = acc[bi][bj][r];
+        float* out = reinterpret_cast<float*>(g.out) + (int64_t)worker * g.ostride;
         if (EPI == EPI_FWD_RELU || EPI == EPI_FWD_LINEAR) {
-          float* out = reinterpret_cast<float*>(g.out) + (int64_t)worker * g.ostride;
           float z = v + g.bias[(int64_t)worker * g.bstride + col];
           if (EPI == EPI_FWD_RELU) z = z > 0.f ? z : 0.f;
           out[(int64_t)row * g.ldo + col] = z;
-        } else if (EPI == EPI_DX_MASK) {
-          float* out = reinterpret_cast<float*>(g.out) + (int64_t)worker * g.ostride;
+        } else {  // EPI_DX_MASK
           out[(int64_t)row * g.ldo + col] = pre[bi][bj][r] > 0.f ? v : 0.f;
-        } else {  // EPI_DW_UPDATE: rows are output units o, columns input units i
-          const int64_t e = wo + (int64_t)row * g.ldw + col;
-          const float nw = pre[bi][bj][r] - g.eta * v;
-          g.w_dst[e] = g.last ? (nw - pre2[bi][bj][r]) / g.lam : nw;
         }
       }
 }
 
-__host__ __device__ inline int tiles_dl(const GemmArgs& g) { return ((g.M + TM - 1) / TM) * ((g.N + TM - 1) / TM) * g.batch; }
+// ---------------------------------------------------------------------------
+// Persistent schedule of the weight-gradient product
+//   dW = dZ^T H (A = dZ [K][M] and B = H [K][N], both K-strided; for the
+//   first layer H is the gathered data rows),
+// fused with the SGD update of the weights (and the bias from the column
+// sums of dZ): W_dst = W_src - eta*dW, on a round's last step
+// (W_src - eta*dW - W_snap) / lambda.
 
-// three LDS stages as separate objects, so that the compiler can tell the
+// Tiles of workgroup `wg` of `nwg` (nwg a multiple of 8): workgroup wg runs
+// on XCD wg % 8 (round-robin dispatch); each XCD owns one contiguous range of
+// logical tiles (tiles of one worker share its dZ and H in that XCD's L2),
+// walked by its nwg/8 workgroups with stride nwg/8.
+struct TileList {
+  int first, stride, count;
+  __device__ int logical(int i) const { return first + i * stride; }
+};
+
+__device__ __forceinline__ TileList tiles_of_wg(int T, int wg, int nwg) {
+  const int xcd = wg % kNumXcd, slot = wg / kNumXcd, per = nwg / kNumXcd;
+  const int q = (T + kNumXcd - 1) / kNumXcd;
+  const int lo = xcd * q, hi = min(T, lo + q);
+  TileList t;
+  t.first = lo + slot;
+  t.stride = per;
+  t.count = t.first < hi ? (hi - t.first + per - 1) / per : 0;
+  return t;
+}
+
+// Per-lane part of the K-strided operand loads of the weight-gradient tiles.
+struct DwLoads {
+  const float* a_base;   // dZ of worker 0
+  const float* b_base;   // H of worker 0 (gathered: the data set)
+  const float* zero;
+  int64_t a_ld, a_ws, b_ld, b_ws;
+  int M, N, K, b_gather;
+  int64_t S, tb;         // gathered rows: worker*S + (tb + k) mod S
+  int kl[2], cc[2];      // the lane's k row and column chunk in its two instructions
+  // current issue-side tile
+  int64_t a_off, b_off;  // worker offsets
+  int m0, n0, worker;
+  bool live;
+
+  __device__ void set_tile(const GemmArgs& g, const TileList& tl, int i) {
+    live = i < tl.count;
+    const TileCoord c = coord_of(g, live ? tl.logical(i) : 0);
+    worker = c.worker;
+    m0 = c.m0;
+    n0 = c.n0;
+    a_off = (int64_t)worker * a_ws;
+    b_off = (int64_t)worker * b_ws;
+  }
+  __device__ const float* a_src(int k0, int u) const {
+    const int kk = k0 + kl[u], o = m0 + 4 * cc[u];
+    if (!live || kk >= K || o >= M) return zero;
+    return a_base + a_off + (int64_t)kk * a_ld + o;
+  }
+  __device__ const float* b_src(int k0, int u) const {
+    const int kk = k0 + kl[u], o = n0 + 4 * cc[u];
+    if (!live || kk >= K || o >= N) return zero;
+    int64_t row = kk;
+    if (b_gather) {
+      const int64_t x = tb + kk;
+      row = (int64_t)worker * S + (x >= S ? x - S : x);
+    }
+    return b_base + b_off + row * b_ld + o;
+  }
+};
+
+// Epilogue operand tile(s) of tile `c` into LDS: rows m0.., columns n0..
+// of W_src (and W_snap), row-major 64 x 64.  This wave: rows 4j .. 4j+3 for
+// j = 4*wave .. 4*wave+3, lane l row 4j + l/16, columns 4*(l%16) .. +3.
+template <bool LAST>
+__device__ __forceinline__ void fire_epi(const GemmArgs& g, const TileCoord& c, float* epi, float* epi2,
+                                         const Lanes& q) {
+  const int64_t wo = (int64_t)c.worker * g.pstride;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int j = 4 * q.wave + u;
+    const int row = c.m0 + 4 * j + q.lane / 16, col = c.n0 + 4 * (q.lane % 16);
+    const bool ok = row < g.M && col < g.N;
+    const int64_t e = wo + (int64_t)row * g.ldw + col;
+    fire(ok ? g.w_src + e : g.zero, lds_off(epi) + 4 * 256 * j);
+    if (LAST) fire(ok ? g.w_snap + e : g.zero, lds_off(epi2) + 4 * 256 * j);
+  }
+}
+
+template <bool LAST>
+__device__ __forceinline__ void dw_tiles(const GemmArgs& g, int wg, int nwg, float* st0, float* st1, float* st2,
+                                         float* st3, float* epi, float* epi2) {
+  constexpr int EPN = LAST ? 8 : 4;  // epilogue load instructions per wave and tile
+  const TileList tl = tiles_of_wg(tiles_dl(g), wg, nwg);
+  if (tl.count == 0) return;
+  const int tid = threadIdx.x;
+  const Lanes q{tid >> 6, tid & 63, (tid >> 6) >> 1, (tid >> 6) & 1, tid & 15, (tid & 63) >> 4};
+  const int nk = (g.K + BKD - 1) / BKD;  // >= NS (checked on the host)
+
+  DwLoads ld;
+  ld.a_base = reinterpret_cast<const float*>(g.a.ptr);
+  ld.b_base = reinterpret_cast<const float*>(g.b.ptr);
+  ld.zero = g.zero;
+  ld.a_ld = g.a.ld;
+  ld.a_ws = g.a.wstride;
+  ld.b_ld = g.b.ld;
+  ld.b_ws = g.b.wstride;
+  ld.M = g.M;
+  ld.N = g.N;
+  ld.K = g.K;
+  ld.b_gather = g.b.gather;
+  ld.S = g.g.S;
+  ld.tb = g.b.gather ? (gather_step(g.g) * g.g.mb) % g.g.S : 0;
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    ld.kl[u] = ks_row(2 * q.wave + u, q.lane);
+    ld.cc[u] = ks_chunk(2 * q.wave + u, q.lane);
+  }
+
+  // prologue: steps 0..NS-1 (all in tile 0, since nk >= NS), then the
+  // epilogue operands of tile 0
+  ld.set_tile(g, tl, 0);
+  {
+    float* stg[NS] = {st0, st1, st2, st3};
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const uint32_t wa = lds_off(stg[s]) + 4 * 256 * (2 * q.wave);
+      fire(ld.a_src(s * BKD, 0), wa);
+      fire(ld.a_src(s * BKD, 1), wa + 4 * 256);
+      fire(ld.b_src(s * BKD, 0), wa + 4 * TILE_F);
+      fire(ld.b_src(s * BKD, 1), wa + 4 * (TILE_F + 256));
+    }
+  }
+  fire_epi<LAST>(g, coord_of(g, tl.logical(0)), epi, epi2, q);
+  wait_vm<4 * (NS - 1) + EPN>();
+  barrier();
+  Frags f0, f1;
+  read_frags<false, false>(st0, q.wm, q.wn, q.li, q.lg, f0);
+
+  float bsum[2] = {0.f, 0.f};
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj) acc[bi][bj] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // step counter: tile i, step kt of that tile; the issue side runs NS steps
+  // ahead: tile i2, step kt2
+  int i = 0, kt = 0, i2 = 0, kt2 = NS;
+  if (kt2 >= nk) {  // (nk == NS)
+    kt2 -= nk;
+    ++i2;
+    ld.set_tile(g, tl, i2);
+  }
+
+  auto step = [&](const Frags& cur, Frags& nxt, const float* rd, float* wr) {
+    const int k0 = kt2 * BKD;
+    const float* const src[4] = {ld.a_src(k0, 0), ld.a_src(k0, 1), ld.b_src(k0, 0), ld.b_src(k0, 1)};
+    // the epilogue loads of tile i were issued after the step loads up to
+    // step kt = NS-1 of tile i: until then they sit behind the next step's
+    if (kt <= NS - 2)
+      k_step<false, false, 4 * (NS - 2) + EPN>(q, cur, nxt, rd, wr, src, acc, bsum);
+    else
+      k_step<false, false, 4 * (NS - 2)>(q, cur, nxt, rd, wr, src, acc, bsum);
+    // advance the issue side
+    if (++kt2 == nk) {
+      kt2 = 0;
+      ld.set_tile(g, tl, ++i2);
+    }
+    if (++kt < nk) return;
+    // ---- tile i complete: epilogue (its operands in LDS since step NS-1)
+    const TileCoord c = coord_of(g, tl.logical(i));
+    const int64_t wo = (int64_t)c.worker * g.pstride;
+    // lane holds rows tr = wm*32 + 2*(4*lg + r) + bi, column pairs
+    // tc = wn*32 + 2*li + (0, 1)
+    float2 nw[2][4];
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int tr = q.wm * 32 + 2 * (4 * q.lg + r) + bi, tc = q.wn * 32 + 2 * q.li;
+        const float2 ws = *reinterpret_cast<const float2*>(epi + tr * TM + tc);
+        float2 v{ws.x - g.eta * acc[bi][0][r], ws.y - g.eta * acc[bi][1][r]};
+        if (LAST) {
+          const float2 sn = *reinterpret_cast<const float2*>(epi2 + tr * TM + tc);
+          v.x = (v.x - sn.x) / g.lam;
+          v.y = (v.y - sn.y) / g.lam;
+        }
+        nw[bi][r] = v;
+      }
+    const bool full = c.m0 + TM <= g.M && c.n0 + TM <= g.N;
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = c.m0 + q.wm * 32 + 2 * (4 * q.lg + r) + bi, col = c.n0 + q.wn * 32 + 2 * q.li;
+        float* dst = g.w_dst + wo + (int64_t)row * g.ldw + col;
+        if (full) {
+          *reinterpret_cast<float2*>(dst) = nw[bi][r];
+        } else if (row < g.M && col < g.N) {  // (N even: col+1 < N too)
+          *reinterpret_cast<float2*>(dst) = nw[bi][r];
+        }
+      }
+    if (c.tile_n == 0 && q.wn == 0) {
+      // lane groups 1..3 hold partial sums of the same columns as group 0:
+      // add them in a fixed order
+      float tot[2];
+#pragma unroll
+      for (int b = 0; b < 2; ++b) {
+        const float p1 = __shfl(bsum[b], q.li + 16), p2 = __shfl(bsum[b], q.li + 32),
+                    p3 = __shfl(bsum[b], q.li + 48);
+        tot[b] = ((bsum[b] + p1) + p2) + p3;
+      }
+      if (q.lg == 0) {
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+          const int o = c.m0 + q.wm * 32 + 2 * q.li + b;
+          if (o < g.M) {
+            const int64_t e = wo + o;
+            const float nb = g.b_src[e] - g.eta * tot[b];
+            g.b_dst[e] = LAST ? (nb - g.b_snap[e]) / g.lam : nb;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int bj = 0; bj < 2; ++bj) acc[bi][bj] = f32x4{0.f, 0.f, 0.f, 0.f};
+    bsum[0] = bsum[1] = 0.f;
+    kt = 0;
+    if (++i < tl.count) {
+      // every wave has read this tile's epilogue operands: load the next's
+      wait_lgkm0();
+      barrier();
+      fire_epi<LAST>(g, coord_of(g, tl.logical(i)), epi, epi2, q);
+    }
+  };
+
+  // stage of step s: s % 4; fragment set: s % 2
+  const int total = tl.count * nk, total4 = total & ~3;
+  for (int s = 0; s < total4; s += 4) {
+    step(f0, f1, st1, st0);
+    step(f1, f0, st2, st1);
+    step(f0, f1, st3, st2);
+    step(f1, f0, st0, st3);
+  }
+  if (total4 < total) step(f0, f1, st1, st0);
+  if (total4 + 1 < total) step(f1, f0, st2, st1);
+  if (total4 + 2 < total) step(f0, f1, st3, st2);
+  // loads of the steps past the end (zero page) still write LDS
+  wait_vm<0>();
+}
+
+// four LDS stages as separate objects, so that the compiler can tell the
 // loads into one stage from the fragment reads of another
-#define DL_LDS                                                   \
+#define DL_STAGES                                                \
   __shared__ __attribute__((aligned(16))) float st0[STAGE_F];     \
   __shared__ __attribute__((aligned(16))) float st1[STAGE_F];     \
   __shared__ __attribute__((aligned(16))) float st2[STAGE_F];     \
-  __shared__ __attribute__((aligned(16))) int64_t tab[GTAB];
+  __shared__ __attribute__((aligned(16))) float st3[STAGE_F];
+#define DL_EPI(LAST)                                                  \
+  __shared__ __attribute__((aligned(16))) float epi[(LAST ? 2 : 1) * EPI_F]; \
+  float* epi2 = epi + (LAST ? EPI_F : 0);  /* (snapshot tile: last step only) */
 
 template <bool A_KC, bool B_KC, int EPI>
 __global__ __launch_bounds__(NT) void gemm_f32_dl_kernel(GemmArgs g) {
-  DL_LDS
-  tile_dl<A_KC, B_KC, EPI>(g, xcd_remap(blockIdx.x, tiles_dl(g)), st0, st1, st2, tab);
+  DL_STAGES
+  tile_dl<A_KC, B_KC, EPI>(g, xcd_remap(blockIdx.x, tiles_dl(g)), st0, st1, st2, st3);
 }
 
-// input-gradient tiles, then weight-gradient tiles of one layer (see the
-// register-staged kernel for the layout over the XCDs)
+template <bool LAST>
+__global__ __launch_bounds__(NT) void gemm_f32_dl_dw_kernel(GemmArgs g) {
+  DL_STAGES
+  DL_EPI(LAST)
+  dw_tiles<LAST>(g, blockIdx.x, gridDim.x, st0, st1, st2, st3, epi, epi2);
+}
+
+// input-gradient tiles (one per workgroup, spread evenly over the XCDs),
+// then the persistent weight-gradient workgroups of the same layer
+template <bool LAST>
 __global__ __launch_bounds__(NT) void gemm_f32_dl_bwd_kernel(GemmArgs dx, GemmArgs dw, int n1, int n1pad) {
-  DL_LDS
+  DL_STAGES
+  DL_EPI(LAST)
   const int pid = blockIdx.x;
   if (pid < n1pad) {
-    if (pid < n1) tile_dl<true, false, EPI_DX_MASK>(dx, xcd_remap(pid, n1), st0, st1, st2, tab);
+    if (pid < n1) tile_dl<true, false, EPI_DX_MASK>(dx, xcd_remap(pid, n1), st0, st1, st2, st3);
   } else {
-    tile_dl<false, false, EPI_DW_UPDATE>(dw, xcd_remap(pid - n1pad, tiles_dl(dw)), st0, st1, st2, tab);
+    dw_tiles<LAST>(dw, pid - n1pad, gridDim.x - n1pad, st0, st1, st2, st3, epi, epi2);
   }
 }
 
@@ -384,13 +650,34 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 // the operand can be staged with 16-byte direct loads
 bool operand_ok(const Operand& op, bool kc, int outer_n, int K) {
   if (!op.vec || !aligned16(op.ptr) || op.ld % 4 || op.wstride % 4 || K % 4) return false;
-  return kc || outer_n % 4 == 0;
+  return kc || (outer_n % 4 == 0 && !op.gather);
+}
+
+// weight-gradient product: K-strided operands (B may be gathered when the
+// batch fits in a shard), at least NS K steps, 16-byte epilogue rows
+bool dw_ok(const GemmArgs& g) {
+  if (g.epi != EPI_DW_UPDATE || !g.zero) return false;
+  const Operand& a = g.a;
+  const Operand& b = g.b;
+  if (!a.vec || !b.vec || a.gather || !aligned16(a.ptr) || !aligned16(b.ptr)) return false;
+  if (a.ld % 4 || a.wstride % 4 || b.ld % 4 || b.wstride % 4) return false;
+  if (g.M % 4 || g.N % 4 || (g.K + BKD - 1) / BKD < NS) return false;
+  if (b.gather && g.K > g.g.S) return false;
+  if (!aligned16(g.w_src) || !aligned16(g.w_dst) || g.ldw % 4 || g.pstride % 4) return false;
+  return !g.last || aligned16(g.w_snap);
+}
+
+int dw_grid(const GemmArgs& g) {
+  const int t = (tiles_dl(g) + kNumXcd - 1) / kNumXcd * kNumXcd;
+  return t < NWG_DW ? t : NWG_DW;
 }
 
 }  // namespace
 
 bool gemm_f32_dl_ok(int a_kc, int b_kc, const GemmArgs& g) {
-  return g.zero && operand_ok(g.a, a_kc, g.M, g.K) && operand_ok(g.b, b_kc, g.N, g.K);
+  if (!a_kc && !b_kc) return dw_ok(g);
+  return g.zero && a_kc && (g.epi == EPI_DX_MASK ? !b_kc : b_kc) && operand_ok(g.a, true, g.M, g.K) &&
+         operand_ok(g.b, b_kc, g.N, g.K);
 }
 
 hipError_t launch_gemm_f32_dl(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s) {
@@ -401,16 +688,32 @@ hipError_t launch_gemm_f32_dl(int a_kc, int b_kc, const GemmArgs& g, hipStream_t
     hipLaunchKernelGGL((gemm_f32_dl_kernel<true, true, EPI_FWD_LINEAR>), grid, block, 0, s, g);
   else if (a_kc && !b_kc && g.epi == EPI_DX_MASK)
     hipLaunchKernelGGL((gemm_f32_dl_kernel<true, false, EPI_DX_MASK>), grid, block, 0, s, g);
-  else if (!a_kc && !b_kc && g.epi == EPI_DW_UPDATE)
-    hipLaunchKernelGGL((gemm_f32_dl_kernel<false, false, EPI_DW_UPDATE>), grid, block, 0, s, g);
-  else
+  else if (!a_kc && !b_kc && g.epi == EPI_DW_UPDATE) {
+    if (g.last)
+      hipLaunchKernelGGL(gemm_f32_dl_dw_kernel<true>, dim3(dw_grid(g)), block, 0, s, g);
+    else
+      hipLaunchKernelGGL(gemm_f32_dl_dw_kernel<false>, dim3(dw_grid(g)), block, 0, s, g);
+  } else {
     return hipErrorInvalidValue;
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_f32_dl_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s) {
   const int n1 = tiles_dl(dx), n1pad = (n1 + kNumXcd - 1) / kNumXcd * kNumXcd;
-  hipLaunchKernelGGL(gemm_f32_dl_bwd_kernel, dim3(n1pad + tiles_dl(dw)), dim3(NT), 0, s, dx, dw, n1, n1pad);
+  // as many persistent weight-gradient workgroups as input-gradient tiles
+  // (an input-gradient tile of a 1000-wide layer carries the MFMA work of
+  // eight weight-gradient tiles), at least 8 and at most one per
+  // weight-gradient tile
+  int n2 = n1pad < NWG_DW ? n1pad : NWG_DW;
+  const int t2 = dw_grid(dw);
+  if (n2 > t2) n2 = t2;
+  if (n2 < kNumXcd) n2 = kNumXcd;
+  const dim3 grid(n1pad + n2), block(NT);
+  if (dw.last)
+    hipLaunchKernelGGL(gemm_f32_dl_bwd_kernel<true>, grid, block, 0, s, dx, dw, n1, n1pad);
+  else
+    hipLaunchKernelGGL(gemm_f32_dl_bwd_kernel<false>, grid, block, 0, s, dx, dw, n1, n1pad);
   return hipGetLastError();
 }
 
