@@ -31,7 +31,7 @@ sys.path.insert(0, ROOT)
 METRIC = "worker-samples/sec per AGN round on 1 MI355X; MFMA util % + commit HBM GB/s"
 PEAK_HBM_GBS = 8000.0
 PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2516.6}   # dense MFMA peaks of MI355X
-CLASSES = ["fwd", "output", "bwd", "commit"]
+CLASSES = ["fwd", "output", "output_dw", "bwd", "dw_first", "commit"]
 
 
 def class_work(agn, g):
@@ -41,8 +41,20 @@ def class_work(agn, g):
     out = {}
     for c in CLASSES:
         f, b = agn.agn_kernel_class_work(g.ctx, agn.KERNEL_CLASSES[c])
-        out[c] = ("flop", f) if f > 0 else ("byte", b)
+        out[c] = {"flops": f, "bytes": b}
     return out
+
+
+def bound_of(w, dtype):
+    """A class of matrix products is MFMA-bound when its algorithmic
+    intensity reaches the ridge point (peak FLOP/s over peak bytes/s), else
+    bound by HBM; classes without products are HBM-bound."""
+    if w["flops"] <= 0:
+        return "hbm"
+    if w["bytes"] <= 0:
+        return "mfma"
+    ridge = PEAK_TFLOPS[dtype] * 1e12 / (PEAK_HBM_GBS * 1e9)
+    return "mfma" if w["flops"] / w["bytes"] >= ridge else "hbm"
 
 
 def cpu_baseline(wl, X, y, orders, budget_s=12.0):
@@ -159,12 +171,16 @@ def main():
     for c in CLASSES:
         ms, cnt = agn.agn_kernel_timing(g.ctx, agn.KERNEL_CLASSES[c])
         agn.agn_set_kernel_timing(g.ctx, agn.KERNEL_CLASSES[c], False)
-        kind, amount = work[c]
-        per_round_ms = ms / prof_rounds
-        rate = amount / (per_round_ms * 1e-3) if per_round_ms > 0 else 0.0
-        breakdown[c] = {"ms_per_round": round(per_round_ms, 4), "launches_per_round": cnt // prof_rounds,
-                        ("TFLOP/s" if kind == "flop" else "GB/s"): round(rate / (1e12 if kind == "flop" else 1e9), 2)}
-    dominant = max(CLASSES, key=lambda c: breakdown[c]["ms_per_round"])
+        if cnt == 0:
+            continue
+        per_round_s = ms * 1e-3 / prof_rounds
+        e = {"ms_per_round": round(per_round_s * 1e3, 4), "launches_per_round": cnt // prof_rounds}
+        if work[c]["flops"] > 0:
+            e["TFLOP/s"] = round(work[c]["flops"] / per_round_s / 1e12, 2)
+        if work[c]["bytes"] > 0:
+            e["GB/s"] = round(work[c]["bytes"] / per_round_s / 1e9, 1)
+        breakdown[c] = e
+    dominant = max(breakdown, key=lambda c: breakdown[c]["ms_per_round"])
 
     # timed region: K rounds, replaying the captured round graph (the product path)
     for i in range(2):
@@ -194,25 +210,25 @@ def main():
     torch.cuda.synchronize()
 
     value = args.steps * wl.worker_samples_per_round / dt
-    kind, amount = work[dominant]
-    per_launch = amount * kt_rounds / max(dom_cnt, 1)
+    wd = work[dominant]
+    bound = bound_of(wd, wl.dtype)
+    launches_per_round = max(dom_cnt, 1) / kt_rounds
     avg_s = dom_ms * 1e-3 / max(dom_cnt, 1)
-    if kind == "flop":
+    if bound == "mfma":
+        per_launch = wd["flops"] / launches_per_round
         achieved = per_launch / avg_s / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": PEAK_TFLOPS[wl.dtype],
-                "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS[wl.dtype], 4),
-                "traffic": stored_traffic(wl.name, dominant),
-                "kernel_class": dominant, "avg_launch_us": round(avg_s * 1e6, 2),
-                "algorithmic_per_launch": per_launch, "launches": dom_cnt}
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_TFLOPS[wl.dtype], 4)}
     else:
+        per_launch = wd["bytes"] / launches_per_round
         achieved = per_launch / avg_s / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": stored_traffic(wl.name, dominant),
-                "kernel_class": dominant,
-                "avg_launch_us": round(avg_s * 1e6, 2), "algorithmic_per_launch": per_launch,
-                "launches": dom_cnt}
+                "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roof.update({"traffic": stored_traffic(wl.name, dominant), "kernel_class": dominant,
+                 "avg_launch_us": round(avg_s * 1e6, 2), "algorithmic_per_launch": per_launch,
+                 "launches": dom_cnt})
     c_avg = c_ms * 1e-3 / max(c_cnt, 1)
-    commit_gbs = work["commit"][1] / c_avg / 1e9
+    commit_gbs = work["commit"]["bytes"] / c_avg / 1e9
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "worker-samples/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(dt * 1e3 / args.steps, 4),
@@ -225,7 +241,7 @@ def main():
         "commit_roofline": {"bound": "hbm", "achieved": round(commit_gbs, 1), "peak": PEAK_HBM_GBS,
                             "unit": "GB/s", "frac": round(commit_gbs / PEAK_HBM_GBS, 4),
                             "avg_launch_us": round(c_avg * 1e6, 2),
-                            "algorithmic_per_launch": work["commit"][1],
+                            "algorithmic_per_launch": work["commit"]["bytes"],
                             "traffic": stored_traffic(wl.name, "commit")},
         "round_mfma_util": round(wl.flops_per_round / (dt / args.steps) / 1e12 / PEAK_TFLOPS[wl.dtype], 4),
         "kernels": breakdown,

@@ -148,24 +148,32 @@ int agn_debug_batch_indices(agn_ctx* ctx, int32_t worker, int64_t step_t,
 
 /* ---- kernel timing ------------------------------------------------------ */
 
-/* Kernel classes, in the order a local step launches them. */
-#define AGN_K_FWD 0    /* forward products + bias + ReLU (and the logits when
-                          the output layer is not fused)                     */
-#define AGN_K_OUTPUT 1 /* output layer: softmax cross-entropy, loss, output
-                          gradient; with few classes also the logits and the
-                          output layer's input gradient, fused               */
-#define AGN_K_BWD 2    /* backward products: per layer the input-gradient
-                          product and the weight-gradient product fused with
-                          the SGD update, launched together                  */
-#define AGN_K_COMMIT 3 /* normalize + commit + pull                          */
-#define AGN_K_NUM 4
+/* Kernel classes, in the order a local step launches them; each class is
+ * one kernel (in float32 mode). */
+#define AGN_K_FWD 0       /* forward products + bias + ReLU (and the logits
+                             when the output layer is not fused)             */
+#define AGN_K_OUTPUT 1    /* output layer: softmax cross-entropy, loss, output
+                             gradient; with few classes also the logits and
+                             the output layer's input gradient, fused        */
+#define AGN_K_OUTPUT_DW 2 /* fused output layer only: its weight gradient
+                             with the SGD update                             */
+#define AGN_K_BWD 3       /* hidden layers l >= 1, one launch per layer: the
+                             input-gradient product and the weight-gradient
+                             product fused with the SGD update               */
+#define AGN_K_DW_FIRST 4  /* first layer: weight-gradient product (rows
+                             gathered from the data set) fused with the SGD
+                             update                                          */
+#define AGN_K_COMMIT 5    /* normalize + commit + pull                       */
+#define AGN_K_NUM 6
 
 /* Algorithmic work of one round attributed to a kernel class, as this
  * context launches it: flops = 2 * multiply-adds of the class's matrix
  * products; bytes = the memory traffic the class cannot avoid (for the
  * commit: central + n deltas read, n pulled copies + central written;
- * for the backward class: every parameter read and written once per local
- * step, plus its bf16 shadow written in bf16 mode).  HOST outputs. */
+ * for the classes with the SGD update: the parameters they update read and
+ * written once per local step, plus their bf16 shadow written in bf16
+ * mode; for the output layer: its activations read and gradients written).
+ * HOST outputs. */
 int agn_kernel_class_work(agn_ctx* ctx, int32_t kernel_class, double* flops,
                           double* bytes);
 

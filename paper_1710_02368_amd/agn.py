@@ -19,8 +19,9 @@ LIB_PATH = os.path.join(_PKG, "libagn.so")
 
 AGN_OK, AGN_EINVAL, AGN_ENOMEM, AGN_EHIP, AGN_ESTATE = 0, -1, -2, -3, -4
 AGN_FP32, AGN_BF16 = 0, 1
-AGN_K_FWD, AGN_K_OUTPUT, AGN_K_BWD, AGN_K_COMMIT = range(4)
-KERNEL_CLASSES = {"fwd": AGN_K_FWD, "output": AGN_K_OUTPUT, "bwd": AGN_K_BWD, "commit": AGN_K_COMMIT}
+AGN_K_FWD, AGN_K_OUTPUT, AGN_K_OUTPUT_DW, AGN_K_BWD, AGN_K_DW_FIRST, AGN_K_COMMIT = range(6)
+KERNEL_CLASSES = {"fwd": AGN_K_FWD, "output": AGN_K_OUTPUT, "output_dw": AGN_K_OUTPUT_DW, "bwd": AGN_K_BWD,
+                  "dw_first": AGN_K_DW_FIRST, "commit": AGN_K_COMMIT}
 
 EXPORTED = [
     "agn_create", "agn_set_stream", "agn_round", "agn_central", "agn_loss",

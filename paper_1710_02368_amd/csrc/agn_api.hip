@@ -259,7 +259,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     w.eta = c->eta;
     w.lam = (float)c->lam;
     w.last = last;
-    HIP_CHECK(c, timed(c, AGN_K_BWD, [&] { return launch_head_dw(w, c->ls); }));
+    HIP_CHECK(c, timed(c, AGN_K_OUTPUT_DW, [&] { return launch_head_dw(w, c->ls); }));
   } else {
     // softmax cross-entropy: per-row loss and the output gradient dZ_L
     SoftmaxArgs s{};
@@ -329,7 +329,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
         return bf ? launch_gemm_bf16_bwd(x, w, c->ls) : launch_gemm_f32_bwd(x, w, c->ls);
       }));
     } else {
-      HIP_CHECK(c, timed(c, AGN_K_BWD, [&] { return gemm(0, 0, w); }));
+      HIP_CHECK(c, timed(c, AGN_K_DW_FIRST, [&] { return gemm(0, 0, w); }));
     }
   }
   (void)dst16;
@@ -613,6 +613,8 @@ int agn_kernel_class_work(agn_ctx* c, int32_t cls, double* flops, double* bytes)
   auto mac = [&](int l) { return (double)c->dims[l] * c->dims[l + 1]; };
   const double C = c->dims[L];
   const double xb = c->dtype == AGN_BF16 ? 2.0 : 4.0;
+  // updated parameters: read + write per local step (+ bf16 shadow write)
+  const double upd = (c->dtype == AGN_BF16 ? 10.0 : 8.0) * (double)c->n * c->lam;
   double f = 0.0, b = 0.0;
   switch (cls) {
     case AGN_K_FWD:
@@ -626,10 +628,23 @@ int agn_kernel_class_work(agn_ctx* c, int32_t cls, double* flops, double* bytes)
         b = rows * (4.0 * C + xb * C + 4.0);
       }
       break;
-    case AGN_K_BWD:  // weight gradients of every layer, input gradients not done in the output kernel
-      for (int l = 0; l < L; ++l) f += 2.0 * mac(l) * rows;
-      for (int l = 1; l < (c->use_head ? L - 1 : L); ++l) f += 2.0 * mac(l) * rows;
-      b = (c->dtype == AGN_BF16 ? 10.0 : 8.0) * (double)c->n * c->P * c->lam;
+    case AGN_K_OUTPUT_DW:
+      if (c->use_head) {
+        f = 2.0 * mac(L - 1) * rows;
+        b = upd * (mac(L - 1) + C);
+      }
+      break;
+    case AGN_K_BWD:  // hidden layers not done in the output kernels
+      for (int l = 1; l < (c->use_head ? L - 1 : L); ++l) {
+        f += 4.0 * mac(l) * rows;
+        b += upd * (mac(l) + c->dims[l + 1]);
+      }
+      break;
+    case AGN_K_DW_FIRST:
+      if (!(c->use_head && L == 1)) {
+        f = 2.0 * mac(0) * rows;
+        b = upd * (mac(0) + c->dims[1]);
+      }
       break;
     case AGN_K_COMMIT:
       b = 8.0 * (double)(c->n + 1) * c->P;  // central + n deltas in, n pulls + central out

@@ -18,7 +18,7 @@
 namespace agn {
 namespace {
 
-constexpr int HEAD_WAVE_ROWS = 2;                  // rows a wave processes together
+constexpr int HEAD_WAVE_ROWS = 1;                  // rows a wave processes together
 constexpr int HEAD_ROWS = 4 * HEAD_WAVE_ROWS;       // rows per workgroup
 constexpr int HEAD_DMAX = 2048;                     // hidden width limit
 
@@ -163,13 +163,18 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
 }
 
 // Output-layer weight gradient + update.  Workgroup = (worker, 64 input
-// units); lane owns input unit i, the 4 waves split the m rows (row j goes
-// to wave j % 4) and their partial sums are added in wave order.
+// units) of 8 waves; lane owns input unit i, wave w takes rows j = w mod 8
+// (16 rows in flight per wave) and the 8 partial sums are added in wave
+// order.  The bias sum over the m rows is split over 16 row groups per class
+// and added in group order.
 constexpr int HDW_CHUNK = 128;  // rows of dZ staged in LDS at a time
+constexpr int HDW_WAVES = 8;
+constexpr int HDW_BG = 16;      // bias row groups
 template <int CMAX>
-__global__ __launch_bounds__(256) void head_dw_kernel(HeadDwArgs a) {
+__global__ __launch_bounds__(64 * HDW_WAVES) void head_dw_kernel(HeadDwArgs a) {
   __shared__ float dzs[HDW_CHUNK * CMAX];
-  __shared__ float part[4][CMAX][64];
+  __shared__ float part[HDW_WAVES][CMAX][64];
+  __shared__ float bpart[HDW_BG][CMAX];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int blocks_per_worker = (a.d + 63) / 64;
   const int k = blockIdx.x / blocks_per_worker;
@@ -183,32 +188,34 @@ __global__ __launch_bounds__(256) void head_dw_kernel(HeadDwArgs a) {
   float acc[CMAX];
 #pragma unroll
   for (int c = 0; c < CMAX; ++c) acc[c] = 0.f;
+  // bias: thread (group, class) for tid < HDW_BG*CMAX
+  const int bg = tid / CMAX, bc = tid % CMAX;
   float bsum = 0.f;
   for (int j0 = 0; j0 < a.m; j0 += HDW_CHUNK) {
     const int rows = min(HDW_CHUNK, a.m - j0);
     __syncthreads();
-    for (int e = tid; e < rows * CMAX; e += 256) {
+    for (int e = tid; e < rows * CMAX; e += 64 * HDW_WAVES) {
       const int r = e / CMAX, c = e - r * CMAX;
       dzs[e] = c < C ? dzb[(int64_t)(j0 + r) * a.lddz + c] : 0.f;
     }
     __syncthreads();
-    if (ib == 0 && tid < C)
-      for (int r = 0; r < rows; ++r) bsum += dzs[r * CMAX + tid];
+    if (ib == 0 && bg < HDW_BG)
+      for (int r = bg; r < rows; r += HDW_BG) bsum += dzs[r * CMAX + bc];
     int r = wave;
-    for (; r + 28 < rows; r += 32) {   // 8 rows per wave in flight
-      float hv[8];
+    for (; r + 15 * HDW_WAVES < rows; r += 16 * HDW_WAVES) {   // 16 rows per wave in flight
+      float hv[16];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int j = j0 + r + 4 * u;
+      for (int u = 0; u < 16; ++u) {
+        const int j = j0 + r + HDW_WAVES * u;
         const int64_t row = a.gather ? batch_row(k, t, a.g.mb, a.g.S, j) : j;
         hv[u] = hb[row * a.ldh + ic];
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u)
+      for (int u = 0; u < 16; ++u)
 #pragma unroll
-        for (int c = 0; c < CMAX; ++c) acc[c] += dzs[(r + 4 * u) * CMAX + c] * hv[u];
+        for (int c = 0; c < CMAX; ++c) acc[c] += dzs[(r + HDW_WAVES * u) * CMAX + c] * hv[u];
     }
-    for (; r < rows; r += 4) {
+    for (; r < rows; r += HDW_WAVES) {
       const int j = j0 + r;
       const int64_t row = a.gather ? batch_row(k, t, a.g.mb, a.g.S, j) : j;
       const float hv = hb[row * a.ldh + ic];
@@ -218,10 +225,13 @@ __global__ __launch_bounds__(256) void head_dw_kernel(HeadDwArgs a) {
   }
 #pragma unroll
   for (int c = 0; c < CMAX; ++c) part[wave][c][lane] = acc[c];
+  if (ib == 0 && bg < HDW_BG) bpart[bg][bc] = bsum;
   __syncthreads();
   const int64_t wo = (int64_t)k * a.pstride;
-  for (int c = wave; c < C; c += 4) {
-    const float g = ((part[0][c][lane] + part[1][c][lane]) + part[2][c][lane]) + part[3][c][lane];
+  for (int c = wave; c < C; c += HDW_WAVES) {
+    float g = part[0][c][lane];
+#pragma unroll
+    for (int w = 1; w < HDW_WAVES; ++w) g += part[w][c][lane];
     if (i < a.d) {
       const int64_t e = wo + (int64_t)c * a.ldw + i;
       const float nw = a.w_src[e] - a.eta * g;
@@ -229,8 +239,11 @@ __global__ __launch_bounds__(256) void head_dw_kernel(HeadDwArgs a) {
     }
   }
   if (ib == 0 && tid < C) {
+    float gb = bpart[0][tid];
+#pragma unroll
+    for (int q = 1; q < HDW_BG; ++q) gb += bpart[q][tid];
     const int64_t e = wo + tid;
-    const float nb = a.b_src[e] - a.eta * bsum;
+    const float nb = a.b_src[e] - a.eta * gb;
     a.b_dst[e] = a.last ? (nb - a.b_snap[e]) / a.lam : nb;
   }
 }
@@ -293,9 +306,9 @@ hipError_t launch_head(const HeadArgs& a, hipStream_t s) { return head_dispatch(
 hipError_t launch_head_dw(const HeadDwArgs& a, hipStream_t s) {
   const int blocks = a.n * ((a.d + 63) / 64);
   switch (head_cmax(a.C)) {
-    case 10: hipLaunchKernelGGL(head_dw_kernel<10>, dim3(blocks), dim3(256), 0, s, a); break;
-    case 16: hipLaunchKernelGGL(head_dw_kernel<16>, dim3(blocks), dim3(256), 0, s, a); break;
-    default: hipLaunchKernelGGL(head_dw_kernel<32>, dim3(blocks), dim3(256), 0, s, a); break;
+    case 10: hipLaunchKernelGGL(head_dw_kernel<10>, dim3(blocks), dim3(64 * HDW_WAVES), 0, s, a); break;
+    case 16: hipLaunchKernelGGL(head_dw_kernel<16>, dim3(blocks), dim3(64 * HDW_WAVES), 0, s, a); break;
+    default: hipLaunchKernelGGL(head_dw_kernel<32>, dim3(blocks), dim3(64 * HDW_WAVES), 0, s, a); break;
   }
   return hipGetLastError();
 }
