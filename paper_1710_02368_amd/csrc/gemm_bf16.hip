@@ -3,12 +3,12 @@
 //
 // A workgroup of 4 waves owns a 128x128 output tile of one worker; each wave
 // owns a 64x64 quarter as 2x2 MFMA blocks (64 accumulator registers).  K is
-// consumed 32 at a time through double-buffered LDS tiles.  Every operand is
-// staged in LDS K-contiguous ([outer][k]) so each MFMA operand fragment is
-// one 16-byte LDS read: K-contiguous operands are copied as they are,
-// K-strided ones (the N-contiguous weights of the input-gradient product and
-// both operands of the weight-gradient product) are transposed on their way
-// into LDS.
+// consumed 32 at a time through double-buffered LDS tiles, each operand in
+// the layout it has in memory.  An MFMA operand fragment is 16 bytes per
+// lane: one 16-byte LDS read from a K-contiguous tile ([outer][k]), two
+// transposing LDS reads (ds_read_b64_tr_b16) from a K-strided one
+// ([k][outer]: the N-contiguous weights of the input-gradient product and
+// both operands of the weight-gradient product).
 //
 // Epilogues: forward  H = bf16(relu(acc + b)) (logits stay float32);
 //            input gradient  dZ = bf16(acc * [H > 0]);
@@ -16,7 +16,9 @@
 //            the bf16 shadow of the new W written alongside (the operand of
 //            the next step's products); b <- b - eta * sum over rows of the
 //            bf16 dZ.  On a round's last step the normalized displacement
-//            (W_new - W_pulled) / lambda is stored instead.
+//            (W_new - W_pulled) / lambda is stored instead.  The weight-
+//            gradient epilogue goes through LDS so that the master weights
+//            stream in 16-byte chunks.
 #include "device_common.h"
 
 namespace agn {
@@ -27,9 +29,15 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 constexpr int TB = 128;          // tile edge (M and N)
 constexpr int BKH = 32;          // k per step
-constexpr int LDK = BKH + 8;     // LDS row stride (bf16 elements) of a [outer][k] tile
-constexpr int TILE = TB * LDK;   // bf16 elements per operand tile
+constexpr int LDK = BKH + 8;     // LDS row stride (bf16 elements) of a K-contiguous [outer][k] tile
+constexpr int LDS_KS = TB + 32;  // LDS row stride (bf16 elements) of a K-strided [k][outer] tile
+constexpr int TILE = TB * LDK;   // bf16 elements per operand tile (either layout)
+static_assert(BKH * LDS_KS <= TILE, "K-strided tile fits the tile buffer");
 constexpr int NT = 256;
+constexpr int EPI_LD = TB + 4;   // LDS row stride (floats) of the weight-gradient epilogue tile
+// LDS per workgroup: the two double-buffered operand tiles, or (after the
+// K loop) the 128x128 float32 accumulator tile of the weight-gradient epilogue
+constexpr int LDS_BYTES = (4 * TILE * 2 > TB * EPI_LD * 4) ? 4 * TILE * 2 : TB * EPI_LD * 4;
 
 __device__ __forceinline__ uint4 load8(const uint16_t* p, int valid, int vec) {
   if (valid >= 8 && vec) return *reinterpret_cast<const uint4*>(p);
@@ -102,28 +110,105 @@ struct Loader16 {
   __device__ static void store(uint16_t* lds, int tid, const uint4 (&v)[2]) {
 #pragma unroll
     for (int p = 0; p < 2; ++p) {
-      if (KC) {
+      if (KC)
         *reinterpret_cast<uint4*>(lds + (tid / 4 + 64 * p) * LDK + 8 * (tid % 4)) = v[p];
-      } else {  // transpose: element e of the chunk goes to row (outer + e), column k
-        const int kr = tid / 16 + 16 * p, c = 8 * (tid % 16);
-        const uint32_t w[4] = {v[p].x, v[p].y, v[p].z, v[p].w};
-#pragma unroll
-        for (int e = 0; e < 8; ++e) lds[(c + e) * LDK + kr] = (uint16_t)(w[e >> 1] >> (16 * (e & 1)));
-      }
+      else  // as stored: row k, 8 outer elements
+        *reinterpret_cast<uint4*>(lds + (tid / 16 + 16 * p) * LDS_KS + 8 * (tid % 16)) = v[p];
     }
   }
 };
 
-__device__ __forceinline__ bf16x8 frag(const uint16_t* lds, int row, int col) {
-  return *reinterpret_cast<const bf16x8*>(lds + row * LDK + col);
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+
+// MFMA operand of lane (li, lh) for outer index `outer` (its row or column)
+// and k = k0 + 8*lh + e, e = 0..7.
+// K-contiguous tile: one 16-byte read.
+// K-strided tile ([k][outer]): two transposing reads (ds_read_b64_tr_b16).
+// Within each group of 16 lanes, lane i of such a read receives element e
+// from mem[A(4e + i/4) + i%4], A(j) being the address lane j supplies; so
+// for read c (e = 4c .. 4c+3) lane j supplies row k0 + 8*lh + 4c + j/4 at
+// column (outer - li) + 16*(li/16) + 4*(j%4), j = li % 16.
+template <bool KC>
+__device__ __forceinline__ bf16x8 frag(const uint16_t* lds, int outer, int k0, int li, int lh) {
+  if (KC) return *reinterpret_cast<const bf16x8*>(lds + outer * LDK + k0 + 8 * lh);
+  const int col = (outer - li) + 16 * (li / 16) + 4 * (li % 4);
+  bf16x4 h[2];
+#pragma unroll
+  for (int c = 0; c < 2; ++c) {
+    const int row = k0 + 8 * lh + 4 * c + (li % 16) / 4;
+    const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(lds + row * LDS_KS + col));
+    h[c] = __builtin_bit_cast(bf16x4, v);
+  }
+  return __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7);
 }
 
 __host__ __device__ inline int tiles_of(const GemmArgs& g) { return ((g.M + TB - 1) / TB) * ((g.N + TB - 1) / TB) * g.batch; }
 
+// Weight-gradient epilogue through LDS: the float32 accumulator tile is
+// written to LDS, then every thread streams 16-byte chunks of rows
+// (W_src read, W_dst and its bf16 shadow written, 16 chunks in flight), so
+// the master-weight traffic is coalesced.  Needs 16-byte rows.
+__device__ __forceinline__ bool dw_vec_ok(const GemmArgs& g) {
+  const uintptr_t p = (uintptr_t)g.w_src | (uintptr_t)g.w_dst | (g.last ? (uintptr_t)g.w_snap : 0);
+  return (p & 15) == 0 && ((uintptr_t)g.w_dst16 & 7) == 0 && g.ldw % 4 == 0 && g.pstride % 4 == 0 && g.N % 4 == 0;
+}
+
+__device__ __forceinline__ void dw_epilogue_lds(const GemmArgs& g, int worker, int m0, int n0, const f32x16 (&acc)[2][2],
+                                                float* et) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1, li = lane & 31, lh = lane >> 5;
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        et[(wm * 64 + 32 * bi + 8 * (r >> 2) + 4 * lh + (r & 3)) * EPI_LD + wn * 64 + 32 * bj + li] = acc[bi][bj][r];
+  __syncthreads();
+  const int64_t wo = (int64_t)worker * g.pstride;
+  constexpr int CH = TB * TB / 4 / NT;  // 16-byte chunks per thread
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    float4 w[CH / 2], sn[CH / 2];
+    int64_t e[CH / 2];
+    bool ok[CH / 2];
+#pragma unroll
+    for (int u = 0; u < CH / 2; ++u) {
+      const int c = tid + NT * (u + half * CH / 2), row = c / (TB / 4), col = 4 * (c % (TB / 4));
+      ok[u] = m0 + row < g.M && n0 + col < g.N;
+      e[u] = wo + (int64_t)(m0 + row) * g.ldw + n0 + col;
+      w[u] = ok[u] ? *reinterpret_cast<const float4*>(g.w_src + e[u]) : make_float4(0.f, 0.f, 0.f, 0.f);
+      if (g.last) sn[u] = ok[u] ? *reinterpret_cast<const float4*>(g.w_snap + e[u]) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < CH / 2; ++u) {
+      const int c = tid + NT * (u + half * CH / 2), row = c / (TB / 4), col = 4 * (c % (TB / 4));
+      const float4 a = *reinterpret_cast<const float4*>(et + row * EPI_LD + col);
+      float4 nw = make_float4(w[u].x - g.eta * a.x, w[u].y - g.eta * a.y, w[u].z - g.eta * a.z, w[u].w - g.eta * a.w);
+      if (!ok[u]) continue;
+      if (g.last) {
+        nw = make_float4((nw.x - sn[u].x) / g.lam, (nw.y - sn[u].y) / g.lam, (nw.z - sn[u].z) / g.lam,
+                         (nw.w - sn[u].w) / g.lam);
+        *reinterpret_cast<float4*>(g.w_dst + e[u]) = nw;
+      } else {
+        *reinterpret_cast<float4*>(g.w_dst + e[u]) = nw;
+        uint2 h;
+        h.x = f32_to_bf16_rne(nw.x) | ((uint32_t)f32_to_bf16_rne(nw.y) << 16);
+        h.y = f32_to_bf16_rne(nw.z) | ((uint32_t)f32_to_bf16_rne(nw.w) << 16);
+        *reinterpret_cast<uint2*>(g.w_dst16 + e[u]) = h;
+      }
+    }
+  }
+}
+
 // One 128x128 output tile (logical tile id `logical`) of one product.
+// lds: LDS_BYTES of LDS.
 template <bool A_KC, bool B_KC, int EPI>
-__device__ __forceinline__ void gemm_tile16(const GemmArgs& g, const int logical, uint16_t (*lds_a)[TILE],
-                                            uint16_t (*lds_b)[TILE]) {
+__device__ __forceinline__ void gemm_tile16(const GemmArgs& g, const int logical, char* lds) {
+  uint16_t (*lds_a)[TILE] = reinterpret_cast<uint16_t (*)[TILE]>(lds);
+  uint16_t (*lds_b)[TILE] = reinterpret_cast<uint16_t (*)[TILE]>(lds + 2 * TILE * 2);
   const int tid = threadIdx.x;
   const int tm = (g.M + TB - 1) / TB, tn = (g.N + TB - 1) / TB;
   const int worker = logical / (tm * tn);
@@ -172,8 +257,8 @@ __device__ __forceinline__ void gemm_tile16(const GemmArgs& g, const int logical
       bf16x8 af[2], bfr[2];
 #pragma unroll
       for (int b = 0; b < 2; ++b) {
-        af[b] = frag(lds_a[cur], wm * 64 + 32 * b + li, 16 * s + 8 * lh);
-        bfr[b] = frag(lds_b[cur], wn * 64 + 32 * b + li, 16 * s + 8 * lh);
+        af[b] = frag<A_KC>(lds_a[cur], wm * 64 + 32 * b + li, 16 * s, li, lh);
+        bfr[b] = frag<B_KC>(lds_b[cur], wn * 64 + 32 * b + li, 16 * s, li, lh);
       }
 #pragma unroll
       for (int bi = 0; bi < 2; ++bi)
@@ -181,10 +266,9 @@ __device__ __forceinline__ void gemm_tile16(const GemmArgs& g, const int logical
         for (int bj = 0; bj < 2; ++bj)
           acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[bi], bfr[bj], acc[bi][bj], 0, 0, 0);
     }
-    if (do_bias) {
-      const uint16_t* row = lds_a[cur] + tid * LDK;
+    if (do_bias) {  // A = dZ^T, K-strided: column tid of the [k][outer] tile
 #pragma unroll 8
-      for (int k = 0; k < BKH; ++k) bsum += bf16_to_f32(row[k]);
+      for (int k = 0; k < BKH; ++k) bsum += bf16_to_f32(lds_a[cur][k * LDS_KS + tid]);
     }
     if (kt + 1 < nk) {
       Loader16<A_KC>::store(lds_a[cur ^ 1], tid, va);
@@ -193,6 +277,10 @@ __device__ __forceinline__ void gemm_tile16(const GemmArgs& g, const int logical
     __syncthreads();
   }
 
+  if (EPI == EPI_DW_UPDATE && dw_vec_ok(g)) {
+    // (the K loop ended with a barrier: the operand tiles are free)
+    dw_epilogue_lds(g, worker, m0, n0, acc, reinterpret_cast<float*>(lds));
+  } else {
   // epilogue: block (bi, bj) lane holds D[i][j], j = lane%32,
   // i = 8*(r/4) + 4*(lane/32) + r%4 within the 32x32 block
 #pragma unroll
@@ -232,6 +320,7 @@ __device__ __forceinline__ void gemm_tile16(const GemmArgs& g, const int logical
       }
     }
   }
+  }
   if (do_bias) {
     const int o = m0 + tid;
     if (o < g.M) {
@@ -244,21 +333,19 @@ __device__ __forceinline__ void gemm_tile16(const GemmArgs& g, const int logical
 
 template <bool A_KC, bool B_KC, int EPI>
 __global__ __launch_bounds__(NT) void gemm_bf16_kernel(GemmArgs g) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds_a[2][TILE];
-  __shared__ __attribute__((aligned(16))) uint16_t lds_b[2][TILE];
-  gemm_tile16<A_KC, B_KC, EPI>(g, xcd_remap(blockIdx.x, tiles_of(g)), lds_a, lds_b);
+  __shared__ __attribute__((aligned(16))) char lds[LDS_BYTES];
+  gemm_tile16<A_KC, B_KC, EPI>(g, xcd_remap(blockIdx.x, tiles_of(g)), lds);
 }
 
 // Input-gradient tiles and weight-gradient tiles of one layer in one launch
 // (see the float32 version).
 __global__ __launch_bounds__(NT) void gemm_bf16_bwd_kernel(GemmArgs dx, GemmArgs dw, int n1, int n1pad) {
-  __shared__ __attribute__((aligned(16))) uint16_t lds_a[2][TILE];
-  __shared__ __attribute__((aligned(16))) uint16_t lds_b[2][TILE];
+  __shared__ __attribute__((aligned(16))) char lds[LDS_BYTES];
   const int pid = blockIdx.x;
   if (pid < n1pad) {
-    if (pid < n1) gemm_tile16<true, false, EPI_DX_MASK>(dx, xcd_remap(pid, n1), lds_a, lds_b);
+    if (pid < n1) gemm_tile16<true, false, EPI_DX_MASK>(dx, xcd_remap(pid, n1), lds);
   } else {
-    gemm_tile16<false, false, EPI_DW_UPDATE>(dw, xcd_remap(pid - n1pad, tiles_of(dw)), lds_a, lds_b);
+    gemm_tile16<false, false, EPI_DW_UPDATE>(dw, xcd_remap(pid - n1pad, tiles_of(dw)), lds);
   }
 }
 
