@@ -97,6 +97,16 @@ int agn_create(const agn_shapes* shapes, int32_t n, int32_t lambda, float eta,
 /* Use `hip_stream` (a hipStream_t; NULL = null stream) for all later work. */
 int agn_set_stream(agn_ctx* ctx, void* hip_stream);
 
+/* Commit rule.  normalize = 1 (the default): each worker commits its
+ * accumulated update divided by lambda (Eq. 1, Algorithm 1's normalization
+ * step: AGN).  normalize = 0: it commits the accumulated update itself,
+ * DOWNPOUR with local exploration (Section 2; the variant whose divergence
+ * the normalization is introduced to prevent).  With lambda = 1 the two
+ * rules coincide and are DOWNPOUR (Section 3, footnote to Eq. 1).
+ * Only before the first round (the round's kernels are recorded once):
+ * AGN_ESTATE afterwards, AGN_EINVAL for a value other than 0 or 1. */
+int agn_set_normalization(agn_ctx* ctx, int32_t normalize);
+
 /* Enqueue one AGN round.  commit_order: HOST, n entries, a permutation of
  * 0..n-1 (checked on the host; AGN_EINVAL leaves the state unchanged).
  * The j-th entry is the worker whose normalized delta is the j-th to be
@@ -136,9 +146,10 @@ int agn_set_central(agn_ctx* ctx, const float* in);
  * variable, the start of its next round) into out (DEVICE, P floats). */
 int agn_worker_params(agn_ctx* ctx, int32_t worker, float* out);
 
-/* Copy the normalized delta worker k committed in the last round (Eq. 1:
- * its accumulated update divided by lambda) into out (DEVICE, P floats,
- * packed).  AGN_ESTATE before the first round. */
+/* Copy the delta worker k committed in the last round (Eq. 1: its
+ * accumulated update divided by lambda; without normalization, see
+ * agn_set_normalization, the accumulated update itself) into out (DEVICE,
+ * P floats, packed).  AGN_ESTATE before the first round. */
 int agn_debug_delta(agn_ctx* ctx, int32_t worker, float* out);
 
 /* The m sample indices worker `worker` uses at local step `step_t`, for a

@@ -11,7 +11,9 @@ Normalization", ACML 2017):
 * Algorithm 1 (worker procedure of AGN): a worker pulls the central
   variable, runs lambda local mini-batch SGD steps while accumulating the
   steps in ``a``, divides ``a`` by lambda (the normalization step), commits
-  ``a`` and pulls the central variable again.
+  ``a`` and pulls the central variable again.  Without the normalization
+  step (``normalize=False``) this is Section 2's DOWNPOUR with accumulated
+  gradients; with lambda = 1 both are DOWNPOUR.
 * Eq. (1): the committed delta is minus the learning rate times the
   lambda-average of mini-batch mean gradients taken along the local path.
 * Eq. (2): the parameter server adds each arriving delta to the central
@@ -236,11 +238,16 @@ class AGNOracle:
     """
 
     def __init__(self, dims, n, lam, eta, m, seed=0, bf16=False, dtype=np.float32,
-                 init=None):
+                 init=None, normalize=True):
         if n < 1 or lam < 1 or m < 1 or len(dims) < 2:
             raise ValueError("bad shapes")
         self.dims = tuple(int(d) for d in dims)
         self.n, self.lam, self.m = int(n), int(lam), int(m)
+        # normalize=False: the worker commits its accumulated update itself
+        # (Section 2: DOWNPOUR with local exploration, the variant whose
+        # divergence motivates the normalization); with lam = 1 both rules
+        # are DOWNPOUR (Section 3, footnote to Eq. 1)
+        self.normalize = bool(normalize)
         self.prec = _Prec(dtype, bf16)
         self.eta = self.prec.dtype.type(eta)
         if init is None:
@@ -276,7 +283,8 @@ class AGNOracle:
                 new_a.append((st(aW + g_W), st(ab + g_b)))           # a <- a + g
                 new_theta.append((st(W + g_W), st(b + g_b)))         # theta <- theta + g
             theta, a = new_theta, new_a
-        a = [(st(aW / np.float64(self.lam)), st(ab / np.float64(self.lam))) for aW, ab in a]
+        if self.normalize:                                  # the normalization step
+            a = [(st(aW / np.float64(self.lam)), st(ab / np.float64(self.lam))) for aW, ab in a]
         return a, float(np.mean(losses)), theta
 
     def round(self, X, y, order):

@@ -27,7 +27,7 @@ EXPORTED = [
     "agn_create", "agn_set_stream", "agn_round", "agn_central", "agn_loss",
     "agn_num_params", "agn_last_error", "agn_destroy", "agn_set_central",
     "agn_worker_params", "agn_debug_batch_indices", "agn_set_kernel_timing",
-    "agn_kernel_timing", "agn_kernel_class_work", "agn_debug_delta",
+    "agn_kernel_timing", "agn_kernel_class_work", "agn_debug_delta", "agn_set_normalization",
 ]
 
 
@@ -64,6 +64,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "agn_create": (i32, [ctypes.POINTER(agn_shapes), i32, i32, ctypes.c_float, ctypes.c_uint64,
                              ctypes.POINTER(vp)]),
         "agn_set_stream": (i32, [vp, vp]),
+        "agn_set_normalization": (i32, [vp, i32]),
         "agn_round": (i32, [vp, ctypes.POINTER(agn_data), ctypes.POINTER(ctypes.c_int32)]),
         "agn_central": (i32, [vp, vp]),
         "agn_loss": (i32, [vp, vp]),
@@ -116,6 +117,10 @@ def agn_create(dims: Sequence[int], batch: int, n: int, lam: int, eta: float, se
     _check(lib.agn_create(ctypes.byref(shapes), int(n), int(lam), float(eta),
                           int(seed) & 0xFFFFFFFFFFFFFFFF, ctypes.byref(ctx)), None)
     return ctx
+
+
+def agn_set_normalization(ctx, normalize: bool):
+    _check(load_library().agn_set_normalization(ctx, int(bool(normalize))), ctx)
 
 
 def agn_set_stream(ctx, stream_ptr=None):
@@ -192,12 +197,14 @@ def agn_kernel_class_work(ctx, kernel_class: int):
 class AGN:
     """One AGN context on the current ROCm device and stream."""
 
-    def __init__(self, dims, n, lam, eta, m, seed, dtype="fp32"):
+    def __init__(self, dims, n, lam, eta, m, seed, dtype="fp32", normalize=True):
         self.dims = tuple(int(d) for d in dims)
         self.n, self.lam, self.m = int(n), int(lam), int(m)
         self.dtype = AGN_BF16 if dtype == "bf16" else AGN_FP32
         self.ctx = agn_create(self.dims, m, n, lam, eta, seed, self.dtype)
         agn_set_stream(self.ctx)
+        if not normalize:
+            agn_set_normalization(self.ctx, False)
         self.P = agn_num_params(self.ctx)
 
     def close(self):

@@ -66,6 +66,7 @@ struct agn_ctx {
   int64_t graph_n = -1;
   int device = 0;
   int use_head = 0;  // fused output-layer kernels (few classes)
+  int normalize = 1; // commit a / lambda (AGN) or a (DOWNPOUR with local exploration)
   int capturing = 0;
   hipStream_t ls = nullptr;           // stream the launch sequence is enqueued on
   int poisoned = 0;
@@ -257,7 +258,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     w.ldw = c->ldw[L - 1];
     w.pstride = ps;
     w.eta = c->eta;
-    w.lam = (float)c->lam;
+    w.lam = c->normalize ? (float)c->lam : 1.f;  // divisor of the committed delta
     w.last = last;
     HIP_CHECK(c, timed(c, AGN_K_OUTPUT_DW, [&] { return launch_head_dw(w, c->ls); }));
   } else {
@@ -305,7 +306,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     w.ldw = c->ldw[l];
     w.pstride = ps;
     w.eta = c->eta;
-    w.lam = (float)c->lam;
+    w.lam = c->normalize ? (float)c->lam : 1.f;  // divisor of the committed delta
     w.last = last;
     w.zero = c->zero;
     if (l >= 1) {  // dZ_l = (dZ_{l+1} W_l) * [H_l > 0]
@@ -471,6 +472,14 @@ int agn_create(const agn_shapes* shapes, int32_t n, int32_t lambda, float eta, u
 int agn_set_stream(agn_ctx* c, void* s) {
   if (int r = check_ctx(c)) return r;
   c->stream = reinterpret_cast<hipStream_t>(s);
+  return AGN_OK;
+}
+
+int agn_set_normalization(agn_ctx* c, int32_t normalize) {
+  if (int r = check_ctx(c)) return r;
+  if (normalize != 0 && normalize != 1) return fail(c, AGN_EINVAL, "normalize must be 0 or 1");
+  if (c->rounds != 0) return fail(c, AGN_ESTATE, "agn_set_normalization is allowed only before the first round");
+  c->normalize = normalize;
   return AGN_OK;
 }
 

@@ -18,7 +18,7 @@ import pytest
 
 import workloads as W
 from oracle import AGNOracle, he_normal_init, flat_params, batch_indices
-from tests.helpers import rel_err, to_device, require_gpu
+from tests.helpers import rel_err, tensor_slices, to_device, require_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -52,20 +52,57 @@ SMALL = [
     ("bf16_many_classes", (256, 300, 300, 100), 4, 2, 70, 0.01, 2, 1000, "gauss_linear", "permutation", "bf16"),
     ("bf16_unaligned_d0", (37, 29, 5), 4, 2, 9, 0.1, 3, 101, "sparse_teacher2", "permutation", "bf16"),
     ("bf16_sgd_n1_lam1", (64, 150, 3), 1, 1, 130, 0.05, 3, 300, "gauss_linear", "sequential", "bf16"),
+    # direct-load products with ragged 64-tiles: the persistent weight-gradient
+    # schedule needs K = m >= 97 (four K steps) and widths divisible by 4
+    ("dl_ragged", (100, 200, 136, 10), 3, 3, 100, 0.05, 3, 650, "sparse_teacher2", "permutation", "fp32"),
+    ("bf16_dl_ragged", (100, 200, 136, 10), 3, 3, 100, 0.05, 2, 650, "sparse_teacher2", "permutation", "bf16"),
+    # without the normalization step (Section 2: DOWNPOUR with local
+    # exploration): the committed delta is the accumulated update itself
+    ("accumulated_ragged", (200, 130, 70, 10), 3, 3, 40, 0.02, 3, 650, "gauss_linear", "permutation", "fp32",
+     False),
+    ("accumulated_dl", (100, 200, 136, 10), 3, 3, 100, 0.02, 2, 650, "sparse_teacher2", "permutation", "fp32",
+     False),
+    # (one round: the bf16 rounding cascade grows with the lambda-times larger
+    # commits; the commit rule is exercised in full by round 1)
+    ("bf16_accumulated", (200, 130, 70, 10), 3, 3, 40, 0.02, 1, 650, "gauss_linear", "permutation", "bf16",
+     False),
 ]
 
 
-def run_parity(wl, tol1, tolN, check_workers=True):
+def delta_err(got, disp, start, dims, div, tol):
+    """A committed delta against the oracle's displacement
+    (theta_lambda - theta_0) / div, per tensor: the error allowed is tol
+    relative to the delta, or 32 float32 ulps of the tensor's parameter scale
+    (divided by div), whichever is larger.  The path stores the displacement
+    of float32 parameters, so a rounding-level difference in theta_lambda is
+    an error of a few ulps of theta in the delta, however small the delta
+    is.  Returns (max over tensors of error / allowed, worst tensor)."""
+    worst, where = 0.0, None
+    got = got.astype(np.float64)
+    for name, a, b in tensor_slices(dims):
+        ref = disp[a:b]
+        scale = np.max(np.abs(start[a:b]))
+        ulp = 2.0 ** (np.floor(np.log2(scale)) - 23) if scale > 0 else 0.0
+        allowed = max(tol * np.max(np.abs(ref)), 32 * ulp / div, 1e-30)
+        e = np.max(np.abs(got[a:b] - ref)) / allowed
+        if e > worst:
+            worst, where = e, name
+    return worst, where
+
+
+def run_parity(wl, tol1, tolN, check_workers=True, normalize=True):
     agn = _agn()
     import torch
     X, y = W.make_data(wl)
     orders = W.commit_orders(wl)
     xd, yd = to_device(X, y)
-    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, dtype=wl.dtype)
-    o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, bf16=wl.dtype == "bf16")
+    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, dtype=wl.dtype, normalize=normalize)
+    o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, bf16=wl.dtype == "bf16",
+                  normalize=normalize)
     # the initial central variable (same generator on both sides)
     init_err, _ = rel_err(g.central().cpu().numpy(), o.central_flat(), wl.dims)
     assert init_err <= 1e-7, f"init mismatch {init_err}"
+    start = o.central_flat().astype(np.float64)   # every worker's round-1 start
     for r, order in enumerate(orders, start=1):
         g.round(xd, yd, order)
         o.round(X, y, order)
@@ -75,10 +112,12 @@ def run_parity(wl, tol1, tolN, check_workers=True):
         assert err <= tol, (r, where, err)
         gl = g.loss().cpu().numpy()
         np.testing.assert_allclose(gl, o.last_loss, rtol=max(tol, 1e-5), atol=1e-6)
-        if r == 1:   # the committed normalized deltas (Eq. 1), from the same start
+        if r == 1:   # the committed deltas (Eq. 1), from the same start
+            div = wl.lam if normalize else 1
             for k in range(wl.n):
-                e, w = rel_err(g.delta(k).cpu().numpy(), flat_params(o.last_deltas[k]), wl.dims)
-                assert e <= tol, (r, k, w, e)
+                disp = (flat_params(o.last_finals[k]).astype(np.float64) - start) / div
+                e, w = delta_err(g.delta(k).cpu().numpy(), disp, start, wl.dims, div, tol)
+                assert e <= 1.0, (r, k, w, e)
         if check_workers:
             for k in range(wl.n):
                 e, w = rel_err(g.worker_params(k).cpu().numpy(), o.worker_flat(k), wl.dims)
@@ -89,10 +128,45 @@ def run_parity(wl, tol1, tolN, check_workers=True):
 
 @pytest.mark.parametrize("case", SMALL, ids=[c[0] for c in SMALL])
 def test_small_shapes(case):
-    name, dims, n, lam, m, eta, R, N, data, order, dtype = case
+    name, dims, n, lam, m, eta, R, N, data, order, dtype = case[:11]
+    normalize = case[11] if len(case) > 11 else True
     wl = W.small_workload(name, dims, n, lam, m, eta, R, N, data=data, order=order, dtype=dtype)
     tol1, tolN = (FP32_TOL_1, FP32_TOL_N) if dtype == "fp32" else (BF16_TOL, BF16_TOL)
-    run_parity(wl, tol1, tolN)
+    run_parity(wl, tol1, tolN, normalize=normalize)
+
+
+def test_downpour_lambda1_rules_coincide():
+    """With lambda = 1 the normalized and the accumulated commit are the same
+    rule (DOWNPOUR, Section 3 footnote to Eq. 1): bitwise equal results."""
+    agn = _agn()
+    wl = W.small_workload("dp", (100, 200, 136, 10), 4, 1, 100, 0.05, 3, 650, data="gauss_linear",
+                          order="permutation")
+    X, y = W.make_data(wl)
+    xd, yd = to_device(X, y)
+    res = []
+    for normalize in (True, False):
+        g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, normalize=normalize)
+        for order in W.commit_orders(wl):
+            g.round(xd, yd, order)
+        res.append(g.central().cpu().numpy())
+        g.close()
+    np.testing.assert_array_equal(res[0], res[1])
+
+
+def test_set_normalization_errors():
+    """Only 0 or 1, and only before the first round (AGN_EINVAL / AGN_ESTATE)."""
+    agn = _agn()
+    wl = W.small_workload("nrm", (20, 12, 4), 3, 2, 5, 0.1, 1, 60)
+    X, y = W.make_data(wl)
+    xd, yd = to_device(X, y)
+    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=4)
+    assert agn.load_library().agn_set_normalization(g.ctx, 2) == -1
+    agn.agn_set_normalization(g.ctx, False)
+    g.round(xd, yd, [0, 1, 2])
+    with pytest.raises(agn.AGNError) as ei:
+        agn.agn_set_normalization(g.ctx, True)
+    assert ei.value.code == -4
+    g.close()
 
 
 def test_tiny_workload_full_size():

@@ -425,3 +425,81 @@ def test_bad_order_rejected():
     X, y = make_xy(9, 3, 2, 0)
     with pytest.raises(ValueError):
         orc.round(X, y, [0, 0, 1])
+
+
+# --------------------------------------------------------------------------
+# Without the normalization step (Section 2: DOWNPOUR with local
+# exploration; Section 3 footnote to Eq. 1: lambda = 1 is DOWNPOUR)
+# --------------------------------------------------------------------------
+@pytest.mark.parametrize("dtype,tol", [(np.float64, 1e-12), (np.float32, 2e-6)])
+def test_accumulated_delta_is_displacement(dtype, tol):
+    """Algorithm 1 adds every local step g to both a and theta, so the
+    un-normalized commit is the displacement theta_lambda - theta_0."""
+    dims, n, lam, m = (12, 9, 5), 3, 6, 4
+    X, y = make_xy(60, dims[0], dims[-1], 5)
+    orc = O.AGNOracle(dims, n=n, lam=lam, eta=0.3, m=m, seed=3, dtype=dtype, normalize=False)
+    for r in range(2):
+        start = [orc.worker_flat(k).astype(np.float64) for k in range(n)]
+        orc.round(X, y, np.random.default_rng(r).permutation(n))
+        for k in range(n):
+            a = O.flat_params(orc.last_deltas[k]).astype(np.float64)
+            disp = O.flat_params(orc.last_finals[k]).astype(np.float64) - start[k]
+            assert np.max(np.abs(a - disp)) <= tol * np.max(np.abs(disp))
+            assert np.max(np.abs(disp)) > 0
+
+
+def test_accumulated_is_lambda_times_normalized():
+    """From the same start the two rules commit a and a / lambda (fp64)."""
+    dims, n, lam, m = (12, 9, 5), 3, 6, 4
+    X, y = make_xy(60, dims[0], dims[-1], 5)
+    a = O.AGNOracle(dims, n=n, lam=lam, eta=0.3, m=m, seed=3, dtype=np.float64, normalize=False)
+    b = O.AGNOracle(dims, n=n, lam=lam, eta=0.3, m=m, seed=3, dtype=np.float64)
+    a.round(X, y, [2, 0, 1])
+    b.round(X, y, [2, 0, 1])
+    for k in range(n):
+        da = O.flat_params(a.last_deltas[k])
+        db = O.flat_params(b.last_deltas[k])
+        assert np.max(np.abs(da - lam * db)) <= 1e-13 * np.max(np.abs(da))
+    # round 1: every worker starts from the same central variable, so the
+    # central variable moves by the sum of the deltas under either rule
+    c0 = O.flat_params(O.he_normal_init(dims, 3, dtype=np.float64))
+    np.testing.assert_allclose(a.central_flat() - c0, lam * (b.central_flat() - c0), rtol=1e-10, atol=1e-14)
+
+
+def test_lambda1_rules_coincide():
+    """lambda = 1: normalized and accumulated commits are the same rule."""
+    dims, n, m = (12, 9, 5), 4, 4
+    X, y = make_xy(80, dims[0], dims[-1], 6)
+    a = O.AGNOracle(dims, n=n, lam=1, eta=0.2, m=m, seed=8, normalize=False)
+    b = O.AGNOracle(dims, n=n, lam=1, eta=0.2, m=m, seed=8)
+    rng = np.random.default_rng(1)
+    for r in range(3):
+        order = rng.permutation(n)
+        a.round(X, y, order)
+        b.round(X, y, order)
+    assert np.array_equal(a.central_flat(), b.central_flat())
+
+
+def test_accumulated_commits_fail_to_converge_where_agn_does():
+    """The paper's motivating observation (Section 2, the accumulated-
+    gradient DOWNPOUR divergence figure): with the same workers, learning
+    rate and local steps, committing accumulated updates makes the central
+    variable oscillate at a high loss while AGN's loss falls every round.
+    Synthetic stand-in: 20-16-4 MLP, n = 8, lambda = 10, eta = 0.1, m = 16."""
+    import workloads as W
+    dims, n, lam, eta, m, R = (20, 16, 4), 8, 10, 0.1, 16, 6
+    wl = W.small_workload("dv", dims, n, lam, m, eta, R, 4096, data="gauss_linear", order="permutation")
+    X, y = W.make_data(wl)
+    prec = O._Prec(np.float32, False)
+    traj = {}
+    for normalize in (True, False):
+        o = O.AGNOracle(dims, n, lam, eta, m, seed=wl.seed, normalize=normalize)
+        losses = []
+        for order in W.commit_orders(wl):
+            o.round(X, y, order)
+            losses.append(O.loss_and_grads(o.central, X[:1024], y[:1024], prec)[0])
+        traj[normalize] = np.array(losses)
+    agn, acc = traj[True], traj[False]
+    assert np.all(np.diff(agn) < 0), agn
+    assert not np.all(np.diff(acc) < 0), acc
+    assert acc[-1] > 1.5 * agn[-1] and acc.mean() > 1.5 * agn.mean(), (agn, acc)
