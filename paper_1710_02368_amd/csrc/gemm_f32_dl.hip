@@ -48,6 +48,7 @@ namespace agn {
 namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int NT = 256, TM = 64, BKD = 32, NS = 4;  // NS: LDS stages
 constexpr int TILE_F = TM * BKD;                     // floats per operand tile
@@ -549,11 +550,16 @@ __device__ __forceinline__ void dw_tiles(const GemmArgs& g, int wg, int nwg, flo
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int row = c.m0 + q.wm * 32 + 2 * (4 * q.lg + r) + bi, col = c.n0 + q.wn * 32 + 2 * q.li;
-        float* dst = g.w_dst + wo + (int64_t)row * g.ldw + col;
-        if (full) {
-          *reinterpret_cast<float2*>(dst) = nw[bi][r];
-        } else if (row < g.M && col < g.N) {  // (N even: col+1 < N too)
-          *reinterpret_cast<float2*>(dst) = nw[bi][r];
+        // streaming stores for the updated weights (read again only by the
+        // next local step's products); the last step's deltas are cached,
+        // the commit reads them next
+        f32x2* dst = reinterpret_cast<f32x2*>(g.w_dst + wo + (int64_t)row * g.ldw + col);
+        const f32x2 v = {nw[bi][r].x, nw[bi][r].y};
+        if (full || (row < g.M && col < g.N)) {  // (N even: col+1 < N too)
+          if (LAST)
+            *dst = v;
+          else
+            __builtin_nontemporal_store(v, dst);
         }
       }
     if (c.tile_n == 0 && q.wn == 0) {

@@ -47,14 +47,17 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
   float* bs = smem + CMAX * LW;
   const int64_t t = gather_step(a.g);
 
-  // rows of this wave: issue every load of H before anything waits
+  // rows of this wave: issue every load of H (and the labels) before
+  // anything waits
   int jr[HEAD_WAVE_ROWS];
+  int label[HEAD_WAVE_ROWS];
   const float* hp[HEAD_WAVE_ROWS];
   float hv[HEAD_WAVE_ROWS][QMAX];
 #pragma unroll
   for (int r = 0; r < HEAD_WAVE_ROWS; ++r) {
     jr[r] = r0 + wave * HEAD_WAVE_ROWS + r;
     const int j = jr[r] < a.m ? jr[r] : a.m - 1;   // rows past m compute a copy, store nothing
+    label[r] = a.y[batch_row(k, t, a.g.mb, a.g.S, j)];
     hp[r] = a.gather ? a.h + batch_row(k, t, a.g.mb, a.g.S, j) * a.ldh
                      : a.h + (int64_t)k * a.hstride + (int64_t)j * a.ldh;
 #pragma unroll
@@ -110,8 +113,7 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
   const float inv_m = 1.f / (float)a.m;
 #pragma unroll
   for (int r = 0; r < HEAD_WAVE_ROWS; ++r) {
-    const int j = jr[r] < a.m ? jr[r] : a.m - 1;
-    const int label = a.y[batch_row(k, t, a.g.mb, a.g.S, j)];
+    const int lb = label[r];
     float mx = -INFINITY;
 #pragma unroll
     for (int c = 0; c < CMAX; ++c) mx = c < C ? fmaxf(mx, p[r][c]) : mx;
@@ -119,14 +121,14 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
 #pragma unroll
     for (int c = 0; c < CMAX; ++c) {
       const float e = c < C ? expf(p[r][c] - mx) : 0.f;
-      zy = c == label ? p[r][c] : zy;
+      zy = c == lb ? p[r][c] : zy;
       s += e;
       p[r][c] = e;
     }
     const float inv_s = 1.f / s;
 #pragma unroll
     for (int c = 0; c < CMAX; ++c)
-      p[r][c] = c < C ? (p[r][c] * inv_s - (c == label ? 1.f : 0.f)) * inv_m : 0.f;
+      p[r][c] = c < C ? (p[r][c] * inv_s - (c == lb ? 1.f : 0.f)) * inv_m : 0.f;
     if (jr[r] < a.m) {
       float* dzo = a.dz + (int64_t)k * a.dzstride + (int64_t)jr[r] * a.lddz;
       float mine = 0.f;
