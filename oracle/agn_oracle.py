@@ -238,7 +238,7 @@ class AGNOracle:
     """
 
     def __init__(self, dims, n, lam, eta, m, seed=0, bf16=False, dtype=np.float32,
-                 init=None, normalize=True):
+                 init=None, normalize=True, adam=None):
         if n < 1 or lam < 1 or m < 1 or len(dims) < 2:
             raise ValueError("bad shapes")
         self.dims = tuple(int(d) for d in dims)
@@ -248,6 +248,14 @@ class AGNOracle:
         # divergence motivates the normalization); with lam = 1 both rules
         # are DOWNPOUR (Section 3, footnote to Eq. 1)
         self.normalize = bool(normalize)
+        # adam=(beta1, beta2, eps): the local step of Algorithm 1 comes from
+        # Adam (Algorithm 1's gradient line names it as an option; Kingma &
+        # Ba 2015): per worker first and second moment estimates of its
+        # gradients, zero at the start and kept across pulls (the worker's
+        # step counter t of Algorithm 1 is not reset by a pull either), and
+        # g = -eta * mhat / (sqrt(vhat) + eps) with mhat = m / (1 - beta1^t),
+        # vhat = v / (1 - beta2^t) at the worker's local step t = 1, 2, ...
+        self.adam = None if adam is None else tuple(float(a) for a in adam)
         self.prec = _Prec(dtype, bf16)
         self.eta = self.prec.dtype.type(eta)
         if init is None:
@@ -258,6 +266,9 @@ class AGNOracle:
         self.central = central
         # Algorithm 1, first line: every worker starts from the pulled central variable
         self.workers = [[(W.copy(), b.copy()) for W, b in central] for _ in range(self.n)]
+        if self.adam is not None:
+            self.moments = [[(np.zeros_like(W), np.zeros_like(b), np.zeros_like(W), np.zeros_like(b))
+                             for W, b in central] for _ in range(self.n)]
         self.r = 0
         self.version = 0
         self.pulled_version = [0] * self.n
@@ -277,15 +288,38 @@ class AGNOracle:
             loss, grads = loss_and_grads(theta, X[idx], y[idx], self.prec)
             losses.append(loss)
             new_theta, new_a = [], []
-            for (W, b), (aW, ab), (gW, gb) in zip(theta, a, grads):
-                g_W = st(-np.float64(self.eta) * gW)       # g = -eta * grad
-                g_b = st(-np.float64(self.eta) * gb)
+            for li, ((W, b), (aW, ab), (gW, gb)) in enumerate(zip(theta, a, grads)):
+                if self.adam is None:
+                    g_W = st(-np.float64(self.eta) * gW)       # g = -eta * grad
+                    g_b = st(-np.float64(self.eta) * gb)
+                else:
+                    g_W, g_b = self._adam_step(k, li, gW, gb, t + 1)
                 new_a.append((st(aW + g_W), st(ab + g_b)))           # a <- a + g
                 new_theta.append((st(W + g_W), st(b + g_b)))         # theta <- theta + g
             theta, a = new_theta, new_a
         if self.normalize:                                  # the normalization step
             a = [(st(aW / np.float64(self.lam)), st(ab / np.float64(self.lam))) for aW, ab in a]
         return a, float(np.mean(losses)), theta
+
+    def _adam_step(self, k, li, gW, gb, t):
+        """Adam's step for worker k, layer li, at the worker's local step t
+        (1-based): moments stored in float32, the step in float64, rounded
+        once."""
+        st = self.prec.st
+        b1, b2, eps = (np.float64(x) for x in self.adam)
+        mW, mb, vW, vb = self.moments[k][li]
+        out = []
+        new = []
+        for g, mo, ve in ((gW, mW, vW), (gb, mb, vb)):
+            g = np.asarray(g, dtype=np.float64)
+            m1 = st(b1 * mo + (1.0 - b1) * g)
+            v1 = st(b2 * ve + (1.0 - b2) * g * g)
+            mhat = m1.astype(np.float64) / (1.0 - b1 ** t)
+            vhat = v1.astype(np.float64) / (1.0 - b2 ** t)
+            out.append(st(-np.float64(self.eta) * mhat / (np.sqrt(vhat) + eps)))
+            new.append((m1, v1))
+        self.moments[k][li] = (new[0][0], new[1][0], new[0][1], new[1][1])
+        return out[0], out[1]
 
     def round(self, X, y, order):
         """One AGN round on data (X [N][d_0], y [N]) with the given commit

@@ -503,3 +503,93 @@ def test_accumulated_commits_fail_to_converge_where_agn_does():
     assert np.all(np.diff(agn) < 0), agn
     assert not np.all(np.diff(acc) < 0), acc
     assert acc[-1] > 1.5 * agn[-1] and acc.mean() > 1.5 * agn.mean(), (agn, acc)
+
+
+# --------------------------------------------------------------------------
+# Adam as the local rule (Algorithm 1's gradient line; Kingma & Ba 2015).
+# Reading: the worker's moment estimates and step counter run on across
+# pulls, as Algorithm 1's t does.
+# --------------------------------------------------------------------------
+ADAM = (0.9, 0.999, 1e-8)
+
+
+def torch_adam_trajectory(init, X, y, m, eta, steps, betas, eps):
+    """Textbook loop: torch modules, autograd, one torch.optim.Adam, a plain
+    cyclic cursor over the rows (one worker, shard = all N rows)."""
+    import torch
+    N = X.shape[0]
+    layers = []
+    for W, b in init:
+        lin = torch.nn.Linear(W.shape[1], W.shape[0]).double()
+        with torch.no_grad():
+            lin.weight.copy_(torch.from_numpy(W))
+            lin.bias.copy_(torch.from_numpy(b))
+        layers.append(lin)
+    opt = torch.optim.Adam([p for lin in layers for p in lin.parameters()], lr=eta, betas=betas, eps=eps)
+    cursor = 0
+    for _ in range(steps):
+        rows = [(cursor + j) % N for j in range(m)]
+        cursor = (cursor + m) % N
+        h = torch.from_numpy(X[rows].astype(np.float64))
+        for i, lin in enumerate(layers):
+            h = lin(h)
+            if i < len(layers) - 1:
+                h = torch.relu(h)
+        loss = torch.nn.functional.cross_entropy(h, torch.from_numpy(y[rows]).long())
+        opt.zero_grad()
+        loss.backward()
+        opt.step()
+    return [(lin.weight.detach().numpy(), lin.bias.detach().numpy()) for lin in layers]
+
+
+@pytest.mark.parametrize("lam,normalize", [(1, True), (3, False)])
+def test_adam_one_worker_is_textbook_adam(lam, normalize):
+    """n = 1: with lambda = 1 (or without the normalization step) the worker
+    pulls back its own parameters, so R rounds are lambda*R steps of plain
+    Adam with one optimizer state, against torch.optim.Adam (fp64)."""
+    pytest.importorskip("torch")
+    dims, m, eta, R, N = (10, 8, 6, 4), 5, 0.01, 4, 23
+    X, y = make_xy(N, dims[0], dims[-1], 21)
+    orc = O.AGNOracle(dims, n=1, lam=lam, eta=eta, m=m, seed=99, dtype=np.float64, normalize=normalize,
+                      adam=ADAM)
+    init = [(W.copy(), b.copy()) for W, b in orc.central]
+    for r in range(R):
+        orc.round(X, y, [0])
+    ref = torch_adam_trajectory(init, X, y, m, eta, lam * R, ADAM[:2], ADAM[2])
+    for (W, b), (Wt, bt) in zip(orc.central, ref):
+        np.testing.assert_allclose(W, Wt, rtol=0, atol=1e-12)
+        np.testing.assert_allclose(b, bt, rtol=0, atol=1e-12)
+
+
+def test_adam_first_step_closed_form():
+    """From zero moments the first Adam step is -eta * g / (|g| + eps)
+    (the bias corrections cancel (1 - beta) exactly)."""
+    dims, m, eta, N = (10, 8, 6, 4), 5, 0.01, 23
+    X, y = make_xy(N, dims[0], dims[-1], 22)
+    orc = O.AGNOracle(dims, n=1, lam=1, eta=eta, m=m, seed=5, dtype=np.float64, adam=ADAM)
+    theta0 = [(W.copy(), b.copy()) for W, b in orc.central]
+    idx = O.batch_indices(0, 0, m, N)
+    _, grads = O.loss_and_grads(theta0, X[idx], y[idx], O._Prec(np.float64, False))
+    orc.round(X, y, [0])
+    for (W0, b0), (gW, gb), (W1, b1) in zip(theta0, grads, orc.central):
+        np.testing.assert_allclose(W1 - W0, -eta * gW / (np.abs(gW) + ADAM[2]), rtol=1e-12, atol=1e-16)
+        np.testing.assert_allclose(b1 - b0, -eta * gb / (np.abs(gb) + ADAM[2]), rtol=1e-12, atol=1e-16)
+
+
+def test_adam_moments_persist_across_pulls():
+    """Two workers, sequential commits: round 2 must use each worker's own
+    moments from round 1 (a fresh optimizer each round gives another
+    result)."""
+    dims, m, eta, N = (10, 8, 6, 4), 5, 0.01, 40
+    X, y = make_xy(N, dims[0], dims[-1], 23)
+    a = O.AGNOracle(dims, n=2, lam=2, eta=eta, m=m, seed=5, dtype=np.float64, adam=ADAM)
+    a.round(X, y, [0, 1])
+    mom = [[tuple(x.copy() for x in t) for t in w] for w in a.moments]
+    assert all(np.max(np.abs(t[0])) > 0 for w in mom for t in w)
+    a.round(X, y, [1, 0])
+    # the same round 2 from zeroed moments differs
+    b = O.AGNOracle(dims, n=2, lam=2, eta=eta, m=m, seed=5, dtype=np.float64, adam=ADAM)
+    b.round(X, y, [0, 1])
+    b.moments = [[tuple(np.zeros_like(x) for x in t) for t in w] for w in b.moments]
+    b.round(X, y, [1, 0])
+    assert np.max(np.abs(a.central_flat() - b.central_flat())) > 1e-6
