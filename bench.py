@@ -57,7 +57,10 @@ def bound_of(w, dtype):
     return "mfma" if w["flops"] / w["bytes"] >= ridge else "hbm"
 
 
-def cpu_baseline(wl, X, y, orders, budget_s=12.0):
+ADAM = (0.9, 0.999, 1e-8)
+
+
+def cpu_baseline(wl, X, y, orders, budget_s=12.0, adam=None):
     """The oracle as it stands, on the host cores, over whole rounds until
     about budget_s seconds have passed (at least one round)."""
     from oracle import AGNOracle
@@ -66,7 +69,7 @@ def cpu_baseline(wl, X, y, orders, budget_s=12.0):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = len(os.sched_getaffinity(0))
-    o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, bf16=wl.dtype == "bf16")
+    o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, bf16=wl.dtype == "bf16", adam=adam)
     t0 = time.perf_counter()
     rounds = 0
     while True:
@@ -130,6 +133,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="mlp1000_n8")
+    ap.add_argument("--optimizer", choices=["sgd", "adam"], default="sgd",
+                    help="local rule: plain SGD (the paper's Eq. 1) or Adam (beta 0.9/0.999, eps 1e-8)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -153,7 +158,8 @@ def main():
     orders = W.commit_orders(wl, rounds=max(wl.rounds, 1))
     xd = torch.from_numpy(X.view(np.int16) if X.dtype == np.uint16 else X).cuda()
     yd = torch.from_numpy(y).cuda()
-    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, dtype=wl.dtype)
+    adam = ADAM if args.optimizer == "adam" else None
+    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, dtype=wl.dtype, adam=adam)
     order_at = lambda i: orders[i % len(orders)]
 
     for i in range(args.warmup):
@@ -234,7 +240,8 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(dt * 1e3 / args.steps, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32" if wl.dtype == "fp32" else "bf16", "data": "synthetic",
-        "config": {"workload": wl.name, "dims": list(wl.dims), "n": wl.n, "lambda": wl.lam, "m": wl.m,
+        "config": {"workload": wl.name, "optimizer": args.optimizer,
+                   "dims": list(wl.dims), "n": wl.n, "lambda": wl.lam, "m": wl.m,
                    "eta": wl.eta, "commit_order": wl.order, "num_samples": wl.N,
                    "worker_samples_per_round": wl.worker_samples_per_round},
         "roofline": roof,
@@ -248,7 +255,7 @@ def main():
     }
     g.close()
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, X, y, orders, budget_s=args.cpu_budget)
+        out["cpu_baseline"] = cpu_baseline(wl, X, y, orders, budget_s=args.cpu_budget, adam=adam)
     print(json.dumps(out), flush=True)
 
 

@@ -107,6 +107,21 @@ int agn_set_stream(agn_ctx* ctx, void* hip_stream);
  * AGN_ESTATE afterwards, AGN_EINVAL for a value other than 0 or 1. */
 int agn_set_normalization(agn_ctx* ctx, int32_t normalize);
 
+/* Local rule of the workers (Algorithm 1's gradient line, which names Adam
+ * as an option).  AGN_OPT_SGD (the default): g = -eta * gradient.
+ * AGN_OPT_ADAM (Kingma & Ba 2015): each worker keeps first and second
+ * moment estimates m, v of its gradients (float32 per parameter, zero when
+ * selected, kept across pulls as Algorithm 1's step counter is) and
+ * g = -eta * mhat / (sqrt(vhat) + eps), mhat = m / (1 - beta1^t),
+ * vhat = v / (1 - beta2^t) at the worker's local step t = r*lambda + i + 1.
+ * Selecting Adam allocates the moment buffers (2 * n * P floats) and
+ * zeroes them.  beta1, beta2 in [0, 1), eps > 0 finite (ignored for SGD).
+ * Only before the first round: AGN_ESTATE afterwards, AGN_EINVAL for bad
+ * values, AGN_ENOMEM if the buffers cannot be allocated. */
+#define AGN_OPT_SGD 0
+#define AGN_OPT_ADAM 1
+int agn_set_optimizer(agn_ctx* ctx, int32_t optimizer, float beta1, float beta2, float eps);
+
 /* Enqueue one AGN round.  commit_order: HOST, n entries, a permutation of
  * 0..n-1 (checked on the host; AGN_EINVAL leaves the state unchanged).
  * The j-th entry is the worker whose normalized delta is the j-th to be
@@ -181,9 +196,10 @@ int agn_debug_batch_indices(agn_ctx* ctx, int32_t worker, int64_t step_t,
  * context launches it: flops = 2 * multiply-adds of the class's matrix
  * products; bytes = the memory traffic the class cannot avoid (for the
  * commit: central + n deltas read, n pulled copies + central written;
- * for the classes with the SGD update: the parameters they update read and
+ * for the classes with the update: the parameters they update read and
  * written once per local step, plus their bf16 shadow written in bf16
- * mode; for the output layer: its activations read and gradients written).
+ * mode and Adam's two moment estimates read and written; for the output
+ * layer: its activations read and gradients written).
  * HOST outputs. */
 int agn_kernel_class_work(agn_ctx* ctx, int32_t kernel_class, double* flops,
                           double* bytes);

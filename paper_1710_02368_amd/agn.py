@@ -28,6 +28,7 @@ EXPORTED = [
     "agn_num_params", "agn_last_error", "agn_destroy", "agn_set_central",
     "agn_worker_params", "agn_debug_batch_indices", "agn_set_kernel_timing",
     "agn_kernel_timing", "agn_kernel_class_work", "agn_debug_delta", "agn_set_normalization",
+    "agn_set_optimizer",
 ]
 
 
@@ -65,6 +66,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                              ctypes.POINTER(vp)]),
         "agn_set_stream": (i32, [vp, vp]),
         "agn_set_normalization": (i32, [vp, i32]),
+        "agn_set_optimizer": (i32, [vp, i32, ctypes.c_float, ctypes.c_float, ctypes.c_float]),
         "agn_round": (i32, [vp, ctypes.POINTER(agn_data), ctypes.POINTER(ctypes.c_int32)]),
         "agn_central": (i32, [vp, vp]),
         "agn_loss": (i32, [vp, vp]),
@@ -121,6 +123,13 @@ def agn_create(dims: Sequence[int], batch: int, n: int, lam: int, eta: float, se
 
 def agn_set_normalization(ctx, normalize: bool):
     _check(load_library().agn_set_normalization(ctx, int(bool(normalize))), ctx)
+
+
+AGN_OPT_SGD, AGN_OPT_ADAM = 0, 1
+
+
+def agn_set_optimizer(ctx, optimizer: int, beta1=0.9, beta2=0.999, eps=1e-8):
+    _check(load_library().agn_set_optimizer(ctx, int(optimizer), float(beta1), float(beta2), float(eps)), ctx)
 
 
 def agn_set_stream(ctx, stream_ptr=None):
@@ -197,7 +206,8 @@ def agn_kernel_class_work(ctx, kernel_class: int):
 class AGN:
     """One AGN context on the current ROCm device and stream."""
 
-    def __init__(self, dims, n, lam, eta, m, seed, dtype="fp32", normalize=True):
+    def __init__(self, dims, n, lam, eta, m, seed, dtype="fp32", normalize=True, adam=None):
+        """adam: None (SGD) or (beta1, beta2, eps)."""
         self.dims = tuple(int(d) for d in dims)
         self.n, self.lam, self.m = int(n), int(lam), int(m)
         self.dtype = AGN_BF16 if dtype == "bf16" else AGN_FP32
@@ -205,6 +215,8 @@ class AGN:
         agn_set_stream(self.ctx)
         if not normalize:
             agn_set_normalization(self.ctx, False)
+        if adam is not None:
+            agn_set_optimizer(self.ctx, AGN_OPT_ADAM, *adam)
         self.P = agn_num_params(self.ctx)
 
     def close(self):

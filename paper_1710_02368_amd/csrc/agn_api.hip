@@ -67,6 +67,10 @@ struct agn_ctx {
   int device = 0;
   int use_head = 0;  // fused output-layer kernels (few classes)
   int normalize = 1; // commit a / lambda (AGN) or a (DOWNPOUR with local exploration)
+  int optimizer = AGN_OPT_SGD;
+  float beta1 = 0.f, beta2 = 0.f, adam_eps = 0.f;
+  float* mom_m = nullptr;  // Adam moment estimates [n][P_pad] (allocated on selection)
+  float* mom_v = nullptr;
   int capturing = 0;
   hipStream_t ls = nullptr;           // stream the launch sequence is enqueued on
   int poisoned = 0;
@@ -167,6 +171,21 @@ int set_device(agn_ctx* c) {
 
 // One local step of every worker: forward, softmax cross-entropy, backward
 // with the SGD update fused into the weight-gradient products.
+// Adam arguments of layer l's weight-gradient epilogue (off when SGD)
+AdamArgs adam_args(const agn_ctx* c, int l) {
+  AdamArgs a{};
+  if (c->optimizer != AGN_OPT_ADAM) return a;
+  a.mw = c->mom_m + c->woff[l];
+  a.vw = c->mom_v + c->woff[l];
+  a.mb = c->mom_m + c->boff[l];
+  a.vb = c->mom_v + c->boff[l];
+  a.beta1 = c->beta1;
+  a.beta2 = c->beta2;
+  a.eps = c->adam_eps;
+  a.on = 1;
+  return a;
+}
+
 int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
   const int L = c->L, m = c->m, n = c->n;
   const bool bf = c->dtype == AGN_BF16;
@@ -260,6 +279,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     w.eta = c->eta;
     w.lam = c->normalize ? (float)c->lam : 1.f;  // divisor of the committed delta
     w.last = last;
+    w.adam = adam_args(c, L - 1);
     HIP_CHECK(c, timed(c, AGN_K_OUTPUT_DW, [&] { return launch_head_dw(w, c->ls); }));
   } else {
     // softmax cross-entropy: per-row loss and the output gradient dZ_L
@@ -309,6 +329,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     w.lam = c->normalize ? (float)c->lam : 1.f;  // divisor of the committed delta
     w.last = last;
     w.zero = c->zero;
+    w.adam = adam_args(c, l);
     if (l >= 1) {  // dZ_l = (dZ_{l+1} W_l) * [H_l > 0]
       GemmArgs x{};
       x.M = m;
@@ -483,6 +504,34 @@ int agn_set_normalization(agn_ctx* c, int32_t normalize) {
   return AGN_OK;
 }
 
+int agn_set_optimizer(agn_ctx* c, int32_t optimizer, float beta1, float beta2, float eps) {
+  if (int r = check_ctx(c)) return r;
+  if (optimizer != AGN_OPT_SGD && optimizer != AGN_OPT_ADAM) return fail(c, AGN_EINVAL, "unknown optimizer");
+  if (optimizer == AGN_OPT_ADAM) {
+    if (!(beta1 >= 0.f && beta1 < 1.f) || !(beta2 >= 0.f && beta2 < 1.f))
+      return fail(c, AGN_EINVAL, "Adam betas must lie in [0, 1)");
+    if (!(eps > 0.f) || !std::isfinite(eps)) return fail(c, AGN_EINVAL, "Adam eps must be positive and finite");
+  }
+  if (c->rounds != 0) return fail(c, AGN_ESTATE, "agn_set_optimizer is allowed only before the first round");
+  if (int r = set_device(c)) return r;
+  if (optimizer == AGN_OPT_ADAM && !c->mom_m) {
+    const int64_t cnt = (int64_t)c->n * c->P_pad;
+    if (dalloc(c, &c->mom_m, cnt) != hipSuccess || dalloc(c, &c->mom_v, cnt) != hipSuccess)
+      return fail(c, AGN_ENOMEM, "cannot allocate the Adam moment buffers");
+  }
+  if (optimizer == AGN_OPT_ADAM) {  // moments start at zero
+    HIP_CHECK(c, hipMemsetAsync(c->mom_m, 0, (size_t)c->n * c->P_pad * sizeof(float), c->stream));
+    HIP_CHECK(c, hipMemsetAsync(c->mom_v, 0, (size_t)c->n * c->P_pad * sizeof(float), c->stream));
+    HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  }
+  c->optimizer = optimizer;
+  c->beta1 = beta1;
+  c->beta2 = beta2;
+  c->adam_eps = eps;
+  drop_graph(c);
+  return AGN_OK;
+}
+
 int agn_round(agn_ctx* c, const agn_data* d, const int32_t* order) {
   if (int r = check_ctx(c)) return r;
   if (!d || !d->x || !d->y) return fail(c, AGN_EINVAL, "data, data->x and data->y must be non-NULL");
@@ -622,8 +671,10 @@ int agn_kernel_class_work(agn_ctx* c, int32_t cls, double* flops, double* bytes)
   auto mac = [&](int l) { return (double)c->dims[l] * c->dims[l + 1]; };
   const double C = c->dims[L];
   const double xb = c->dtype == AGN_BF16 ? 2.0 : 4.0;
-  // updated parameters: read + write per local step (+ bf16 shadow write)
-  const double upd = (c->dtype == AGN_BF16 ? 10.0 : 8.0) * (double)c->n * c->lam;
+  // updated parameters: read + write per local step (+ bf16 shadow write,
+  // + Adam's two moment estimates read and written)
+  const double upd = ((c->dtype == AGN_BF16 ? 10.0 : 8.0) + (c->optimizer == AGN_OPT_ADAM ? 16.0 : 0.0)) *
+                     (double)c->n * c->lam;
   double f = 0.0, b = 0.0;
   switch (cls) {
     case AGN_K_FWD:

@@ -33,6 +33,19 @@ enum Epilogue : int32_t {
                        // (last step: store (new - snapshot) / lambda instead)
 };
 
+// Adam as the local rule (weight-gradient epilogues): moment estimates of
+// the layer's weights (mw, vw) and bias (mb, vb), laid out like the
+// parameters ([n][P_pad], worker stride pstride), updated in place; the
+// bias corrections use the worker's local step t = round*lambda + step + 1.
+struct AdamArgs {
+  float* mw;
+  float* vw;
+  float* mb;
+  float* vb;
+  float beta1, beta2, eps;
+  int32_t on;
+};
+
 struct GemmArgs {
   int32_t M, N, K, batch;
   Operand a;  // A[M][K]: stored [M][K] when a_kc, else [K][M]
@@ -58,6 +71,7 @@ struct GemmArgs {
   float eta, lam;
   int32_t last;
   const float* zero;  // a zeroed page (operand reads past an edge)
+  AdamArgs adam;      // EPI_DW_UPDATE: Adam instead of SGD when adam.on
 };
 
 // launchers (return hipError_t of the launch)
@@ -122,6 +136,7 @@ struct HeadDwArgs {        // output-layer weight gradient + update (M = C <= 32
   int64_t ldw, pstride;
   float eta, lam;
   int32_t last;
+  AdamArgs adam;
 };
 bool head_prepare(int C, int d);
 hipError_t launch_head(const HeadArgs& a, hipStream_t s);

@@ -29,6 +29,27 @@ __device__ __forceinline__ int64_t gather_step(const Gather& g) {
   return (*g.round) * (int64_t)g.lam + g.step;
 }
 
+// Adam (Kingma & Ba 2015) bias corrections 1/(1 - beta^t) at the worker's
+// local step t = round*lambda + step + 1 (the round counter lives on the
+// device, so a recorded round stays valid in every replay).
+struct AdamCoef {
+  float c1, c2;
+};
+__device__ __forceinline__ AdamCoef adam_coef(const Gather& g, const AdamArgs& a) {
+  const double t = (double)(*g.round) * g.lam + g.step + 1;
+  return {(float)(1.0 / (1.0 - pow((double)a.beta1, t))), (float)(1.0 / (1.0 - pow((double)a.beta2, t)))};
+}
+// One Adam moment update of element e (in place); returns the step
+// direction mhat / (sqrt(vhat) + eps), to be scaled by -eta.
+__device__ __forceinline__ float adam_dir(float g, float* m, float* v, int64_t e, const AdamArgs& a,
+                                          const AdamCoef& c) {
+  const float m1 = a.beta1 * m[e] + (1.f - a.beta1) * g;
+  const float v1 = a.beta2 * v[e] + (1.f - a.beta2) * g * g;
+  m[e] = m1;
+  v[e] = v1;
+  return (m1 * c.c1) / (sqrtf(v1 * c.c2) + a.eps);
+}
+
 // float32 -> bfloat16 bits, round to nearest even (finite inputs).
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);

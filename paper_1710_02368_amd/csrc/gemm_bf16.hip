@@ -156,7 +156,7 @@ __device__ __forceinline__ bool dw_vec_ok(const GemmArgs& g) {
 }
 
 __device__ __forceinline__ void dw_epilogue_lds(const GemmArgs& g, int worker, int m0, int n0, const f32x16 (&acc)[2][2],
-                                                float* et) {
+                                                float* et, const AdamCoef& ac) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1, li = lane & 31, lh = lane >> 5;
 #pragma unroll
@@ -185,9 +185,15 @@ __device__ __forceinline__ void dw_epilogue_lds(const GemmArgs& g, int worker, i
 #pragma unroll
     for (int u = 0; u < CH / 2; ++u) {
       const int c = tid + NT * (u + half * CH / 2), row = c / (TB / 4), col = 4 * (c % (TB / 4));
-      const float4 a = *reinterpret_cast<const float4*>(et + row * EPI_LD + col);
-      float4 nw = make_float4(w[u].x - g.eta * a.x, w[u].y - g.eta * a.y, w[u].z - g.eta * a.z, w[u].w - g.eta * a.w);
+      float4 a = *reinterpret_cast<const float4*>(et + row * EPI_LD + col);
       if (!ok[u]) continue;
+      if (g.adam.on) {
+        a.x = adam_dir(a.x, g.adam.mw, g.adam.vw, e[u], g.adam, ac);
+        a.y = adam_dir(a.y, g.adam.mw, g.adam.vw, e[u] + 1, g.adam, ac);
+        a.z = adam_dir(a.z, g.adam.mw, g.adam.vw, e[u] + 2, g.adam, ac);
+        a.w = adam_dir(a.w, g.adam.mw, g.adam.vw, e[u] + 3, g.adam, ac);
+      }
+      float4 nw = make_float4(w[u].x - g.eta * a.x, w[u].y - g.eta * a.y, w[u].z - g.eta * a.z, w[u].w - g.eta * a.w);
       if (g.last) {
         nw = make_float4((nw.x - sn[u].x) / g.lam, (nw.y - sn[u].y) / g.lam, (nw.z - sn[u].z) / g.lam,
                          (nw.w - sn[u].w) / g.lam);
@@ -277,9 +283,10 @@ __device__ __forceinline__ void gemm_tile16(const GemmArgs& g, const int logical
     __syncthreads();
   }
 
+  const AdamCoef ac = (EPI == EPI_DW_UPDATE && g.adam.on) ? adam_coef(g.g, g.adam) : AdamCoef{1.f, 1.f};
   if (EPI == EPI_DW_UPDATE && dw_vec_ok(g)) {
     // (the K loop ended with a barrier: the operand tiles are free)
-    dw_epilogue_lds(g, worker, m0, n0, acc, reinterpret_cast<float*>(lds));
+    dw_epilogue_lds(g, worker, m0, n0, acc, reinterpret_cast<float*>(lds), ac);
   } else {
   // epilogue: block (bi, bj) lane holds D[i][j], j = lane%32,
   // i = 8*(r/4) + 4*(lane/32) + r%4 within the 32x32 block
@@ -309,7 +316,8 @@ __device__ __forceinline__ void gemm_tile16(const GemmArgs& g, const int logical
               f32_to_bf16_rne(on ? v : 0.f);
         } else {  // EPI_DW_UPDATE
           const int64_t e = (int64_t)worker * g.pstride + (int64_t)row * g.ldw + col;
-          const float nw = g.w_src[e] - g.eta * v;
+          const float step = g.adam.on ? adam_dir(v, g.adam.mw, g.adam.vw, e, g.adam, ac) : v;
+          const float nw = g.w_src[e] - g.eta * step;
           if (g.last) {
             g.w_dst[e] = (nw - g.w_snap[e]) / g.lam;
           } else {
@@ -325,7 +333,8 @@ __device__ __forceinline__ void gemm_tile16(const GemmArgs& g, const int logical
     const int o = m0 + tid;
     if (o < g.M) {
       const int64_t e = (int64_t)worker * g.pstride + o;
-      const float nb = g.b_src[e] - g.eta * bsum;
+      const float step = g.adam.on ? adam_dir(bsum, g.adam.mb, g.adam.vb, e, g.adam, ac) : bsum;
+      const float nb = g.b_src[e] - g.eta * step;
       g.b_dst[e] = g.last ? (nb - g.b_snap[e]) / g.lam : nb;
     }
   }

@@ -264,13 +264,15 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, const int logical, 
       }
     }
   } else {  // EPI_DW_UPDATE: rows are output units o, columns input units i
+    const AdamCoef ac = g.adam.on ? adam_coef(g.g, g.adam) : AdamCoef{1.f, 1.f};
     if (col < g.N) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = m0 + wm * 32 + 8 * (r >> 2) + 4 * lh + (r & 3);
         if (row < g.M) {
           const int64_t e = wo + (int64_t)row * g.ldw + col;
-          const float nw = pre[r] - g.eta * acc[r];
+          const float step = g.adam.on ? adam_dir(acc[r], g.adam.mw, g.adam.vw, e, g.adam, ac) : acc[r];
+          const float nw = pre[r] - g.eta * step;
           g.w_dst[e] = g.last ? (nw - pre2[r]) / g.lam : nw;
         }
       }
@@ -279,7 +281,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& g, const int logical, 
       const int o = m0 + tid;
       if (o < g.M) {
         const int64_t e = wo + o;
-        const float nb = g.b_src[e] - g.eta * bsum;
+        const float step = g.adam.on ? adam_dir(bsum, g.adam.mb, g.adam.vb, e, g.adam, ac) : bsum;
+        const float nb = g.b_src[e] - g.eta * step;
         g.b_dst[e] = g.last ? (nb - g.b_snap[e]) / g.lam : nb;
       }
     }

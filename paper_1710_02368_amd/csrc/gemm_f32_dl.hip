@@ -662,7 +662,7 @@ bool operand_ok(const Operand& op, bool kc, int outer_n, int K) {
 // weight-gradient product: K-strided operands (B may be gathered when the
 // batch fits in a shard), at least NS K steps, 16-byte epilogue rows
 bool dw_ok(const GemmArgs& g) {
-  if (g.epi != EPI_DW_UPDATE || !g.zero) return false;
+  if (g.epi != EPI_DW_UPDATE || !g.zero || g.adam.on) return false;  // (Adam: register-staged kernel)
   const Operand& a = g.a;
   const Operand& b = g.b;
   if (!a.vec || !b.vec || a.gather || !aligned16(a.ptr) || !aligned16(b.ptr)) return false;

@@ -230,13 +230,15 @@ __global__ __launch_bounds__(64 * HDW_WAVES) void head_dw_kernel(HeadDwArgs a) {
   if (ib == 0 && bg < HDW_BG) bpart[bg][bc] = bsum;
   __syncthreads();
   const int64_t wo = (int64_t)k * a.pstride;
+  const AdamCoef ac = a.adam.on ? adam_coef(a.g, a.adam) : AdamCoef{1.f, 1.f};
   for (int c = wave; c < C; c += HDW_WAVES) {
     float g = part[0][c][lane];
 #pragma unroll
     for (int w = 1; w < HDW_WAVES; ++w) g += part[w][c][lane];
     if (i < a.d) {
       const int64_t e = wo + (int64_t)c * a.ldw + i;
-      const float nw = a.w_src[e] - a.eta * g;
+      const float step = a.adam.on ? adam_dir(g, a.adam.mw, a.adam.vw, e, a.adam, ac) : g;
+      const float nw = a.w_src[e] - a.eta * step;
       a.w_dst[e] = a.last ? (nw - a.w_snap[e]) / a.lam : nw;
     }
   }
@@ -245,7 +247,8 @@ __global__ __launch_bounds__(64 * HDW_WAVES) void head_dw_kernel(HeadDwArgs a) {
 #pragma unroll
     for (int q = 1; q < HDW_BG; ++q) gb += bpart[q][tid];
     const int64_t e = wo + tid;
-    const float nb = a.b_src[e] - a.eta * gb;
+    const float step = a.adam.on ? adam_dir(gb, a.adam.mb, a.adam.vb, e, a.adam, ac) : gb;
+    const float nb = a.b_src[e] - a.eta * step;
     a.b_dst[e] = a.last ? (nb - a.b_snap[e]) / a.lam : nb;
   }
 }
