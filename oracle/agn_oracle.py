@@ -57,7 +57,7 @@ import numpy as np
 
 __all__ = [
     "splitmix64", "he_normal_init", "bf16_round", "batch_indices",
-    "loss_and_grads", "AGNOracle", "flat_params", "unflat_params",
+    "loss_and_grads", "forward", "evaluate", "AGNOracle", "flat_params", "unflat_params",
 ]
 
 _GAMMA = np.uint64(0x9E3779B97F4A7C15)
@@ -162,6 +162,24 @@ def batch_indices(k: int, t: int, m: int, S: int) -> np.ndarray:
 # Mini-batch loss and gradient of the ReLU MLP (the gradient term of Eq. 1)
 # ---------------------------------------------------------------------------
 
+def forward(params, xb: np.ndarray, prec: _Prec):
+    """Forward pass of the ReLU MLP over the rows of xb.
+
+    Returns (H, logits): H[0] is the input batch, H[l+1] =
+    relu(H[l] W_l^T + b_l) for the hidden layers (bf16-rounded in bf16
+    mode, as operands of the next product), and the stored logits
+    H[L-1] W_{L-1}^T + b_{L-1}."""
+    L = len(params)
+    H = [prec.op(np.asarray(xb, dtype=prec.dtype))]
+    for l in range(L - 1):
+        W, b = params[l]
+        z = prec.st(prec.mm(H[l], prec.op(W).T) + b)
+        H.append(prec.op(np.maximum(z, 0)))
+    W, b = params[L - 1]
+    logits = prec.st(prec.mm(H[L - 1], prec.op(W).T) + b)
+    return H, logits
+
+
 def loss_and_grads(params, xb: np.ndarray, yb: np.ndarray, prec: _Prec):
     """Mean softmax cross-entropy over the m rows of the batch and its
     gradient with respect to every W_l and b_l (Eq. 1: the inner average
@@ -170,14 +188,7 @@ def loss_and_grads(params, xb: np.ndarray, yb: np.ndarray, prec: _Prec):
     Returns (loss as float64, [(dW_0, db_0), ...])."""
     L = len(params)
     m = xb.shape[0]
-    # forward: H[0] is the input batch, H[l+1] = relu(H[l] W_l^T + b_l)
-    H = [prec.op(np.asarray(xb, dtype=prec.dtype))]
-    for l in range(L - 1):
-        W, b = params[l]
-        z = prec.st(prec.mm(H[l], prec.op(W).T) + b)
-        H.append(prec.op(np.maximum(z, 0)))
-    W, b = params[L - 1]
-    logits = prec.st(prec.mm(H[L - 1], prec.op(W).T) + b)
+    H, logits = forward(params, xb, prec)
 
     # softmax cross-entropy, evaluated in float64 from the stored logits
     z = logits.astype(np.float64)
@@ -202,6 +213,34 @@ def loss_and_grads(params, xb: np.ndarray, yb: np.ndarray, prec: _Prec):
             back = prec.st(prec.mm(dzq, prec.op(params[l][0])))
             dz = back * (H[l] > 0)           # ReLU'(0) = 0
     return loss, grads
+
+
+# ---------------------------------------------------------------------------
+# Evaluation of a model over a labelled set (Section 4: the training and
+# validation accuracy of the central variable, the f(t) of Eq. 4)
+# ---------------------------------------------------------------------------
+
+def evaluate(params, X: np.ndarray, y: np.ndarray, bf16: bool = False, dtype=np.float32):
+    """Per-row softmax cross-entropy and predicted class of the model
+    ``params`` on every row of (X, y).
+
+    The logits are those of ``forward`` (stored in the storage type); the
+    loss of row j is logsumexp(z_j) - z_{j,y_j}, evaluated in float64 from
+    them; the prediction is the index of the largest logit, the lowest such
+    index when several are equal.  Returns (row_loss float64 [N],
+    pred int64 [N], logits [N][C])."""
+    prec = _Prec(dtype, bf16)
+    X = np.asarray(X)
+    if X.dtype == np.uint16:                          # bf16 bit patterns
+        X = (X.astype(np.uint32) << np.uint32(16)).view(np.float32)
+    y = np.asarray(y, dtype=np.int64)
+    _, logits = forward(params, X, prec)
+    z = logits.astype(np.float64)
+    zmax = z.max(axis=1, keepdims=True)
+    lse = zmax[:, 0] + np.log(np.exp(z - zmax).sum(axis=1))
+    row_loss = lse - z[np.arange(z.shape[0]), y]
+    pred = np.argmax(logits, axis=1).astype(np.int64)   # first maximum on ties
+    return row_loss, pred, logits
 
 
 # ---------------------------------------------------------------------------
