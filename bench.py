@@ -1,6 +1,7 @@
 """Benchmark of the AGN hot path on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+    python bench.py --mode eval [--workload NAME]     (evaluation only)
 
 One step is one AGN round: lambda local SGD steps of all n workers
 (forward, softmax cross-entropy, backward with the fused update) and the
@@ -14,6 +15,12 @@ bounded sample on the host cores.  The timed region replays the captured
 round graph; the dominant class's average launch duration comes from HIP
 events around each of its launches in an eager pass of the same kernels on
 the same stream right after the timed region.
+
+The line also carries "eval": the evaluation of the central variable on a
+held-out set of 10,000 rows (the f(t) of the paper's Eq. 4 curves), in
+rows per second, with the roofline of its forward products and the
+oracle's evaluation timed on the host.  --mode eval runs only that part
+(for a profile that holds only the evaluation's kernels).
 """
 from __future__ import annotations
 
@@ -84,6 +91,60 @@ def cpu_baseline(wl, X, y, orders, budget_s=12.0, adam=None):
                       f"worker-samples) in {dt:.1f} s, float32 storage / float64 accumulation"}
 
 
+def measure_eval(agn, g, wl, xh, yh, Xh, yh_host, reps=20, cpu=True):
+    """Held-out evaluation of the central variable: rows/s over `reps`
+    calls (inputs resident in HBM, one stream synchronization at the end),
+    the roofline of the forward products (their launches bracketed by HIP
+    events in a separate pass), and the oracle's evaluation on the host."""
+    import torch
+    rows = int(xh.shape[0])
+    for _ in range(2):
+        g.evaluate(xh, yh)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        agn.agn_evaluate(g.ctx, xh, yh, rows, g.dtype, want_result=False)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / reps
+    res = g.evaluate(xh, yh)
+    k = agn.KERNEL_CLASSES["eval"]
+    agn.agn_set_kernel_timing(g.ctx, k, True)
+    kt = 5
+    for _ in range(kt):
+        agn.agn_evaluate(g.ctx, xh, yh, rows, g.dtype, want_result=False)
+    ms, cnt = agn.agn_kernel_timing(g.ctx, k)
+    agn.agn_set_kernel_timing(g.ctx, k, False)
+    flops, nbytes = agn.agn_kernel_class_work(g.ctx, k)
+    per_call_s = ms * 1e-3 / kt
+    dtype = wl.dtype
+    tf = flops / per_call_s / 1e12
+    out = {"rows": rows, "rows_per_s": round(rows / dt, 1), "ms_per_eval": round(dt * 1e3, 4),
+           "mean_loss": round(res[0], 6), "accuracy": res[1],
+           "roofline": {"bound": bound_of({"flops": flops, "bytes": nbytes}, dtype),
+                        "achieved": round(tf, 3), "peak": PEAK_TFLOPS[dtype], "unit": "TFLOP/s",
+                        "frac": round(tf / PEAK_TFLOPS[dtype], 4), "kernel_class": "eval",
+                        "launches_per_eval": cnt // kt,
+                        "avg_launch_us": round(ms * 1e3 / max(cnt, 1), 2),
+                        "algorithmic_per_eval": flops}}
+    if cpu:
+        from oracle import evaluate
+        try:
+            from threadpoolctl import threadpool_info
+            threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        except Exception:
+            threads = len(os.sched_getaffinity(0))
+        # the initial model's parameters (the library draws the same ones)
+        from oracle import he_normal_init
+        params = he_normal_init(wl.dims, wl.seed)
+        t0 = time.perf_counter()
+        evaluate(params, Xh, yh_host, bf16=dtype == "bf16")
+        ct = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": round(rows / ct, 1), "unit": "rows/s", "cores": int(threads),
+                               "kind": "oracle",
+                               "sample": f"{rows} held-out rows evaluated once in {ct:.2f} s"}
+    return out
+
+
 KERNEL_SOURCES = os.path.join(ROOT, "paper_1710_02368_amd", "csrc")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
@@ -137,6 +198,8 @@ def main():
                     help="local rule: plain SGD (the paper's Eq. 1) or Adam (beta 0.9/0.999, eps 1e-8)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--mode", choices=["round", "eval"], default="round",
+                    help="round: the AGN round (default line, with the evaluation); eval: evaluation only")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration)")
     args = ap.parse_args()
@@ -161,6 +224,24 @@ def main():
     adam = ADAM if args.optimizer == "adam" else None
     g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, dtype=wl.dtype, adam=adam)
     order_at = lambda i: orders[i % len(orders)]
+    Xh, yh = W.make_heldout(wl)
+    xh = torch.from_numpy(Xh.view(np.int16) if Xh.dtype == np.uint16 else Xh).cuda()
+    yh_d = torch.from_numpy(yh).cuda()
+
+    if args.mode == "eval":
+        ev = measure_eval(agn, g, wl, xh, yh_d, Xh, yh, reps=max(args.steps, 1),
+                          cpu=not args.no_cpu_baseline)
+        out = {"metric": "held-out rows/sec evaluated (central variable, forward + loss + argmax)",
+               "value": ev["rows_per_s"], "unit": "rows/s", "n_gpus": 1, "steps": max(args.steps, 1),
+               "warmup": 2, "ms_per_step": ev["ms_per_eval"], "higher_is_better": True, "scaling": "weak",
+               "vs_baseline": None, "dtype": "f32" if wl.dtype == "fp32" else "bf16", "data": "synthetic",
+               "config": {"workload": wl.name + "_heldout", "dims": list(wl.dims), "rows": ev["rows"]},
+               "roofline": dict(ev["roofline"], traffic=None)}
+        if "cpu_baseline" in ev:
+            out["cpu_baseline"] = ev["cpu_baseline"]
+        g.close()
+        print(json.dumps(out), flush=True)
+        return
 
     for i in range(args.warmup):
         g.round(xd, yd, order_at(i))
@@ -215,6 +296,9 @@ def main():
     agn.agn_set_kernel_timing(g.ctx, agn.KERNEL_CLASSES["commit"], False)
     torch.cuda.synchronize()
 
+    # evaluation of the trained central variable on the held-out set
+    ev = measure_eval(agn, g, wl, xh, yh_d, Xh, yh, cpu=not args.no_cpu_baseline)
+
     value = args.steps * wl.worker_samples_per_round / dt
     wd = work[dominant]
     bound = bound_of(wd, wl.dtype)
@@ -252,6 +336,7 @@ def main():
                             "traffic": stored_traffic(wl.name, "commit")},
         "round_mfma_util": round(wl.flops_per_round / (dt / args.steps) / 1e12 / PEAK_TFLOPS[wl.dtype], 4),
         "kernels": breakdown,
+        "eval": ev,
     }
     g.close()
     if not args.no_cpu_baseline:

@@ -141,6 +141,47 @@ int agn_central(agn_ctx* ctx, float* out);
  * AGN_ESTATE before the first round. */
 int agn_loss(agn_ctx* ctx, float* out);
 
+/* Result of agn_evaluate. */
+typedef struct {
+  double mean_loss;  /* mean over the rows of the softmax cross-entropy     */
+  double accuracy;   /* correct / num_samples                               */
+  int64_t correct;   /* rows whose predicted class equals the label         */
+} agn_eval_result;
+
+/* Evaluate the central variable on a labelled set: Section 4 follows the
+ * training and validation accuracy of the central model over time (the
+ * f(t) of Eq. 4).  data: the rows to evaluate, x and y as for agn_round
+ * (num_samples >= 1, not split into shards, x_dtype as for agn_round).
+ * For every row: the logits of the MLP at the central variable (the same
+ * forward products as a training step; bfloat16 operands in AGN_BF16
+ * contexts), the softmax cross-entropy logsumexp(z) - z_y and the
+ * predicted class argmax z (the lowest index among equal maxima; a NaN
+ * logit counts as larger than any number).
+ *   row_loss: DEVICE, num_samples floats, or NULL.
+ *   row_pred: DEVICE, num_samples int32, or NULL.
+ *   out:      HOST, or NULL.  The mean loss is summed in float64 in a
+ *             fixed order: repeated calls give identical results.
+ * Rows go through the forward pass 8192 at a time in the evaluation's own
+ * workspace, which the first call allocates (activations of 8192 rows, two
+ * buffers of the widest hidden layer; AGN_ENOMEM if that fails) and no
+ * round touches: a call between rounds changes nothing a round reads.  It
+ * works before the first round (the initial model).  With out != NULL the
+ * call waits for the stream; with out == NULL it returns after enqueueing. */
+int agn_evaluate(agn_ctx* ctx, const agn_data* data, float* row_loss, int32_t* row_pred,
+                 agn_eval_result* out);
+
+/* Temporal efficiency E(a, b) of Eq. 4 (Section 4): the area under
+ * performance curve f_a over the area under f_b, both over [0, tm] with tm
+ * the minimal shared training time, min(last time of a, last time of b).
+ * A curve is n >= 2 samples (t_i, f_i), HOST arrays: t_0 = 0 < t_1 < ...,
+ * all finite; between samples f is the straight line (trapezoid rule), and
+ * the curve that runs longer is cut at tm on the line through the samples
+ * around it.  *out = area_a / area_b (HOST).  AGN_EINVAL for a bad curve or
+ * a zero area of b; the message is agn_last_error(NULL).  Host arithmetic
+ * only: no context and no device work. */
+int agn_temporal_efficiency(const double* t_a, const double* f_a, int64_t n_a, const double* t_b,
+                            const double* f_b, int64_t n_b, double* out);
+
 /* Number of parameters P (-1 for a NULL context). */
 int64_t agn_num_params(const agn_ctx* ctx);
 
@@ -190,7 +231,9 @@ int agn_debug_batch_indices(agn_ctx* ctx, int32_t worker, int64_t step_t,
                              gathered from the data set) fused with the SGD
                              update                                          */
 #define AGN_K_COMMIT 5    /* normalize + commit + pull                       */
-#define AGN_K_NUM 6
+#define AGN_K_EVAL 6      /* agn_evaluate's forward products (not part of a
+                             round)                                          */
+#define AGN_K_NUM 7
 
 /* Algorithmic work of one round attributed to a kernel class, as this
  * context launches it: flops = 2 * multiply-adds of the class's matrix
@@ -199,7 +242,9 @@ int agn_debug_batch_indices(agn_ctx* ctx, int32_t worker, int64_t step_t,
  * for the classes with the update: the parameters they update read and
  * written once per local step, plus their bf16 shadow written in bf16
  * mode and Adam's two moment estimates read and written; for the output
- * layer: its activations read and gradients written).
+ * layer: its activations read and gradients written).  AGN_K_EVAL: the
+ * work of the last agn_evaluate call instead (its rows' inputs and the
+ * weights read once, the logits written once), zero before the first.
  * HOST outputs. */
 int agn_kernel_class_work(agn_ctx* ctx, int32_t kernel_class, double* flops,
                           double* bytes);

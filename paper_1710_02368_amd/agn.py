@@ -19,16 +19,16 @@ LIB_PATH = os.path.join(_PKG, "libagn.so")
 
 AGN_OK, AGN_EINVAL, AGN_ENOMEM, AGN_EHIP, AGN_ESTATE = 0, -1, -2, -3, -4
 AGN_FP32, AGN_BF16 = 0, 1
-AGN_K_FWD, AGN_K_OUTPUT, AGN_K_OUTPUT_DW, AGN_K_BWD, AGN_K_DW_FIRST, AGN_K_COMMIT = range(6)
+AGN_K_FWD, AGN_K_OUTPUT, AGN_K_OUTPUT_DW, AGN_K_BWD, AGN_K_DW_FIRST, AGN_K_COMMIT, AGN_K_EVAL = range(7)
 KERNEL_CLASSES = {"fwd": AGN_K_FWD, "output": AGN_K_OUTPUT, "output_dw": AGN_K_OUTPUT_DW, "bwd": AGN_K_BWD,
-                  "dw_first": AGN_K_DW_FIRST, "commit": AGN_K_COMMIT}
+                  "dw_first": AGN_K_DW_FIRST, "commit": AGN_K_COMMIT, "eval": AGN_K_EVAL}
 
 EXPORTED = [
     "agn_create", "agn_set_stream", "agn_round", "agn_central", "agn_loss",
     "agn_num_params", "agn_last_error", "agn_destroy", "agn_set_central",
     "agn_worker_params", "agn_debug_batch_indices", "agn_set_kernel_timing",
     "agn_kernel_timing", "agn_kernel_class_work", "agn_debug_delta", "agn_set_normalization",
-    "agn_set_optimizer",
+    "agn_set_optimizer", "agn_evaluate", "agn_temporal_efficiency",
 ]
 
 
@@ -40,6 +40,11 @@ class agn_shapes(ctypes.Structure):
 class agn_data(ctypes.Structure):
     _fields_ = [("x", ctypes.c_void_p), ("y", ctypes.c_void_p),
                 ("num_samples", ctypes.c_int64), ("x_dtype", ctypes.c_int32)]
+
+
+class agn_eval_result(ctypes.Structure):
+    _fields_ = [("mean_loss", ctypes.c_double), ("accuracy", ctypes.c_double),
+                ("correct", ctypes.c_int64)]
 
 
 class AGNError(RuntimeError):
@@ -68,6 +73,10 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "agn_set_normalization": (i32, [vp, i32]),
         "agn_set_optimizer": (i32, [vp, i32, ctypes.c_float, ctypes.c_float, ctypes.c_float]),
         "agn_round": (i32, [vp, ctypes.POINTER(agn_data), ctypes.POINTER(ctypes.c_int32)]),
+        "agn_evaluate": (i32, [vp, ctypes.POINTER(agn_data), vp, vp, ctypes.POINTER(agn_eval_result)]),
+        "agn_temporal_efficiency": (i32, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), i64,
+                                          ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), i64,
+                                          ctypes.POINTER(ctypes.c_double)]),
         "agn_central": (i32, [vp, vp]),
         "agn_loss": (i32, [vp, vp]),
         "agn_num_params": (i64, [vp]),
@@ -145,6 +154,32 @@ def agn_round(ctx, x, y, num_samples: int, commit_order, x_dtype: int = AGN_FP32
 
 def agn_central(ctx, out):
     _check(load_library().agn_central(ctx, ctypes.c_void_p(out.data_ptr())), ctx)
+
+
+def agn_evaluate(ctx, x, y, num_samples: int, x_dtype: int = AGN_FP32, row_loss=None, row_pred=None,
+                 want_result: bool = True):
+    """Returns (mean_loss, accuracy, correct) when want_result, else None
+    (the call then returns without waiting)."""
+    data = agn_data(x.data_ptr(), y.data_ptr(), int(num_samples), int(x_dtype))
+    res = agn_eval_result()
+    _check(load_library().agn_evaluate(
+        ctx, ctypes.byref(data),
+        ctypes.c_void_p(row_loss.data_ptr()) if row_loss is not None else None,
+        ctypes.c_void_p(row_pred.data_ptr()) if row_pred is not None else None,
+        ctypes.byref(res) if want_result else None), ctx)
+    return (res.mean_loss, res.accuracy, res.correct) if want_result else None
+
+
+def agn_temporal_efficiency(t_a, f_a, t_b, f_b) -> float:
+    """E(a, b) of Eq. 4 from two sampled curves (host arrays)."""
+    arrs = [np.ascontiguousarray(v, dtype=np.float64) for v in (t_a, f_a, t_b, f_b)]
+    if arrs[0].shape != arrs[1].shape or arrs[2].shape != arrs[3].shape:
+        raise ValueError("times and values of a curve must have the same length")
+    p = [a.ctypes.data_as(ctypes.POINTER(ctypes.c_double)) for a in arrs]
+    out = ctypes.c_double()
+    _check(load_library().agn_temporal_efficiency(p[0], p[1], arrs[0].size, p[2], p[3], arrs[2].size,
+                                                  ctypes.byref(out)), None)
+    return out.value
 
 
 def agn_loss(ctx, out):
@@ -256,6 +291,17 @@ class AGN:
         out = torch.empty(self.P, dtype=torch.float32, device="cuda")
         agn_debug_delta(self.ctx, k, out)
         return out
+
+    def evaluate(self, x, y, row_outputs=False):
+        """Mean loss, accuracy and correct count of the central variable on
+        (x, y); with row_outputs also the per-row losses and predictions."""
+        torch = _torch()
+        if not row_outputs:
+            return agn_evaluate(self.ctx, x, y, x.shape[0], self.dtype)
+        rl = torch.empty(x.shape[0], dtype=torch.float32, device="cuda")
+        rp = torch.empty(x.shape[0], dtype=torch.int32, device="cuda")
+        res = agn_evaluate(self.ctx, x, y, x.shape[0], self.dtype, rl, rp)
+        return res, rl, rp
 
     def set_central(self, vec):
         agn_set_central(self.ctx, vec)

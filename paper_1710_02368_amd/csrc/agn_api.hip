@@ -18,6 +18,7 @@
 // and writes dst = buf[i%2]; reading and writing different buffers lets the
 // input-gradient and weight-gradient products of one layer run in either
 // order.  Nothing is allocated after agn_create.
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -71,6 +72,13 @@ struct agn_ctx {
   float beta1 = 0.f, beta2 = 0.f, adam_eps = 0.f;
   float* mom_m = nullptr;  // Adam moment estimates [n][P_pad] (allocated on selection)
   float* mom_v = nullptr;
+  // evaluation workspace (allocated by the first agn_evaluate call)
+  void* ev_h[2] = {nullptr, nullptr};  // activations of EVAL_CHUNK rows, ping-pong
+  float* ev_z = nullptr;               // logits of EVAL_CHUNK rows (unfused output layer)
+  uint16_t* ev_w16 = nullptr;          // bf16 copy of the central variable
+  double* ev_part = nullptr;           // per-block partial sums of one chunk
+  double* ev_acc = nullptr;            // loss sum and correct count over all rows
+  int64_t eval_N = 0;                  // rows of the last agn_evaluate call
   int capturing = 0;
   hipStream_t ls = nullptr;           // stream the launch sequence is enqueued on
   int poisoned = 0;
@@ -377,6 +385,136 @@ int enqueue_round(agn_ctx* c, const agn_data* d) {
   return AGN_OK;
 }
 
+// Rows the evaluation takes through its forward pass at a time: large
+// enough that each product of a 1000-wide layer spreads over several
+// workgroups per compute unit.
+constexpr int64_t EVAL_CHUNK = 8192;
+
+// The evaluation's own buffers (nothing a round uses), allocated once.
+int eval_alloc(agn_ctx* c) {
+  if (c->ev_acc) return AGN_OK;
+  const bool bf = c->dtype == AGN_BF16;
+  int64_t wmax = 0;
+  for (int l = 1; l < c->L; ++l) wmax = std::max(wmax, c->lda[l]);
+  const int64_t act = bf ? 2 : 4;
+  const int64_t blocks = std::max(eval_blocks(EVAL_CHUNK), head_eval_blocks(EVAL_CHUNK));
+  // (a failed call keeps what it got; the next call allocates the rest)
+  bool ok = true;
+  for (int i = 0; ok && i < 2 && wmax > 0; ++i) {
+    char* p = nullptr;
+    if (!c->ev_h[i]) ok = dalloc(c, &p, EVAL_CHUNK * wmax * act) == hipSuccess, c->ev_h[i] = p;
+  }
+  if (ok && !c->use_head && !c->ev_z) ok = dalloc(c, &c->ev_z, EVAL_CHUNK * c->lda[c->L]) == hipSuccess;
+  if (ok && bf && !c->ev_w16) ok = dalloc(c, &c->ev_w16, c->P_pad) == hipSuccess;
+  if (ok && !c->ev_part) ok = dalloc(c, &c->ev_part, 2 * blocks) == hipSuccess;
+  double* acc = nullptr;
+  if (ok) ok = dalloc(c, &acc, 2) == hipSuccess;
+  if (!ok) return fail(c, AGN_ENOMEM, "cannot allocate the evaluation workspace");
+  c->ev_acc = acc;  // (set last: marks the workspace complete)
+  return AGN_OK;
+}
+
+// The central variable's forward pass over data->x, EVAL_CHUNK rows at a
+// time: the hidden layers' products (bias + ReLU), then either the fused
+// output-layer kernel (logits, loss, prediction) or the logits product and
+// the per-row kernel; per-chunk partial sums are folded into ev_acc in row
+// order.
+int enqueue_eval(agn_ctx* c, const agn_data* d, float* row_loss, int32_t* row_pred) {
+  const int L = c->L;
+  const bool bf = c->dtype == AGN_BF16;
+  const int64_t N = d->num_samples, d0 = c->dims[0];
+  const int64_t xes = bf ? 2 : 4;
+  if (bf) HIP_CHECK(c, launch_copy_bf16(c->central, c->ev_w16, c->P_pad, c->ls));
+  const Gather rows_as_stored{c->round_dev, c->lam, 0, c->m, 1};  // (no gathered operand)
+  const int products = c->use_head ? L - 1 : L;
+  for (int64_t r0 = 0; r0 < N; r0 += EVAL_CHUNK) {
+    const int32_t rows = (int32_t)std::min(EVAL_CHUNK, N - r0);
+    const void* x = static_cast<const char*>(d->x) + r0 * d0 * xes;
+    const int x_vec = (d0 % (bf ? 8 : 4) == 0) && ((uintptr_t)x % 16 == 0);
+    for (int l = 0; l < products; ++l) {
+      GemmArgs g{};
+      g.M = rows;
+      g.N = c->dims[l + 1];
+      g.K = c->dims[l];
+      g.batch = 1;
+      g.a = l == 0 ? Operand{x, d0, 0, 0, x_vec} : Operand{c->ev_h[(l - 1) & 1], c->lda[l], 0, 0, 1};
+      g.b = bf ? Operand{c->ev_w16 + c->woff[l], c->ldw[l], 0, 0, 1}
+               : Operand{c->central + c->woff[l], c->ldw[l], 0, 0, 1};
+      g.g = rows_as_stored;
+      g.epi = l < L - 1 ? EPI_FWD_RELU : EPI_FWD_LINEAR;
+      g.out = l < L - 1 ? c->ev_h[l & 1] : (void*)c->ev_z;
+      g.ldo = c->lda[l + 1];
+      g.ostride = 0;
+      g.bias = c->central + c->boff[l];
+      g.bstride = 0;
+      g.zero = c->zero;
+      HIP_CHECK(c, timed(c, AGN_K_EVAL, [&] {
+        return bf ? launch_gemm_bf16(1, 1, g, c->ls) : launch_gemm_f32(1, 1, g, c->ls);
+      }));
+    }
+    int64_t blocks = 0;
+    if (c->use_head) {  // fused output layer (float32, few classes)
+      HeadArgs h{};
+      h.h = L == 1 ? static_cast<const float*>(x) : static_cast<const float*>(c->ev_h[(L - 2) & 1]);
+      h.ldh = L == 1 ? d0 : c->lda[L - 1];
+      h.hstride = 0;
+      h.gather = 0;
+      h.w = c->central + c->woff[L - 1];
+      h.b = c->central + c->boff[L - 1];
+      h.ldw = c->ldw[L - 1];
+      h.pstride = 0;
+      h.y = d->y + r0;
+      h.g = rows_as_stored;
+      h.n = 1;
+      h.m = rows;
+      h.d = c->dims[L - 1];
+      h.C = c->dims[L];
+      h.row_loss = row_loss ? row_loss + r0 : nullptr;
+      h.row_pred = row_pred ? row_pred + r0 : nullptr;
+      h.part = c->ev_part;
+      HIP_CHECK(c, timed(c, AGN_K_EVAL, [&] { return launch_head_eval(h, c->ls); }));
+      blocks = head_eval_blocks(rows);
+    } else {
+      EvalArgs e{};
+      e.z = c->ev_z;
+      e.ldz = c->lda[L];
+      e.y = d->y + r0;
+      e.rows = rows;
+      e.C = c->dims[L];
+      e.row_loss = row_loss ? row_loss + r0 : nullptr;
+      e.row_pred = row_pred ? row_pred + r0 : nullptr;
+      e.part = c->ev_part;
+      HIP_CHECK(c, launch_eval_rows(e, c->ls));
+      blocks = eval_blocks(rows);
+    }
+    HIP_CHECK(c, launch_eval_reduce(c->ev_part, blocks, c->ev_acc, r0 == 0, c->ls));
+  }
+  return AGN_OK;
+}
+
+// Eq. 4 helpers: a curve is valid when it has >= 2 finite samples starting
+// at time 0 with increasing times; its area over [0, tm] follows the
+// straight lines between samples, the segment around tm cut on its line.
+bool te_curve_ok(const double* t, const double* f, int64_t n) {
+  if (!t || !f || n < 2 || t[0] != 0.0) return false;
+  for (int64_t i = 0; i < n; ++i)
+    if (!std::isfinite(t[i]) || !std::isfinite(f[i]) || (i > 0 && !(t[i] > t[i - 1]))) return false;
+  return true;
+}
+
+double te_area(const double* t, const double* f, int64_t n, double tm) {
+  double area = 0.0;
+  for (int64_t i = 1; i < n && t[i - 1] < tm; ++i) {
+    double t1 = t[i], f1 = f[i];
+    if (t1 > tm) {
+      f1 = f[i - 1] + (f[i] - f[i - 1]) * (tm - t[i - 1]) / (t[i] - t[i - 1]);
+      t1 = tm;
+    }
+    area += 0.5 * (f[i - 1] + f1) * (t1 - t[i - 1]);
+  }
+  return area;
+}
+
 }  // namespace
 
 extern "C" {
@@ -553,7 +691,7 @@ int agn_round(agn_ctx* c, const agn_data* d, const int32_t* order) {
   // the commit order of this round (read by the commit kernel)
   HIP_CHECK(c, launch_set_order(order, c->n, c->order, c->stream));
   bool timing = false;
-  for (const auto& t : c->timing) timing = timing || t.enabled;
+  for (int k = 0; k < AGN_K_EVAL; ++k) timing = timing || c->timing[k].enabled;
   if (timing) {  // eager launches, each timed class bracketed by events
     c->ls = c->stream;
     if (int r = enqueue_round(c, d)) return r;
@@ -602,6 +740,42 @@ int agn_loss(agn_ctx* c, float* out) {
   if (int r = set_device(c)) return r;
   HIP_CHECK(c, launch_loss_reduce(c->loss, c->n, (int64_t)c->lam * c->m, out, c->stream));
   HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  return AGN_OK;
+}
+
+int agn_evaluate(agn_ctx* c, const agn_data* d, float* row_loss, int32_t* row_pred,
+                 agn_eval_result* out) {
+  if (int r = check_ctx(c)) return r;
+  if (!d || !d->x || !d->y) return fail(c, AGN_EINVAL, "data, data->x and data->y must be non-NULL");
+  if (d->x_dtype != (c->dtype == AGN_BF16 ? 1 : 0))
+    return fail(c, AGN_EINVAL, "x_dtype must be 1 for AGN_BF16 contexts and 0 otherwise");
+  if (d->num_samples < 1) return fail(c, AGN_EINVAL, "num_samples must be >= 1");
+  if (int r = set_device(c)) return r;
+  if (int r = eval_alloc(c)) return r;
+  c->ls = c->stream;
+  if (int r = enqueue_eval(c, d, row_loss, row_pred)) return r;
+  c->eval_N = d->num_samples;
+  if (out) {
+    double acc[2] = {0.0, 0.0};
+    HIP_CHECK(c, hipMemcpyAsync(acc, c->ev_acc, sizeof acc, hipMemcpyDeviceToHost, c->stream));
+    HIP_CHECK(c, hipStreamSynchronize(c->stream));
+    out->mean_loss = acc[0] / (double)d->num_samples;
+    out->correct = (int64_t)acc[1];
+    out->accuracy = (double)out->correct / (double)d->num_samples;
+  }
+  return AGN_OK;
+}
+
+int agn_temporal_efficiency(const double* t_a, const double* f_a, int64_t n_a, const double* t_b,
+                            const double* f_b, int64_t n_b, double* out) {
+  if (!out) return fail(nullptr, AGN_EINVAL, "out is NULL");
+  if (!te_curve_ok(t_a, f_a, n_a) || !te_curve_ok(t_b, f_b, n_b))
+    return fail(nullptr, AGN_EINVAL,
+                "a curve needs >= 2 finite samples, times starting at 0 and increasing");
+  const double tm = std::min(t_a[n_a - 1], t_b[n_b - 1]);
+  const double den = te_area(t_b, f_b, n_b, tm);
+  if (den == 0.0) return fail(nullptr, AGN_EINVAL, "the area under curve b is zero");
+  *out = te_area(t_a, f_a, n_a, tm) / den;
   return AGN_OK;
 }
 
@@ -709,6 +883,12 @@ int agn_kernel_class_work(agn_ctx* c, int32_t cls, double* flops, double* bytes)
     case AGN_K_COMMIT:
       b = 8.0 * (double)(c->n + 1) * c->P;  // central + n deltas in, n pulls + central out
       break;
+    case AGN_K_EVAL: {  // the last evaluation: inputs and weights read, logits written
+      const double N = (double)c->eval_N;
+      for (int l = 0; l < L; ++l) f += 2.0 * mac(l) * N;
+      b = c->eval_N > 0 ? N * (xb * c->dims[0] + 4.0 * C) + xb * (double)c->P : 0.0;
+      break;
+    }
   }
   *flops = f;
   *bytes = b;

@@ -118,6 +118,10 @@ struct HeadArgs {
   float* dprev;            // dZ_{L-1}, same layout as h (null when L == 1)
   float* loss;             // [n][lam][m]
   int32_t lam, step;
+  // evaluation variant (n = 1, rows not gathered, y = the rows' labels)
+  float* row_loss;         // [m] or null
+  int32_t* row_pred;       // [m] or null
+  double* part;            // [2 * head_eval_blocks(m)]
 };
 struct HeadDwArgs {        // output-layer weight gradient + update (M = C <= 32)
   const float* h;
@@ -141,6 +145,8 @@ struct HeadDwArgs {        // output-layer weight gradient + update (M = C <= 32
 bool head_prepare(int C, int d);
 hipError_t launch_head(const HeadArgs& a, hipStream_t s);
 hipError_t launch_head_dw(const HeadDwArgs& a, hipStream_t s);
+int64_t head_eval_blocks(int64_t rows);
+hipError_t launch_head_eval(const HeadArgs& a, hipStream_t s);
 
 struct CommitArgs {
   float* central;          // [P_pad]
@@ -174,6 +180,24 @@ hipError_t launch_set_order(const int32_t* host_order, int32_t n, int32_t* dev_o
 hipError_t launch_batch_indices(int32_t worker, int64_t t, int32_t mb, int64_t S, int64_t* out,
                                 hipStream_t s);
 hipError_t launch_copy_bf16(const float* src, uint16_t* dst, int64_t count, hipStream_t s);
+
+// Evaluation rows: per-row softmax cross-entropy and argmax of the logits,
+// with per-block partial sums for a fixed-order total.
+struct EvalArgs {
+  const float* z;      // logits [rows][ldz]
+  int64_t ldz;
+  const int32_t* y;    // labels of these rows
+  int64_t rows;
+  int32_t C;
+  float* row_loss;     // [rows] or null
+  int32_t* row_pred;   // [rows] or null
+  double* part;        // [2 * blocks]: loss sum, correct count of each block
+};
+int64_t eval_blocks(int64_t rows);
+hipError_t launch_eval_rows(const EvalArgs& a, hipStream_t s);
+// acc[0..1] (= or +=) the sums of part[0..2*blocks) in a fixed order
+hipError_t launch_eval_reduce(const double* part, int64_t blocks, double* acc, int32_t first,
+                              hipStream_t s);
 
 // host-side He-normal initial parameters (packed layout)
 void he_normal_init(const int32_t* dims, int32_t L, uint64_t seed, float* packed);

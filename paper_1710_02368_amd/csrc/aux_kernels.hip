@@ -170,6 +170,91 @@ __global__ void copy_bf16_kernel(const float* src, uint16_t* dst, int64_t count)
   if (e < count) dst[e] = f32_to_bf16_rne(src[e]);
 }
 
+// Evaluation of one row per wave: loss = logsumexp(z) - z_y and the
+// predicted class argmax z.  Argmax order: a NaN beats any number, a larger
+// value beats a smaller one, and among equals (or among NaNs) the lower
+// class index wins; the order is total, so the wave reduction gives the
+// same class whatever the lanes' pairing.
+__device__ __forceinline__ bool beats(float v, int i, float bv, int bi) {
+  const bool vn = v != v, bn = bv != bv;
+  if (vn != bn) return vn;
+  if (vn) return i < bi;
+  return v > bv || (v == bv && i < bi);
+}
+
+constexpr int EVAL_ROWS_PER_BLOCK = 4;
+
+__global__ __launch_bounds__(256) void eval_rows_kernel(EvalArgs a) {
+  __shared__ double lsum[EVAL_ROWS_PER_BLOCK];
+  __shared__ double csum[EVAL_ROWS_PER_BLOCK];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t row = (int64_t)blockIdx.x * EVAL_ROWS_PER_BLOCK + wave;
+  double l = 0.0, ok = 0.0;
+  if (row < a.rows) {
+    const float* z = a.z + row * a.ldz;
+    float mx = -INFINITY, bv = -INFINITY;
+    int bi = 0x7fffffff;
+    for (int c = lane; c < a.C; c += 64) {
+      const float v = z[c];
+      mx = fmaxf(mx, v);
+      if (beats(v, c, bv, bi)) bv = v, bi = c;
+    }
+    mx = wave_max(mx);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const float ov = __shfl_xor(bv, off, 64);
+      const int oi = __shfl_xor(bi, off, 64);
+      if (beats(ov, oi, bv, bi)) bv = ov, bi = oi;
+    }
+    float s = 0.f;
+    for (int c = lane; c < a.C; c += 64) s += expf(z[c] - mx);
+    s = wave_sum(s);
+    const int label = a.y[row];
+    const bool in_range = label >= 0 && label < a.C;
+    const float loss = in_range ? mx + logf(s) - z[in_range ? label : 0] : NAN;
+    l = (double)loss;
+    ok = (in_range && bi == label) ? 1.0 : 0.0;
+    if (lane == 0) {
+      if (a.row_loss) a.row_loss[row] = loss;
+      if (a.row_pred) a.row_pred[row] = bi;
+    }
+  }
+  if (lane == 0) {
+    lsum[wave] = l;
+    csum[wave] = ok;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double ls = 0.0, cs = 0.0;
+    for (int w = 0; w < EVAL_ROWS_PER_BLOCK; ++w) ls += lsum[w], cs += csum[w];
+    a.part[2 * blockIdx.x] = ls;
+    a.part[2 * blockIdx.x + 1] = cs;
+  }
+}
+
+// acc (=, or += when !first) the column sums of part[blocks][2], each
+// thread summing a strided subset in increasing order, then a fixed tree
+__global__ __launch_bounds__(256) void eval_reduce_kernel(const double* part, int64_t blocks,
+                                                          double* acc, int32_t first) {
+  __shared__ double sl[256], sc[256];
+  double l = 0.0, c = 0.0;
+  for (int64_t b = threadIdx.x; b < blocks; b += 256) l += part[2 * b], c += part[2 * b + 1];
+  sl[threadIdx.x] = l;
+  sc[threadIdx.x] = c;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) {
+      sl[threadIdx.x] += sl[threadIdx.x + w];
+      sc[threadIdx.x] += sc[threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    acc[0] = (first ? 0.0 : acc[0]) + sl[0];
+    acc[1] = (first ? 0.0 : acc[1]) + sc[0];
+  }
+}
+
 inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1) / per); }
 
 }  // namespace
@@ -215,6 +300,19 @@ hipError_t launch_batch_indices(int32_t worker, int64_t t, int32_t mb, int64_t S
                                 hipStream_t s) {
   hipLaunchKernelGGL(batch_indices_kernel, dim3(blocks_for(mb, 256)), dim3(256), 0, s, worker, t, mb,
                      S, out);
+  return hipGetLastError();
+}
+
+int64_t eval_blocks(int64_t rows) { return (rows + EVAL_ROWS_PER_BLOCK - 1) / EVAL_ROWS_PER_BLOCK; }
+
+hipError_t launch_eval_rows(const EvalArgs& a, hipStream_t s) {
+  hipLaunchKernelGGL(eval_rows_kernel, dim3((unsigned)eval_blocks(a.rows)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_eval_reduce(const double* part, int64_t blocks, double* acc, int32_t first,
+                              hipStream_t s) {
+  hipLaunchKernelGGL(eval_reduce_kernel, dim3(1), dim3(256), 0, s, part, blocks, acc, first);
   return hipGetLastError();
 }
 

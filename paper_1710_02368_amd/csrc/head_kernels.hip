@@ -11,6 +11,9 @@
 //   dZ_prev[j][i] = (sum_c dZ[j][c] W[c][i]) * [H[j][i] > 0]
 // Weight gradient (summed over the m rows) fused with the update:
 //   W[c][i] <- W[c][i] - eta * sum_j dZ[j][c] H[j][i];  b[c] <- b[c] - eta * sum_j dZ[j][c]
+// The evaluation variant (EVAL) computes the same logits for rows of a
+// held-out set and, instead of the gradients, the loss, the predicted class
+// and the block's partial sums.
 #include <math.h>
 
 #include "device_common.h"
@@ -19,7 +22,6 @@ namespace agn {
 namespace {
 
 constexpr int HEAD_WAVE_ROWS = 1;                  // rows a wave processes together
-constexpr int HEAD_ROWS = 4 * HEAD_WAVE_ROWS;       // rows per workgroup
 constexpr int HEAD_DMAX = 2048;                     // hidden width limit
 
 __device__ __forceinline__ float wsum(float v) {
@@ -28,18 +30,33 @@ __device__ __forceinline__ float wsum(float v) {
   return v;
 }
 
+// Argmax order of the evaluation: a NaN beats any number, a larger value a
+// smaller one, and among equals (or NaNs) the lower class index wins.
+__device__ __forceinline__ bool beats_h(float v, int i, float bv, int bi) {
+  const bool vn = v != v, bn = bv != bv;
+  if (vn != bn) return vn;
+  if (vn) return i < bi;
+  return v > bv || (v == bv && i < bi);
+}
+
+constexpr int EVAL_WAVE_ROWS = 4;                   // rows per wave in the evaluation variant
+__host__ __device__ constexpr int head_rows(bool eval) { return 4 * (eval ? EVAL_WAVE_ROWS : HEAD_WAVE_ROWS); }
+
 // LDS: W padded to CMAX rows x 64*QMAX columns (zeros outside C x d), then b.
 // Each wave keeps its rows of H in registers (QMAX per lane per row, all
 // loaded at once); padding rows and columns are zero, so the loops are
 // static and branch-free.
-template <int CMAX, int QMAX>
+template <int CMAX, int QMAX, bool EVAL>
 __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
   extern __shared__ float smem[];
+  __shared__ double epart[EVAL ? 8 : 1];
   constexpr int LW = 64 * QMAX;
+  constexpr int WR = EVAL ? EVAL_WAVE_ROWS : HEAD_WAVE_ROWS;  // rows per wave
+  constexpr int RB = 4 * WR;                                     // rows per workgroup
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int blocks_per_worker = (a.m + HEAD_ROWS - 1) / HEAD_ROWS;
+  const int blocks_per_worker = (a.m + RB - 1) / RB;
   const int k = blockIdx.x / blocks_per_worker;
-  const int r0 = (blockIdx.x % blocks_per_worker) * HEAD_ROWS;
+  const int r0 = (blockIdx.x % blocks_per_worker) * RB;
   const int d = a.d, C = a.C;
   const float* W = a.w + (int64_t)k * a.pstride;
   const float* bias = a.b + (int64_t)k * a.pstride;
@@ -49,15 +66,15 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
 
   // rows of this wave: issue every load of H (and the labels) before
   // anything waits
-  int jr[HEAD_WAVE_ROWS];
-  int label[HEAD_WAVE_ROWS];
-  const float* hp[HEAD_WAVE_ROWS];
-  float hv[HEAD_WAVE_ROWS][QMAX];
+  int jr[WR];
+  int label[WR];
+  const float* hp[WR];
+  float hv[WR][QMAX];
 #pragma unroll
-  for (int r = 0; r < HEAD_WAVE_ROWS; ++r) {
-    jr[r] = r0 + wave * HEAD_WAVE_ROWS + r;
+  for (int r = 0; r < WR; ++r) {
+    jr[r] = r0 + wave * WR + r;
     const int j = jr[r] < a.m ? jr[r] : a.m - 1;   // rows past m compute a copy, store nothing
-    label[r] = a.y[batch_row(k, t, a.g.mb, a.g.S, j)];
+    label[r] = EVAL ? a.y[j] : a.y[batch_row(k, t, a.g.mb, a.g.S, j)];
     hp[r] = a.gather ? a.h + batch_row(k, t, a.g.mb, a.g.S, j) * a.ldh
                      : a.h + (int64_t)k * a.hstride + (int64_t)j * a.ldh;
 #pragma unroll
@@ -84,15 +101,15 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
   }
   if (tid < CMAX) bs[tid] = tid < C ? bias[tid] : 0.f;
 #pragma unroll
-  for (int r = 0; r < HEAD_WAVE_ROWS; ++r)
+  for (int r = 0; r < WR; ++r)
 #pragma unroll
     for (int q = 0; q < QMAX; ++q) hv[r][q] = lane + 64 * q < d ? hv[r][q] : 0.f;
   __syncthreads();
 
   // logits: lane-partial dot products, then one wave reduction per (row, class)
-  float p[HEAD_WAVE_ROWS][CMAX];
+  float p[WR][CMAX];
 #pragma unroll
-  for (int r = 0; r < HEAD_WAVE_ROWS; ++r)
+  for (int r = 0; r < WR; ++r)
 #pragma unroll
     for (int c = 0; c < CMAX; ++c) p[r][c] = 0.f;
 #pragma unroll
@@ -101,18 +118,64 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
     for (int c = 0; c < CMAX; ++c) {
       const float w = Ws[c * LW + lane + 64 * q];
 #pragma unroll
-      for (int r = 0; r < HEAD_WAVE_ROWS; ++r) p[r][c] += hv[r][q] * w;
+      for (int r = 0; r < WR; ++r) p[r][c] += hv[r][q] * w;
     }
   }
 #pragma unroll
-  for (int r = 0; r < HEAD_WAVE_ROWS; ++r)
+  for (int r = 0; r < WR; ++r)
 #pragma unroll
     for (int c = 0; c < CMAX; ++c) p[r][c] = wsum(p[r][c]) + bs[c];
+
+  if constexpr (EVAL) {
+    // loss, predicted class and the block's partial sums (fixed order)
+    double ls = 0.0, cs = 0.0;
+#pragma unroll
+    for (int r = 0; r < WR; ++r) {
+      const int lb = label[r];
+      float mx = -INFINITY, bv = -INFINITY;
+      int bi = 0x7fffffff;
+#pragma unroll
+      for (int c = 0; c < CMAX; ++c) {
+        if (c < C) {
+          mx = fmaxf(mx, p[r][c]);
+          if (beats_h(p[r][c], c, bv, bi)) bv = p[r][c], bi = c;
+        }
+      }
+      float s = 0.f, zy = 0.f;
+#pragma unroll
+      for (int c = 0; c < CMAX; ++c) {
+        s += c < C ? expf(p[r][c] - mx) : 0.f;
+        zy = c == lb ? p[r][c] : zy;
+      }
+      const bool in_range = lb >= 0 && lb < C;
+      const float loss = in_range ? mx + logf(s) - zy : NAN;
+      if (jr[r] < a.m) {
+        if (lane == 0) {
+          if (a.row_loss) a.row_loss[jr[r]] = loss;
+          if (a.row_pred) a.row_pred[jr[r]] = bi;
+        }
+        ls += (double)loss;
+        cs += (in_range && bi == lb) ? 1.0 : 0.0;
+      }
+    }
+    if (lane == 0) {
+      epart[2 * wave] = ls;
+      epart[2 * wave + 1] = cs;
+    }
+    __syncthreads();
+    if (tid == 0) {
+      double l = 0.0, c = 0.0;
+      for (int w = 0; w < 4; ++w) l += epart[2 * w], c += epart[2 * w + 1];
+      a.part[2 * blockIdx.x] = l;
+      a.part[2 * blockIdx.x + 1] = c;
+    }
+    return;
+  }
 
   // softmax cross-entropy per row; p becomes dZ
   const float inv_m = 1.f / (float)a.m;
 #pragma unroll
-  for (int r = 0; r < HEAD_WAVE_ROWS; ++r) {
+  for (int r = 0; r < WR; ++r) {
     const int lb = label[r];
     float mx = -INFINITY;
 #pragma unroll
@@ -144,17 +207,17 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
 #pragma unroll
     for (int q = 0; q < QMAX; ++q) {
       const int i = lane + 64 * q;
-      float acc[HEAD_WAVE_ROWS];
+      float acc[WR];
 #pragma unroll
-      for (int r = 0; r < HEAD_WAVE_ROWS; ++r) acc[r] = 0.f;
+      for (int r = 0; r < WR; ++r) acc[r] = 0.f;
 #pragma unroll
       for (int c = 0; c < CMAX; ++c) {
         const float w = Ws[c * LW + i];
 #pragma unroll
-        for (int r = 0; r < HEAD_WAVE_ROWS; ++r) acc[r] += p[r][c] * w;
+        for (int r = 0; r < WR; ++r) acc[r] += p[r][c] * w;
       }
 #pragma unroll
-      for (int r = 0; r < HEAD_WAVE_ROWS; ++r) {
+      for (int r = 0; r < WR; ++r) {
         if (jr[r] < a.m && i < d) {
           float* dp = a.dprev + (int64_t)k * a.hstride + (int64_t)jr[r] * a.ldh;
           dp[i] = hv[r][q] > 0.f ? acc[r] : 0.f;
@@ -263,34 +326,35 @@ size_t head_lds_bytes(int C, int d) {
   return ((size_t)cm * 64 * head_qmax(d) + cm) * sizeof(float);
 }
 
-template <int CM, int QM>
+template <int CM, int QM, bool EVAL>
 static hipError_t head_go(const HeadArgs& a, hipStream_t s, bool prepare) {
   const size_t lds = head_lds_bytes(a.C, a.d);
   if (prepare) {
     if (lds <= 64 * 1024) return hipSuccess;
-    return hipFuncSetAttribute((const void*)head_kernel<CM, QM>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                               (int)lds);
+    return hipFuncSetAttribute((const void*)head_kernel<CM, QM, EVAL>,
+                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   }
-  const int blocks = a.n * ((a.m + HEAD_ROWS - 1) / HEAD_ROWS);
-  hipLaunchKernelGGL((head_kernel<CM, QM>), dim3(blocks), dim3(256), lds, s, a);
+  const int blocks = a.n * ((a.m + head_rows(EVAL) - 1) / head_rows(EVAL));
+  hipLaunchKernelGGL((head_kernel<CM, QM, EVAL>), dim3(blocks), dim3(256), lds, s, a);
   return hipGetLastError();
 }
 
-template <int CM>
+template <int CM, bool EVAL>
 static hipError_t head_dispatch_q(const HeadArgs& a, hipStream_t s, bool prepare) {
   switch (head_qmax(a.d)) {
-    case 2: return head_go<CM, 2>(a, s, prepare);
-    case 8: return head_go<CM, 8>(a, s, prepare);
-    case 16: return head_go<CM, 16>(a, s, prepare);
-    default: return head_go<CM, 32>(a, s, prepare);
+    case 2: return head_go<CM, 2, EVAL>(a, s, prepare);
+    case 8: return head_go<CM, 8, EVAL>(a, s, prepare);
+    case 16: return head_go<CM, 16, EVAL>(a, s, prepare);
+    default: return head_go<CM, 32, EVAL>(a, s, prepare);
   }
 }
 
+template <bool EVAL>
 static hipError_t head_dispatch(const HeadArgs& a, hipStream_t s, bool prepare) {
   switch (head_cmax(a.C)) {
-    case 10: return head_dispatch_q<10>(a, s, prepare);
-    case 16: return head_dispatch_q<16>(a, s, prepare);
-    default: return head_dispatch_q<32>(a, s, prepare);
+    case 10: return head_dispatch_q<10, EVAL>(a, s, prepare);
+    case 16: return head_dispatch_q<16, EVAL>(a, s, prepare);
+    default: return head_dispatch_q<32, EVAL>(a, s, prepare);
   }
 }
 
@@ -303,10 +367,15 @@ bool head_prepare(int C, int d) {
   HeadArgs a{};
   a.C = C;
   a.d = d;
-  return head_dispatch(a, nullptr, true) == hipSuccess;
+  return head_dispatch<false>(a, nullptr, true) == hipSuccess &&
+         head_dispatch<true>(a, nullptr, true) == hipSuccess;
 }
 
-hipError_t launch_head(const HeadArgs& a, hipStream_t s) { return head_dispatch(a, s, false); }
+hipError_t launch_head(const HeadArgs& a, hipStream_t s) { return head_dispatch<false>(a, s, false); }
+
+int64_t head_eval_blocks(int64_t rows) { return (rows + head_rows(true) - 1) / head_rows(true); }
+
+hipError_t launch_head_eval(const HeadArgs& a, hipStream_t s) { return head_dispatch<true>(a, s, false); }
 
 hipError_t launch_head_dw(const HeadDwArgs& a, hipStream_t s) {
   const int blocks = a.n * ((a.d + 63) / 64);

@@ -4,6 +4,7 @@ import ctypes
 import os
 import re
 
+import numpy as np
 import pytest
 
 import paper_1710_02368_amd as agn
@@ -65,3 +66,51 @@ def test_null_arguments_are_rejected():
     assert lib.agn_loss(None, None) == -1
     lib.agn_destroy(None)  # no-op
     assert isinstance(agn.agn_last_error(None), str)
+
+
+def test_null_evaluate_arguments_are_rejected():
+    lib = agn.load_library()
+    assert lib.agn_evaluate(None, None, None, None, None) == -1
+    assert lib.agn_temporal_efficiency(None, None, 0, None, None, 0, None) == -1
+
+
+# --------------------------------------------------------------------------
+# temporal efficiency (Eq. 4): host arithmetic in the library, checked
+# against the oracle's independent implementation
+# --------------------------------------------------------------------------
+def _curve(rng, k, start=0.0):
+    t = np.concatenate([[start], start + np.cumsum(rng.random(k - 1) + 1e-3)])
+    return t, rng.random(k)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_temporal_efficiency_matches_oracle(seed):
+    from oracle import temporal_efficiency
+    rng = np.random.default_rng(seed)
+    ta, fa = _curve(rng, int(rng.integers(2, 60)))
+    tb, fb = _curve(rng, int(rng.integers(2, 60)))
+    got = agn.agn_temporal_efficiency(ta, fa, tb, fb)
+    want = temporal_efficiency(ta, fa, tb, fb)
+    assert got == pytest.approx(want, rel=1e-12)
+
+
+def test_temporal_efficiency_closed_forms():
+    # f_a = t on [0, 2] against f_b = 1 on [0, 1]: cut at 1, E = 1/2
+    assert agn.agn_temporal_efficiency([0, 2], [0, 2], [0, 1], [1, 1]) == pytest.approx(0.5, rel=1e-15)
+    # lines are integrated exactly: 0.3 t against 0.6 over m = 3 -> 3/4
+    ta = [0.0, 0.13, 0.9, 1.05, 2.4, 4.0]
+    assert agn.agn_temporal_efficiency(ta, [0.3 * t for t in ta], [0, 1.1, 3.0], [0.6] * 3) == \
+        pytest.approx(0.75, rel=1e-14)
+
+
+@pytest.mark.parametrize("ta,fa,tb,fb", [
+    ([0.0], [1.0], [0, 1], [1, 1]),                 # one sample
+    ([0.5, 1.0], [1, 1], [0, 1], [1, 1]),           # not starting at 0
+    ([0.0, 1.0, 1.0], [1, 1, 1], [0, 1], [1, 1]),   # times not increasing
+    ([0.0, 1.0], [1.0, float("inf")], [0, 1], [1, 1]),
+    ([0.0, 1.0], [1, 1], [0, 1], [0, 0]),           # zero area of b
+])
+def test_temporal_efficiency_rejects_bad_curves(ta, fa, tb, fb):
+    with pytest.raises(agn.AGNError) as ei:
+        agn.agn_temporal_efficiency(ta, fa, tb, fb)
+    assert ei.value.code == -1

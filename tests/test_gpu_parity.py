@@ -315,6 +315,7 @@ def test_graph_replay_and_eager_launches_agree():
             g.round(xd, yd, order)
         res.append((g.central().cpu().numpy(), g.loss().cpu().numpy()))
         if eager:
+            g.evaluate(xd, yd)   # (the evaluation's class: not part of a round)
             for name, c in agn.KERNEL_CLASSES.items():
                 ms, cnt = agn.agn_kernel_timing(g.ctx, c)
                 assert cnt > 0 and ms > 0, name

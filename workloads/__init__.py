@@ -20,7 +20,8 @@ from typing import List, Sequence
 import numpy as np
 
 __all__ = [
-    "Workload", "WORKLOADS", "workload", "make_data", "commit_orders",
+    "Workload", "WORKLOADS", "workload", "make_data", "make_heldout", "HELDOUT_ROWS", "commit_orders",
+    "random_params",
     "bf16_bits_from_f32", "f32_from_bf16_bits", "data_digest", "small_workload",
 ]
 
@@ -147,34 +148,33 @@ def f32_from_bf16_bits(b: np.ndarray) -> np.ndarray:
 # data and labels
 # ---------------------------------------------------------------------------
 
-def _teacher_labels(wl: Workload, X_chunks: Sequence[np.ndarray], rng_t) -> np.ndarray:
+def _teacher_logits(wl: Workload, X_chunks: Sequence[np.ndarray], rng_t) -> np.ndarray:
+    """Logits of the workload's teacher on the float32 inputs (float64)."""
     d0, C = wl.dims[0], wl.dims[-1]
     if wl.data == "gauss_linear":
         T = rng_t.standard_normal((d0, C))
-        ys = [np.argmax(xc.astype(np.float64) @ T, axis=1) for xc in X_chunks]
-    else:
-        # two-layer ReLU teacher; its logits are centred per class over the
-        # data set so that the classes come out roughly balanced
-        A = rng_t.standard_normal((d0, TEACHER_HIDDEN)) / np.sqrt(d0)
-        B = rng_t.standard_normal((TEACHER_HIDDEN, C)) / np.sqrt(TEACHER_HIDDEN)
-        z = np.concatenate([np.maximum(xc.astype(np.float64) @ A, 0.0) @ B for xc in X_chunks])
-        z -= z.mean(axis=0)
-        ys = [np.argmax(z, axis=1)]
-    return np.concatenate(ys).astype(np.int32)
+        return np.concatenate([xc.astype(np.float64) @ T for xc in X_chunks])
+    # two-layer ReLU teacher
+    A = rng_t.standard_normal((d0, TEACHER_HIDDEN)) / np.sqrt(d0)
+    B = rng_t.standard_normal((TEACHER_HIDDEN, C)) / np.sqrt(TEACHER_HIDDEN)
+    return np.concatenate([np.maximum(xc.astype(np.float64) @ A, 0.0) @ B for xc in X_chunks])
 
 
-def make_data(wl: Workload):
-    """Return (X, y).
+def _teacher_labels(wl: Workload, X_chunks: Sequence[np.ndarray], rng_t,
+                    centre: np.ndarray | None = None) -> np.ndarray:
+    """Labels = argmax of the teacher's logits (ties to the lowest class).
+    The two-layer teacher's logits are centred per class over the training
+    set so that the classes come out roughly balanced; ``centre`` passes the
+    training set's per-class means for other rows."""
+    z = _teacher_logits(wl, X_chunks, rng_t)
+    if wl.data != "gauss_linear":
+        z = z - (z.mean(axis=0) if centre is None else centre)
+    return np.argmax(z, axis=1).astype(np.int32)
 
-    X is float32 [N][d_0] for fp32 workloads and uint16 bf16 bit patterns
-    [N][d_0] for bf16 workloads; y is int32 [N] with labels in [0, C).
-    Labels are computed from the float32 inputs (before bf16 rounding);
-    argmax ties go to the lowest class index.
-    """
-    ds = wl.data_seed if wl.data_seed is not None else wl.seed
-    rng_x = np.random.default_rng([ds, 0])
-    rng_t = np.random.default_rng([ds, 1])
-    N, d0 = wl.N, wl.dims[0]
+
+def _draw(wl: Workload, rng_x, N: int):
+    """N input rows from the stream rng_x: (stored X, float32 chunks)."""
+    d0 = wl.dims[0]
     bf16 = wl.dtype == "bf16"
     X = np.empty((N, d0), dtype=np.uint16 if bf16 else np.float32)
     chunks = []
@@ -190,8 +190,51 @@ def make_data(wl: Workload):
             raise ValueError(f"unknown data kind {wl.data!r}")
         X[r0:r0 + rows] = bf16_bits_from_f32(xc) if bf16 else xc
         chunks.append(xc)
-    y = _teacher_labels(wl, chunks, rng_t)
+    return X, chunks
+
+
+def make_data(wl: Workload):
+    """Return (X, y).
+
+    X is float32 [N][d_0] for fp32 workloads and uint16 bf16 bit patterns
+    [N][d_0] for bf16 workloads; y is int32 [N] with labels in [0, C).
+    Labels are computed from the float32 inputs (before bf16 rounding);
+    argmax ties go to the lowest class index.
+    """
+    ds = wl.data_seed if wl.data_seed is not None else wl.seed
+    X, chunks = _draw(wl, np.random.default_rng([ds, 0]), wl.N)
+    y = _teacher_labels(wl, chunks, np.random.default_rng([ds, 1]))
     return X, y
+
+
+HELDOUT_ROWS = 10000      # stands in for the size of MNIST's test set
+
+
+def make_heldout(wl: Workload, rows: int = HELDOUT_ROWS):
+    """A held-out set (X, y) in make_data's format: inputs from a stream of
+    their own, labelled by the training set's teacher (for the two-layer
+    teacher, centred by the training set's per-class means).  It stands in
+    for the validation set of Section 4's figures."""
+    ds = wl.data_seed if wl.data_seed is not None else wl.seed
+    centre = None
+    if wl.data != "gauss_linear":
+        _, train = _draw(wl, np.random.default_rng([ds, 0]), wl.N)
+        centre = _teacher_logits(wl, train, np.random.default_rng([ds, 1])).mean(axis=0)
+    X, chunks = _draw(wl, np.random.default_rng([ds, 3]), rows)
+    y = _teacher_labels(wl, chunks, np.random.default_rng([ds, 1]), centre)
+    return X, y
+
+
+def random_params(dims: Sequence[int], seed: int, scale: float = 1.0) -> np.ndarray:
+    """A seeded float32 parameter vector in the packed layout (W_0 row-major
+    [d_1][d_0], b_0, W_1, b_1, ...): weights N(0, scale^2 / d_in), biases
+    N(0, 0.1^2).  For tests that set a model on both sides."""
+    rng = np.random.default_rng([seed, 4])
+    parts = []
+    for l in range(len(dims) - 1):
+        parts.append(rng.standard_normal(dims[l] * dims[l + 1]) * (scale / np.sqrt(dims[l])))
+        parts.append(rng.standard_normal(dims[l + 1]) * 0.1)
+    return np.concatenate(parts).astype(np.float32)
 
 
 def commit_orders(wl: Workload, rounds: int | None = None) -> List[np.ndarray]:
