@@ -21,6 +21,12 @@ Normalization", ACML 2017):
 * Section 1 (caption of the asynchronous data-parallelism figure): the
   server applies commits as a FIFO queue; with n homogeneous workers the
   expected staleness of a commit is n - 1.
+* Section 4 (the DynSGD comparison): a commit scaled down by its staleness
+  (``staleness_scaled=True``), read as the factor 1 / (tau + 1), tau the
+  number of commits applied since the worker's last pull.  The paper gives
+  only the effect (about 1 / (n - 1) at E[tau] = n - 1); the cited work
+  holding the exact rule is not available, so this reading is partly
+  unpinned.
 
 Readings of points the paper leaves open (each one is listed in the design
 notes of the repository):
@@ -277,7 +283,7 @@ class AGNOracle:
     """
 
     def __init__(self, dims, n, lam, eta, m, seed=0, bf16=False, dtype=np.float32,
-                 init=None, normalize=True, adam=None):
+                 init=None, normalize=True, adam=None, staleness_scaled=False):
         if n < 1 or lam < 1 or m < 1 or len(dims) < 2:
             raise ValueError("bad shapes")
         self.dims = tuple(int(d) for d in dims)
@@ -295,6 +301,11 @@ class AGNOracle:
         # g = -eta * mhat / (sqrt(vhat) + eps) with mhat = m / (1 - beta1^t),
         # vhat = v / (1 - beta2^t) at the worker's local step t = 1, 2, ...
         self.adam = None if adam is None else tuple(float(a) for a in adam)
+        # staleness_scaled: the server multiplies each commit by
+        # 1 / (tau + 1) (rounded to float32), tau = commits applied since
+        # the committing worker's last pull (Section 4's DynSGD rule,
+        # scaling commits down by their staleness)
+        self.staleness_scaled = bool(staleness_scaled)
         self.prec = _Prec(dtype, bf16)
         self.eta = self.prec.dtype.type(eta)
         if init is None:
@@ -380,10 +391,19 @@ class AGNOracle:
         st = self.prec.st
         stale = []
         for k in order:
-            # Commit (Eq. 2): central <- central + delta_k
-            self.central = [(st(W + dW), st(b + db))
-                            for (W, b), (dW, db) in zip(self.central, deltas[k])]
-            stale.append(self.version - self.pulled_version[k])
+            tau = self.version - self.pulled_version[k]
+            if self.staleness_scaled:
+                # central <- central + s * delta_k, s = fl32(1 / (tau + 1)),
+                # the product and the sum rounded once
+                sc = np.float64(np.float32(1.0 / (tau + 1)))
+                self.central = [(st(W + sc * np.asarray(dW, dtype=np.float64)),
+                                 st(b + sc * np.asarray(db, dtype=np.float64)))
+                                for (W, b), (dW, db) in zip(self.central, deltas[k])]
+            else:
+                # Commit (Eq. 2): central <- central + delta_k
+                self.central = [(st(W + dW), st(b + db))
+                                for (W, b), (dW, db) in zip(self.central, deltas[k])]
+            stale.append(tau)
             self.version += 1
             # Pull right after the worker's own commit
             self.workers[k] = [(W.copy(), b.copy()) for W, b in self.central]

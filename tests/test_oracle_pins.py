@@ -593,3 +593,56 @@ def test_adam_moments_persist_across_pulls():
     b.moments = [[tuple(np.zeros_like(x) for x in t) for t in w] for w in b.moments]
     b.round(X, y, [1, 0])
     assert np.max(np.abs(a.central_flat() - b.central_flat())) > 1e-6
+
+
+# --------------------------------------------------------------------------
+# Staleness-scaled commits (Section 4's DynSGD rule, read as 1 / (tau + 1))
+# --------------------------------------------------------------------------
+def test_staleness_scaling_one_worker_is_plain():
+    """n = 1: every commit has staleness 0, so the scale is exactly 1."""
+    dims = (12, 9, 5)
+    X, y = make_xy(40, dims[0], dims[-1], 3)
+    a = O.AGNOracle(dims, n=1, lam=3, eta=0.2, m=4, seed=5, staleness_scaled=True)
+    b = O.AGNOracle(dims, n=1, lam=3, eta=0.2, m=4, seed=5)
+    for r in range(3):
+        a.round(X, y, [0])
+        b.round(X, y, [0])
+    assert np.array_equal(a.central_flat(), b.central_flat())
+
+
+@pytest.mark.parametrize("n", [2, 4, 7])
+def test_staleness_scaling_harmonic_first_round(n):
+    """Every worker holds the same rows, so in round 1 (one common start)
+    all n deltas equal the one-worker delta D, and the j-th commit has
+    staleness j: the central variable moves by sum_j D / (j + 1) = H_n D
+    (harmonic number; scales rounded to float32, float64 storage)."""
+    dims, lam, m, S = (10, 8, 4), 3, 5, 23
+    X1, y1 = make_xy(S, dims[0], dims[-1], 9)
+    X, y = np.tile(X1, (n, 1)), np.tile(y1, n)
+    one = O.AGNOracle(dims, n=1, lam=lam, eta=0.25, m=m, seed=2, dtype=np.float64)
+    one.round(X1, y1, [0])
+    c0 = O.flat_params(O.he_normal_init(dims, 2, dtype=np.float64))
+    D = one.central_flat() - c0
+    o = O.AGNOracle(dims, n=n, lam=lam, eta=0.25, m=m, seed=2, dtype=np.float64, staleness_scaled=True)
+    o.round(X, y, np.random.default_rng(n).permutation(n))
+    H = sum(1.0 / (j + 1) for j in range(n))
+    np.testing.assert_allclose(o.central_flat() - c0, H * D, rtol=1e-7, atol=1e-15)
+
+
+def test_staleness_scaling_uses_staleness_not_position():
+    """n = 2, orders [0, 1] then [1, 0]: in round 2 worker 1 commits first
+    with staleness 0 (it pulled the latest central variable) and worker 0
+    second with staleness 2 (it pulled before worker 1's round-1 commit), so
+    the scales are 1 and 1/3, not the positions' 1 and 1/2."""
+    dims = (10, 8, 4)
+    X, y = make_xy(40, dims[0], dims[-1], 4)
+    o = O.AGNOracle(dims, n=2, lam=2, eta=0.25, m=5, seed=6, dtype=np.float64, staleness_scaled=True)
+    o.round(X, y, [0, 1])
+    c1 = o.central_flat().copy()
+    o.round(X, y, [1, 0])
+    assert o.staleness == [[0, 1], [0, 2]]
+    d0 = O.flat_params(o.last_deltas[0])
+    d1 = O.flat_params(o.last_deltas[1])
+    want = c1 + d1 + np.float32(1.0 / 3.0) * d0
+    np.testing.assert_allclose(o.central_flat(), want, rtol=1e-14, atol=1e-15)
+    assert np.max(np.abs(o.central_flat() - (c1 + d1 + 0.5 * d0))) > 1e-6
