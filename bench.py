@@ -65,9 +65,12 @@ def bound_of(w, dtype):
 
 
 ADAM = (0.9, 0.999, 1e-8)
+# commit rule -> (normalize, staleness_scaled)
+COMMIT_RULES = {"agn": (True, False), "accumulated": (False, False), "agn_scaled": (True, True),
+                "dynsgd": (False, True)}
 
 
-def cpu_baseline(wl, X, y, orders, budget_s=12.0, adam=None):
+def cpu_baseline(wl, X, y, orders, budget_s=12.0, adam=None, normalize=True, scaled=False):
     """The oracle as it stands, on the host cores, over whole rounds until
     about budget_s seconds have passed (at least one round)."""
     from oracle import AGNOracle
@@ -76,7 +79,8 @@ def cpu_baseline(wl, X, y, orders, budget_s=12.0, adam=None):
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         threads = len(os.sched_getaffinity(0))
-    o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, bf16=wl.dtype == "bf16", adam=adam)
+    o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, bf16=wl.dtype == "bf16", adam=adam,
+                  normalize=normalize, staleness_scaled=scaled)
     t0 = time.perf_counter()
     rounds = 0
     while True:
@@ -198,6 +202,9 @@ def main():
                     help="local rule: plain SGD (the paper's Eq. 1) or Adam (beta 0.9/0.999, eps 1e-8)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--commit", choices=sorted(COMMIT_RULES), default="agn",
+                    help="commit rule: agn (a / lambda, the default), accumulated (a), or either scaled by "
+                         "1 / (staleness + 1) (agn_scaled, dynsgd)")
     ap.add_argument("--mode", choices=["round", "eval"], default="round",
                     help="round: the AGN round (default line, with the evaluation); eval: evaluation only")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -222,7 +229,9 @@ def main():
     xd = torch.from_numpy(X.view(np.int16) if X.dtype == np.uint16 else X).cuda()
     yd = torch.from_numpy(y).cuda()
     adam = ADAM if args.optimizer == "adam" else None
-    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, dtype=wl.dtype, adam=adam)
+    normalize, scaled = COMMIT_RULES[args.commit]
+    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, dtype=wl.dtype, adam=adam,
+                normalize=normalize, staleness_scaled=scaled)
     order_at = lambda i: orders[i % len(orders)]
     Xh, yh = W.make_heldout(wl)
     xh = torch.from_numpy(Xh.view(np.int16) if Xh.dtype == np.uint16 else Xh).cuda()
@@ -324,7 +333,7 @@ def main():
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(dt * 1e3 / args.steps, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32" if wl.dtype == "fp32" else "bf16", "data": "synthetic",
-        "config": {"workload": wl.name, "optimizer": args.optimizer,
+        "config": {"workload": wl.name, "optimizer": args.optimizer, "commit": args.commit,
                    "dims": list(wl.dims), "n": wl.n, "lambda": wl.lam, "m": wl.m,
                    "eta": wl.eta, "commit_order": wl.order, "num_samples": wl.N,
                    "worker_samples_per_round": wl.worker_samples_per_round},
@@ -340,7 +349,8 @@ def main():
     }
     g.close()
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, X, y, orders, budget_s=args.cpu_budget, adam=adam)
+        out["cpu_baseline"] = cpu_baseline(wl, X, y, orders, budget_s=args.cpu_budget, adam=adam,
+                                           normalize=normalize, scaled=scaled)
     print(json.dumps(out), flush=True)
 
 

@@ -107,6 +107,25 @@ int agn_set_stream(agn_ctx* ctx, void* hip_stream);
  * AGN_ESTATE afterwards, AGN_EINVAL for a value other than 0 or 1. */
 int agn_set_normalization(agn_ctx* ctx, int32_t normalize);
 
+/* Staleness-scaled commits (Section 4 compares AGN with DynSGD, which
+ * scales each commit down by its staleness).  enable = 1: the j-th commit
+ * of a round adds s_j * delta instead of delta, s_j = 1 / (tau_j + 1)
+ * rounded to float32, tau_j = the number of commits applied since the
+ * committing worker's last pull (agn_staleness).  The paper gives only the
+ * effect (about 1 / (n - 1) at the expected staleness n - 1); the factor
+ * 1 / (tau + 1) is this library's reading.  Combined with
+ * agn_set_normalization(ctx, 0) the scaled delta is the accumulated update
+ * (DynSGD-style commits of local work).  Default 0.  Only before the first
+ * round: AGN_ESTATE afterwards, AGN_EINVAL for a value other than 0 or 1. */
+int agn_set_staleness_scaling(agn_ctx* ctx, int32_t enable);
+
+/* Staleness of the last round's commits, by commit position: out[j] = the
+ * number of commits the server applied between the pull of the j-th
+ * committing worker and its commit (Section 1: the FIFO queue; the expected
+ * staleness with n workers is n - 1).  out: HOST, n int64.  AGN_ESTATE
+ * before the first round.  Host bookkeeping; does not wait. */
+int agn_staleness(agn_ctx* ctx, int64_t* out);
+
 /* Local rule of the workers (Algorithm 1's gradient line, which names Adam
  * as an option).  AGN_OPT_SGD (the default): g = -eta * gradient.
  * AGN_OPT_ADAM (Kingma & Ba 2015): each worker keeps first and second

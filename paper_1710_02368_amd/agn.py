@@ -28,7 +28,8 @@ EXPORTED = [
     "agn_num_params", "agn_last_error", "agn_destroy", "agn_set_central",
     "agn_worker_params", "agn_debug_batch_indices", "agn_set_kernel_timing",
     "agn_kernel_timing", "agn_kernel_class_work", "agn_debug_delta", "agn_set_normalization",
-    "agn_set_optimizer", "agn_evaluate", "agn_temporal_efficiency",
+    "agn_set_optimizer", "agn_evaluate", "agn_temporal_efficiency", "agn_set_staleness_scaling",
+    "agn_staleness",
 ]
 
 
@@ -71,6 +72,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
                              ctypes.POINTER(vp)]),
         "agn_set_stream": (i32, [vp, vp]),
         "agn_set_normalization": (i32, [vp, i32]),
+        "agn_set_staleness_scaling": (i32, [vp, i32]),
+        "agn_staleness": (i32, [vp, ctypes.POINTER(i64)]),
         "agn_set_optimizer": (i32, [vp, i32, ctypes.c_float, ctypes.c_float, ctypes.c_float]),
         "agn_round": (i32, [vp, ctypes.POINTER(agn_data), ctypes.POINTER(ctypes.c_int32)]),
         "agn_evaluate": (i32, [vp, ctypes.POINTER(agn_data), vp, vp, ctypes.POINTER(agn_eval_result)]),
@@ -132,6 +135,16 @@ def agn_create(dims: Sequence[int], batch: int, n: int, lam: int, eta: float, se
 
 def agn_set_normalization(ctx, normalize: bool):
     _check(load_library().agn_set_normalization(ctx, int(bool(normalize))), ctx)
+
+
+def agn_set_staleness_scaling(ctx, enable: bool):
+    _check(load_library().agn_set_staleness_scaling(ctx, int(bool(enable))), ctx)
+
+
+def agn_staleness(ctx, n: int):
+    out = (ctypes.c_int64 * int(n))()
+    _check(load_library().agn_staleness(ctx, out), ctx)
+    return [int(v) for v in out]
 
 
 AGN_OPT_SGD, AGN_OPT_ADAM = 0, 1
@@ -241,7 +254,8 @@ def agn_kernel_class_work(ctx, kernel_class: int):
 class AGN:
     """One AGN context on the current ROCm device and stream."""
 
-    def __init__(self, dims, n, lam, eta, m, seed, dtype="fp32", normalize=True, adam=None):
+    def __init__(self, dims, n, lam, eta, m, seed, dtype="fp32", normalize=True, adam=None,
+                 staleness_scaled=False):
         """adam: None (SGD) or (beta1, beta2, eps)."""
         self.dims = tuple(int(d) for d in dims)
         self.n, self.lam, self.m = int(n), int(lam), int(m)
@@ -252,6 +266,8 @@ class AGN:
             agn_set_normalization(self.ctx, False)
         if adam is not None:
             agn_set_optimizer(self.ctx, AGN_OPT_ADAM, *adam)
+        if staleness_scaled:
+            agn_set_staleness_scaling(self.ctx, True)
         self.P = agn_num_params(self.ctx)
 
     def close(self):
@@ -273,6 +289,9 @@ class AGN:
         out = torch.empty(self.P, dtype=torch.float32, device="cuda")
         agn_central(self.ctx, out)
         return out
+
+    def staleness(self):
+        return agn_staleness(self.ctx, self.n)
 
     def loss(self):
         torch = _torch()

@@ -68,6 +68,11 @@ struct agn_ctx {
   int device = 0;
   int use_head = 0;  // fused output-layer kernels (few classes)
   int normalize = 1; // commit a / lambda (AGN) or a (DOWNPOUR with local exploration)
+  int staleness_scaling = 0;           // scale each commit by 1 / (tau + 1)
+  float* commit_scale = nullptr;       // device, n factors of the current round
+  std::vector<int64_t> pulled_version; // per worker: commits applied when it last pulled
+  std::vector<int64_t> last_staleness; // per commit position of the last round
+  int64_t version = 0;                 // commits applied so far
   int optimizer = AGN_OPT_SGD;
   float beta1 = 0.f, beta2 = 0.f, adam_eps = 0.f;
   float* mom_m = nullptr;  // Adam moment estimates [n][P_pad] (allocated on selection)
@@ -377,6 +382,7 @@ int enqueue_round(agn_ctx* c, const agn_data* d) {
   ca.delta = c->buf[(c->lam - 1) & 1];
   ca.snap16 = c->snap16;
   ca.order = c->order;
+  ca.scale = c->staleness_scaling ? c->commit_scale : nullptr;
   ca.round = c->round_dev;
   ca.pstride = c->P_pad;
   ca.count = c->P_pad;
@@ -547,6 +553,8 @@ int agn_create(const agn_shapes* shapes, int32_t n, int32_t lambda, float eta, u
   c->n = n;
   c->lam = lambda;
   c->eta = eta;
+  c->pulled_version.assign(n, 0);
+  c->last_staleness.assign(n, 0);
   for (int l = 0; l <= L; ++l) c->dims[l] = shapes->dims[l];
 
   // parameter layout: W_l rows padded to 8 elements, tensors 64-element aligned
@@ -587,6 +595,7 @@ int agn_create(const agn_shapes* shapes, int32_t n, int32_t lambda, float eta, u
             dalloc(c, &c->Z, (int64_t)n * c->m * c->lda[L]) == hipSuccess &&
             dalloc(c, &c->loss, (int64_t)n * lambda * c->m) == hipSuccess &&
             dalloc(c, &c->order, n) == hipSuccess && dalloc(c, &c->round_dev, 1) == hipSuccess &&
+            dalloc(c, &c->commit_scale, n) == hipSuccess &&
             dalloc(c, &c->zero, 1024) == hipSuccess;
   if (ok && bf)
     ok = dalloc(c, &c->snap16, nps) == hipSuccess && dalloc(c, &c->buf16[0], nps) == hipSuccess &&
@@ -642,6 +651,23 @@ int agn_set_normalization(agn_ctx* c, int32_t normalize) {
   return AGN_OK;
 }
 
+int agn_set_staleness_scaling(agn_ctx* c, int32_t enable) {
+  if (int r = check_ctx(c)) return r;
+  if (enable != 0 && enable != 1) return fail(c, AGN_EINVAL, "enable must be 0 or 1");
+  if (c->rounds != 0) return fail(c, AGN_ESTATE, "agn_set_staleness_scaling is allowed only before the first round");
+  c->staleness_scaling = enable;
+  drop_graph(c);
+  return AGN_OK;
+}
+
+int agn_staleness(agn_ctx* c, int64_t* out) {
+  if (int r = check_ctx(c)) return r;
+  if (!out) return fail(c, AGN_EINVAL, "out is NULL");
+  if (c->rounds == 0) return fail(c, AGN_ESTATE, "no round has run yet");
+  for (int j = 0; j < c->n; ++j) out[j] = c->last_staleness[j];
+  return AGN_OK;
+}
+
 int agn_set_optimizer(agn_ctx* c, int32_t optimizer, float beta1, float beta2, float eps) {
   if (int r = check_ctx(c)) return r;
   if (optimizer != AGN_OPT_SGD && optimizer != AGN_OPT_ADAM) return fail(c, AGN_EINVAL, "unknown optimizer");
@@ -688,8 +714,17 @@ int agn_round(agn_ctx* c, const agn_data* d, const int32_t* order) {
     }
   }
   if (int r = set_device(c)) return r;
+  // staleness of each commit (commits applied since the worker's last pull;
+  // it pulls right after its own commit) and, when enabled, its scale
+  std::vector<int64_t> tau(c->n);
+  std::vector<float> scale(c->n);
+  for (int j = 0; j < c->n; ++j) {
+    tau[j] = c->version + j - c->pulled_version[order[j]];
+    scale[j] = (float)(1.0 / (double)(tau[j] + 1));
+  }
   // the commit order of this round (read by the commit kernel)
-  HIP_CHECK(c, launch_set_order(order, c->n, c->order, c->stream));
+  HIP_CHECK(c, launch_set_order(order, c->staleness_scaling ? scale.data() : nullptr, c->n, c->order,
+                                c->commit_scale, c->stream));
   bool timing = false;
   for (int k = 0; k < AGN_K_EVAL; ++k) timing = timing || c->timing[k].enabled;
   if (timing) {  // eager launches, each timed class bracketed by events
@@ -721,6 +756,9 @@ int agn_round(agn_ctx* c, const agn_data* d, const int32_t* order) {
   }
   c->N_fixed = d->num_samples;
   ++c->rounds;
+  for (int j = 0; j < c->n; ++j) c->pulled_version[order[j]] = c->version + j + 1;
+  c->version += c->n;
+  c->last_staleness = tau;
   return AGN_OK;
 }
 

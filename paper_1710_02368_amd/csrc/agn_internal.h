@@ -154,6 +154,7 @@ struct CommitArgs {
   const float* delta;      // [n][P_pad] normalized deltas of the round
   uint16_t* snap16;        // bf16 shadow of the pulled copies (or null)
   const int32_t* order;    // device, n entries
+  const float* scale;      // device, n factors by commit position (null: unscaled commits)
   int64_t* round;          // device round counter (incremented)
   int64_t pstride;         // P_pad
   int64_t count;           // elements to process (P_pad)
@@ -175,7 +176,10 @@ hipError_t launch_unpack(const PackArgs& pa, const float* packed, float* padded,
                          uint16_t* padded16, int32_t copies, int64_t pstride, hipStream_t s);
 hipError_t launch_loss_reduce(const float* loss, int32_t n, int64_t per_worker, float* out,
                               hipStream_t s);
-hipError_t launch_set_order(const int32_t* host_order, int32_t n, int32_t* dev_order,
+// writes the round's commit order and, when dev_scale is not null, the
+// commits' scale factors (host_scale) to the device
+hipError_t launch_set_order(const int32_t* host_order, const float* host_scale, int32_t n,
+                            int32_t* dev_order, float* dev_scale,
                             hipStream_t s);
 hipError_t launch_batch_indices(int32_t worker, int64_t t, int32_t mb, int64_t S, int64_t* out,
                                 hipStream_t s);

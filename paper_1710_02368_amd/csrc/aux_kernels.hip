@@ -62,7 +62,9 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(SoftmaxArgs a) {
 // 1/lambda normalization (stored by the last local step).  In commit order
 // j = 0..n-1, worker k = order[j]:  c <- c + delta_k;  pulled_k <- c.
 // Finally central <- c.  Elements are independent, so the sequential order
-// per element is exact and needs no atomics.
+// per element is exact and needs no atomics.  SCALED: c <- c + scale[j] *
+// delta_k, the staleness factor of the j-th commit (the DynSGD comparison
+// of Section 4).
 __device__ __forceinline__ void store_bf16x4(uint16_t* base, int64_t i4, f32x4 c) {
   uint2 h;
   h.x = (uint32_t)f32_to_bf16_rne(c.x) | ((uint32_t)f32_to_bf16_rne(c.y) << 16);
@@ -70,6 +72,7 @@ __device__ __forceinline__ void store_bf16x4(uint16_t* base, int64_t i4, f32x4 c
   reinterpret_cast<uint2*>(base)[i4] = h;
 }
 
+template <bool SCALED>
 __global__ __launch_bounds__(256) void commit_kernel(CommitArgs a) {
   const int64_t e4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t n4 = a.count / 4, ps4 = a.pstride / 4;
@@ -89,14 +92,20 @@ __global__ __launch_bounds__(256) void commit_kernel(CommitArgs a) {
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        c += d[u];
+        if (SCALED)
+          c += a.scale[j + u] * d[u];
+        else
+          c += d[u];
         snap[(int64_t)kk[u] * ps4 + e4] = c;
         if (a.snap16) store_bf16x4(a.snap16, (int64_t)kk[u] * ps4 + e4, c);
       }
     }
     for (; j < a.n; ++j) {
       const int k = a.order[j];
-      c += __builtin_nontemporal_load(&delta[(int64_t)k * ps4 + e4]);
+      if (SCALED)
+        c += a.scale[j] * __builtin_nontemporal_load(&delta[(int64_t)k * ps4 + e4]);
+      else
+        c += __builtin_nontemporal_load(&delta[(int64_t)k * ps4 + e4]);
       snap[(int64_t)k * ps4 + e4] = c;
       if (a.snap16) store_bf16x4(a.snap16, (int64_t)k * ps4 + e4, c);
     }
@@ -154,10 +163,14 @@ __global__ __launch_bounds__(256) void loss_reduce_kernel(const float* loss, int
 
 struct OrderArg {
   int32_t v[256];
+  float sc[256];
 };
-__global__ void set_order_kernel(OrderArg o, int32_t n, int32_t* dst) {
+__global__ void set_order_kernel(OrderArg o, int32_t n, int32_t* dst, float* dst_scale) {
   const int j = threadIdx.x;
-  if (j < n) dst[j] = o.v[j];
+  if (j < n) {
+    dst[j] = o.v[j];
+    if (dst_scale) dst_scale[j] = o.sc[j];
+  }
 }
 
 __global__ void batch_indices_kernel(int32_t worker, int64_t t, int32_t mb, int64_t S, int64_t* out) {
@@ -267,7 +280,10 @@ hipError_t launch_softmax_ce(const SoftmaxArgs& a, hipStream_t s) {
 
 hipError_t launch_commit(const CommitArgs& a, hipStream_t s) {
   const int64_t n4 = a.count / 4;
-  hipLaunchKernelGGL(commit_kernel, dim3(blocks_for(n4 > 0 ? n4 : 1, 256)), dim3(256), 0, s, a);
+  if (a.scale)
+    hipLaunchKernelGGL(commit_kernel<true>, dim3(blocks_for(n4 > 0 ? n4 : 1, 256)), dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(commit_kernel<false>, dim3(blocks_for(n4 > 0 ? n4 : 1, 256)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -289,10 +305,15 @@ hipError_t launch_loss_reduce(const float* loss, int32_t n, int64_t per_worker, 
   return hipGetLastError();
 }
 
-hipError_t launch_set_order(const int32_t* host_order, int32_t n, int32_t* dev_order, hipStream_t s) {
+hipError_t launch_set_order(const int32_t* host_order, const float* host_scale, int32_t n,
+                            int32_t* dev_order, float* dev_scale, hipStream_t s) {
   OrderArg o;
-  for (int j = 0; j < 256; ++j) o.v[j] = j < n ? host_order[j] : 0;
-  hipLaunchKernelGGL(set_order_kernel, dim3(1), dim3(256), 0, s, o, n, dev_order);
+  for (int j = 0; j < 256; ++j) {
+    o.v[j] = j < n ? host_order[j] : 0;
+    o.sc[j] = (j < n && host_scale) ? host_scale[j] : 1.f;
+  }
+  hipLaunchKernelGGL(set_order_kernel, dim3(1), dim3(256), 0, s, o, n, dev_order,
+                     host_scale ? dev_scale : nullptr);
   return hipGetLastError();
 }
 

@@ -74,6 +74,16 @@ SMALL = [
      True, ADAM),
     ("adam_many_classes", (60, 50, 40), 3, 2, 24, 0.002, 2, 300, "gauss_linear", "permutation", "fp32", True, ADAM),
     ("bf16_adam", (200, 130, 70, 10), 3, 3, 40, 0.002, 2, 650, "gauss_linear", "permutation", "bf16", True, ADAM),
+    # staleness-scaled commits (Section 4's DynSGD comparison): with the
+    # normalized delta, and DynSGD-style with the accumulated update
+    ("stale_scaled_ragged", (200, 130, 70, 10), 3, 3, 40, 0.05, 3, 650, "gauss_linear", "permutation", "fp32",
+     True, None, True),
+    ("dynsgd_accumulated_dl", (100, 200, 136, 10), 4, 3, 100, 0.02, 3, 900, "sparse_teacher2", "permutation",
+     "fp32", False, None, True),
+    ("dynsgd_sequential", (64, 48, 10), 5, 2, 16, 0.05, 4, 400, "gauss_linear", "sequential", "fp32",
+     False, None, True),
+    ("bf16_dynsgd", (200, 130, 70, 10), 3, 3, 40, 0.02, 2, 650, "gauss_linear", "permutation", "bf16",
+     False, None, True),
 ]
 
 
@@ -98,15 +108,16 @@ def delta_err(got, disp, start, dims, div, tol):
     return worst, where
 
 
-def run_parity(wl, tol1, tolN, check_workers=True, normalize=True, adam=None):
+def run_parity(wl, tol1, tolN, check_workers=True, normalize=True, adam=None, staleness_scaled=False):
     agn = _agn()
     import torch
     X, y = W.make_data(wl)
     orders = W.commit_orders(wl)
     xd, yd = to_device(X, y)
-    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, dtype=wl.dtype, normalize=normalize, adam=adam)
+    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, dtype=wl.dtype, normalize=normalize, adam=adam,
+                staleness_scaled=staleness_scaled)
     o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, bf16=wl.dtype == "bf16",
-                  normalize=normalize, adam=adam)
+                  normalize=normalize, adam=adam, staleness_scaled=staleness_scaled)
     # the initial central variable (same generator on both sides)
     init_err, _ = rel_err(g.central().cpu().numpy(), o.central_flat(), wl.dims)
     assert init_err <= 1e-7, f"init mismatch {init_err}"
@@ -115,6 +126,7 @@ def run_parity(wl, tol1, tolN, check_workers=True, normalize=True, adam=None):
         g.round(xd, yd, order)
         o.round(X, y, order)
         tol = tol1 if r == 1 else tolN
+        assert g.staleness() == o.staleness[-1]     # integer bookkeeping: exact
         err, where = rel_err(g.central().cpu().numpy(), o.central_flat(), wl.dims)
         print(f"{wl.name} round {r}: central rel err {err:.3e} ({where})", flush=True)
         assert err <= tol, (r, where, err)
@@ -147,9 +159,10 @@ def test_small_shapes(case):
     name, dims, n, lam, m, eta, R, N, data, order, dtype = case[:11]
     normalize = case[11] if len(case) > 11 else True
     adam = case[12] if len(case) > 12 else None
+    scaled = case[13] if len(case) > 13 else False
     wl = W.small_workload(name, dims, n, lam, m, eta, R, N, data=data, order=order, dtype=dtype)
     tol1, tolN = (FP32_TOL_1, FP32_TOL_N) if dtype == "fp32" else (BF16_TOL, BF16_TOL)
-    run_parity(wl, tol1, tolN, normalize=normalize, adam=adam)
+    run_parity(wl, tol1, tolN, normalize=normalize, adam=adam, staleness_scaled=scaled)
 
 
 def test_downpour_lambda1_rules_coincide():
@@ -168,6 +181,43 @@ def test_downpour_lambda1_rules_coincide():
         res.append(g.central().cpu().numpy())
         g.close()
     np.testing.assert_array_equal(res[0], res[1])
+
+
+def test_staleness_scaling_one_worker_is_plain():
+    """n = 1: every commit has staleness 0, its scale is exactly 1, and the
+    scaled commit is bitwise the plain one."""
+    agn = _agn()
+    wl = W.small_workload("s1", (100, 200, 136, 10), 1, 3, 100, 0.05, 3, 400, data="gauss_linear",
+                          order="sequential")
+    X, y = W.make_data(wl)
+    xd, yd = to_device(X, y)
+    res = []
+    for scaled in (False, True):
+        g = agn.AGN(wl.dims, 1, wl.lam, wl.eta, wl.m, seed=wl.seed, staleness_scaled=scaled)
+        for order in W.commit_orders(wl):
+            g.round(xd, yd, order)
+            assert g.staleness() == [0]
+        res.append(g.central().cpu().numpy())
+        g.close()
+    np.testing.assert_array_equal(res[0], res[1])
+
+
+def test_set_staleness_scaling_errors():
+    agn = _agn()
+    g = agn.AGN((20, 16, 6), 2, 1, 0.05, 8, seed=1)
+    assert agn.load_library().agn_set_staleness_scaling(g.ctx, 2) == -1   # (the binding passes a bool)
+    with pytest.raises(agn.AGNError) as ei:
+        g.staleness()
+    assert ei.value.code == -4
+    wl = W.small_workload("se", (20, 16, 6), 2, 1, 8, 0.05, 1, 64)
+    X, y = W.make_data(wl)
+    xd, yd = to_device(X, y)
+    g.round(xd, yd, [1, 0])
+    assert g.staleness() == [0, 1]
+    with pytest.raises(agn.AGNError) as ei:
+        agn.agn_set_staleness_scaling(g.ctx, True)
+    assert ei.value.code == -4
+    g.close()
 
 
 def test_set_optimizer_errors():
