@@ -270,8 +270,18 @@ __device__ __forceinline__ void tile_dl(const GemmArgs& g, const int logical, fl
   // accumulator (bi, bj, r) sits at row rbase + tile_idx<A_KC>(bi, 4*lg + r),
   // column cbase + tile_idx<B_KC>(bj, li)
 
-  // mask of the input-gradient epilogue first (oldest in the memory queue),
-  // so the K loop's counted waits cover it
+  // operands of the epilogue first, oldest in the memory queue: the
+  // forward's bias of this lane's two columns, the input gradient's mask.
+  // The loads are unconditional (indices clamped into the matrix; values
+  // outside it are never stored), so they issue back to back
+  float bpre[2] = {0.f, 0.f};
+  if (EPI == EPI_FWD_RELU || EPI == EPI_FWD_LINEAR) {
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj) {
+      const int col = min(cbase + tile_idx<B_KC>(bj, q.li), g.N - 1);
+      bpre[bj] = g.bias[(int64_t)worker * g.bstride + col];
+    }
+  }
   float pre[2][2][4];
   if (EPI == EPI_DX_MASK) {
     const float* mk = reinterpret_cast<const float*>(g.mask) + (int64_t)worker * g.mstride;
@@ -281,8 +291,9 @@ __device__ __forceinline__ void tile_dl(const GemmArgs& g, const int logical, fl
       for (int r = 0; r < 4; ++r)
 #pragma unroll
         for (int bj = 0; bj < 2; ++bj) {
-          const int row = rbase + tile_idx<A_KC>(bi, 4 * q.lg + r), col = cbase + tile_idx<B_KC>(bj, q.li);
-          pre[bi][bj][r] = (row < g.M && col < g.N) ? mk[(int64_t)row * g.ldm + col] : 0.f;
+          const int row = min(rbase + tile_idx<A_KC>(bi, 4 * q.lg + r), g.M - 1),
+                    col = min(cbase + tile_idx<B_KC>(bj, q.li), g.N - 1);
+          pre[bi][bj][r] = mk[(int64_t)row * g.ldm + col];
         }
   }
 
@@ -336,6 +347,17 @@ __device__ __forceinline__ void tile_dl(const GemmArgs& g, const int logical, fl
   if (nk4 + 2 < nk) step(nk4 + 2, f0, f1, st3, st2);
   // loads of the steps past the end (zero page) still write LDS
   wait_vm<0>();
+  // the epilogue operands are in registers now (nothing is in flight): use
+  // them here, in straight-line code, so that the compiler's own waits for
+  // them land here and not between the conditional stores below (where each
+  // would wait for the stores before it)
+  if (EPI == EPI_FWD_RELU || EPI == EPI_FWD_LINEAR) asm volatile("" ::"v"(bpre[0]), "v"(bpre[1]));
+  if (EPI == EPI_DX_MASK) {
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) asm volatile("" ::"v"(pre[bi][0][r]), "v"(pre[bi][1][r]));
+  }
 
 #pragma unroll
   for (int bi = 0; bi < 2; ++bi)
@@ -348,7 +370,7 @@ __device__ __forceinline__ void tile_dl(const GemmArgs& g, const int logical, fl
         const float v = acc[bi][bj][r];
         float* out = reinterpret_cast<float*>(g.out) + (int64_t)worker * g.ostride;
         if (EPI == EPI_FWD_RELU || EPI == EPI_FWD_LINEAR) {
-          float z = v + g.bias[(int64_t)worker * g.bstride + col];
+          float z = v + bpre[bj];
           if (EPI == EPI_FWD_RELU) z = z > 0.f ? z : 0.f;
           out[(int64_t)row * g.ldo + col] = z;
         } else {  // EPI_DX_MASK
