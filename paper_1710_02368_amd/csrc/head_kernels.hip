@@ -83,23 +83,34 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
       hv[r][q] = hp[r][i < d ? i : d - 1];
     }
   }
-  // W and b into LDS, float4 at a time (W rows are 16-byte aligned)
-  constexpr int NW4 = CMAX * LW / 4;
+  // W and b into LDS, float4 at a time (W rows are 16-byte aligned).  All
+  // loads first, unconditionally (row and column clamped into the padded W:
+  // rows are ldw >= d floats, ldw a multiple of 8), then the LDS writes with
+  // the parts outside C x d zeroed: the loads are in flight together
+  constexpr int NW4 = CMAX * LW / 4, WIT = (NW4 + 255) / 256;
+  float4 wv[WIT];
 #pragma unroll
-  for (int it = 0; it < (NW4 + 255) / 256; ++it) {
+  for (int it = 0; it < WIT; ++it) {
+    const int e4 = min(tid + 256 * it, NW4 - 1);
+    const int c = min(e4 / (LW / 4), C - 1), i = min(4 * (e4 % (LW / 4)), (int)a.ldw - 4);
+    wv[it] = *reinterpret_cast<const float4*>(W + (int64_t)c * a.ldw + i);
+  }
+#pragma unroll
+  for (int it = 0; it < WIT; ++it) {
     const int e4 = tid + 256 * it;
     if (NW4 % 256 != 0 && e4 >= NW4) break;
     const int c = e4 / (LW / 4), i = 4 * (e4 % (LW / 4));
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (c < C && i < d) {
-      v = *reinterpret_cast<const float4*>(W + (int64_t)c * a.ldw + i);
-      if (i + 1 >= d) v.y = 0.f;
-      if (i + 2 >= d) v.z = 0.f;
-      if (i + 3 >= d) v.w = 0.f;
-    }
+    float4 v = wv[it];
+    if (c >= C || i >= d) v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (i + 1 >= d) v.y = 0.f;
+    if (i + 2 >= d) v.z = 0.f;
+    if (i + 3 >= d) v.w = 0.f;
     *reinterpret_cast<float4*>(Ws + c * LW + i) = v;
   }
-  if (tid < CMAX) bs[tid] = tid < C ? bias[tid] : 0.f;
+  {
+    const float bv = bias[min(tid, C - 1)];  // (unconditional: clamped into the bias)
+    if (tid < CMAX) bs[tid] = tid < C ? bv : 0.f;
+  }
 #pragma unroll
   for (int r = 0; r < WR; ++r)
 #pragma unroll
@@ -250,18 +261,41 @@ __global__ __launch_bounds__(64 * HDW_WAVES) void head_dw_kernel(HeadDwArgs a) {
   const int64_t t = a.gather ? gather_step(a.g) : 0;
   const float* hb = a.h + (int64_t)k * a.hstride;
   const float* dzb = a.dz + (int64_t)k * a.dzstride;
+  const int64_t wo = (int64_t)k * a.pstride;
+  // operands of the epilogue first, all in flight together (indices clamped
+  // into the tensors, so the loads are unconditional): this thread's weights
+  // (class wave + 8s, input unit ic) and snapshot, and the bias
+  constexpr int CPW = (CMAX + HDW_WAVES - 1) / HDW_WAVES;
+  float wsrc[CPW], wsnap[CPW];
+#pragma unroll
+  for (int s = 0; s < CPW; ++s) {
+    const int64_t e = wo + (int64_t)min(wave + HDW_WAVES * s, C - 1) * a.ldw + ic;
+    wsrc[s] = a.w_src[e];
+    wsnap[s] = a.w_snap[e];
+  }
+  const float bsrc = a.b_src[wo + min(tid, C - 1)], bsnap = a.b_snap[wo + min(tid, C - 1)];
   float acc[CMAX];
 #pragma unroll
   for (int c = 0; c < CMAX; ++c) acc[c] = 0.f;
   // bias: thread (group, class) for tid < HDW_BG*CMAX
   const int bg = tid / CMAX, bc = tid % CMAX;
   float bsum = 0.f;
+  constexpr int FIT = (HDW_CHUNK * CMAX + 64 * HDW_WAVES - 1) / (64 * HDW_WAVES);
   for (int j0 = 0; j0 < a.m; j0 += HDW_CHUNK) {
     const int rows = min(HDW_CHUNK, a.m - j0);
+    // this chunk of dZ: loads first (clamped), then the LDS writes
+    float dv[FIT];
+#pragma unroll
+    for (int s = 0; s < FIT; ++s) {
+      const int e = min(tid + 64 * HDW_WAVES * s, rows * CMAX - 1);
+      const int r = e / CMAX, c = min(e - r * CMAX, C - 1);
+      dv[s] = dzb[(int64_t)(j0 + r) * a.lddz + c];
+    }
     __syncthreads();
-    for (int e = tid; e < rows * CMAX; e += 64 * HDW_WAVES) {
-      const int r = e / CMAX, c = e - r * CMAX;
-      dzs[e] = c < C ? dzb[(int64_t)(j0 + r) * a.lddz + c] : 0.f;
+#pragma unroll
+    for (int s = 0; s < FIT; ++s) {
+      const int e = tid + 64 * HDW_WAVES * s;
+      if (e < rows * CMAX) dzs[e] = e % CMAX < C ? dv[s] : 0.f;
     }
     __syncthreads();
     if (ib == 0 && bg < HDW_BG)
@@ -292,17 +326,24 @@ __global__ __launch_bounds__(64 * HDW_WAVES) void head_dw_kernel(HeadDwArgs a) {
   for (int c = 0; c < CMAX; ++c) part[wave][c][lane] = acc[c];
   if (ib == 0 && bg < HDW_BG) bpart[bg][bc] = bsum;
   __syncthreads();
-  const int64_t wo = (int64_t)k * a.pstride;
+  // the prefetched operands are in registers by now: use them here, in
+  // straight-line code, so that no wait for them lands between the stores
+#pragma unroll
+  for (int s = 0; s < CPW; ++s) asm volatile("" ::"v"(wsrc[s]), "v"(wsnap[s]));
+  asm volatile("" ::"v"(bsrc), "v"(bsnap));
   const AdamCoef ac = a.adam.on ? adam_coef(a.g, a.adam) : AdamCoef{1.f, 1.f};
-  for (int c = wave; c < C; c += HDW_WAVES) {
+#pragma unroll
+  for (int s = 0; s < CPW; ++s) {
+    const int c = wave + HDW_WAVES * s;
+    if (c >= C) break;
     float g = part[0][c][lane];
 #pragma unroll
     for (int w = 1; w < HDW_WAVES; ++w) g += part[w][c][lane];
     if (i < a.d) {
       const int64_t e = wo + (int64_t)c * a.ldw + i;
       const float step = a.adam.on ? adam_dir(g, a.adam.mw, a.adam.vw, e, a.adam, ac) : g;
-      const float nw = a.w_src[e] - a.eta * step;
-      a.w_dst[e] = a.last ? (nw - a.w_snap[e]) / a.lam : nw;
+      const float nw = wsrc[s] - a.eta * step;
+      a.w_dst[e] = a.last ? (nw - wsnap[s]) / a.lam : nw;
     }
   }
   if (ib == 0 && tid < C) {
@@ -311,8 +352,8 @@ __global__ __launch_bounds__(64 * HDW_WAVES) void head_dw_kernel(HeadDwArgs a) {
     for (int q = 1; q < HDW_BG; ++q) gb += bpart[q][tid];
     const int64_t e = wo + tid;
     const float step = a.adam.on ? adam_dir(gb, a.adam.mb, a.adam.vb, e, a.adam, ac) : gb;
-    const float nb = a.b_src[e] - a.eta * step;
-    a.b_dst[e] = a.last ? (nb - a.b_snap[e]) / a.lam : nb;
+    const float nb = bsrc - a.eta * step;
+    a.b_dst[e] = a.last ? (nb - bsnap) / a.lam : nb;
   }
 }
 
