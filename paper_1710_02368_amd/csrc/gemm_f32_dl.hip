@@ -42,6 +42,9 @@
 //     step, snapshot) tile of the epilogue is loaded into LDS by the same
 //     direct loads, so that every wait on the load counter has a known
 //     count.
+#include <cmath>
+#include <type_traits>
+
 #include "device_common.h"
 
 namespace agn {
@@ -466,14 +469,13 @@ __device__ __forceinline__ void fire_epi(const GemmArgs& g, const TileCoord& c, 
 }
 
 template <bool LAST>
-__device__ __forceinline__ void dw_tiles(const GemmArgs& g, int wg, int nwg, float* st0, float* st1, float* st2,
+__device__ __forceinline__ void dw_tiles(const GemmArgs& g, const TileList tl, float* st0, float* st1, float* st2,
                                          float* st3, float* epi, float* epi2) {
   constexpr int EPN = LAST ? 8 : 4;  // epilogue load instructions per wave and tile
-  const TileList tl = tiles_of_wg(tiles_dl(g), wg, nwg);
   if (tl.count == 0) return;
   const int tid = threadIdx.x;
   const Lanes q{tid >> 6, tid & 63, (tid >> 6) >> 1, (tid >> 6) & 1, tid & 15, (tid & 63) >> 4};
-  const int nk = (g.K + BKD - 1) / BKD;  // >= NS (checked on the host)
+  const int nk = (g.K + BKD - 1) / BKD;  // a multiple of NS (checked on the host)
 
   DwLoads ld;
   ld.a_base = reinterpret_cast<const float*>(g.a.ptr);
@@ -522,31 +524,44 @@ __device__ __forceinline__ void dw_tiles(const GemmArgs& g, int wg, int nwg, flo
 #pragma unroll
     for (int bj = 0; bj < 2; ++bj) acc[bi][bj] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // step counter: tile i, step kt of that tile; the issue side runs NS steps
-  // ahead: tile i2, step kt2
-  int i = 0, kt = 0, i2 = 0, kt2 = NS;
+  // the issue side runs NS steps ahead of the compute side: tile i2, step kt2
+  int i2 = 0, kt2 = NS;
   if (kt2 >= nk) {  // (nk == NS)
     kt2 -= nk;
     ++i2;
     ld.set_tile(g, tl, i2);
   }
 
-  auto step = [&](const Frags& cur, Frags& nxt, const float* rd, float* wr) {
+  // one K step: wait for the fragments of the next step, read them, issue
+  // the loads NS steps ahead, run this step's MFMAs
+  auto step = [&](auto vm, const Frags& cur, Frags& nxt, const float* rd, float* wr) {
     const int k0 = kt2 * BKD;
     const float* const src[4] = {ld.a_src(k0, 0), ld.a_src(k0, 1), ld.b_src(k0, 0), ld.b_src(k0, 1)};
-    // the epilogue loads of tile i were issued after the step loads up to
-    // step kt = NS-1 of tile i: until then they sit behind the next step's
-    if (kt <= NS - 2)
-      k_step<false, false, 4 * (NS - 2) + EPN>(q, cur, nxt, rd, wr, src, acc, bsum);
-    else
-      k_step<false, false, 4 * (NS - 2)>(q, cur, nxt, rd, wr, src, acc, bsum);
-    // advance the issue side
+    k_step<false, false, decltype(vm)::value>(q, cur, nxt, rd, wr, src, acc, bsum);
     if (++kt2 == nk) {
       kt2 = 0;
       ld.set_tile(g, tl, ++i2);
     }
-    if (++kt < nk) return;
-    // ---- tile i complete: epilogue (its operands in LDS since step NS-1)
+  };
+  // the epilogue loads of a tile were issued after the step loads up to
+  // its step NS-1: until then they sit behind the next step's loads
+  using VM_E = std::integral_constant<int, 4 * (NS - 2) + EPN>;
+  using VM_0 = std::integral_constant<int, 4 * (NS - 2)>;
+
+  for (int i = 0; i < tl.count; ++i) {
+    // K steps of tile i (nk a multiple of 4: step kt uses stage kt % 4 and
+    // fragment set kt % 2)
+    step(VM_E{}, f0, f1, st1, st0);
+    step(VM_E{}, f1, f0, st2, st1);
+    step(VM_E{}, f0, f1, st3, st2);
+    step(VM_0{}, f1, f0, st0, st3);
+    for (int kt = 4; kt < nk; kt += 4) {
+      step(VM_0{}, f0, f1, st1, st0);
+      step(VM_0{}, f1, f0, st2, st1);
+      step(VM_0{}, f0, f1, st3, st2);
+      step(VM_0{}, f1, f0, st0, st3);
+    }
+    // ---- epilogue of tile i (its operands in LDS since step NS-1)
     const TileCoord c = coord_of(g, tl.logical(i));
     const int64_t wo = (int64_t)c.worker * g.pstride;
     // lane holds rows tr = wm*32 + 2*(4*lg + r) + bi, column pairs
@@ -611,26 +626,13 @@ __device__ __forceinline__ void dw_tiles(const GemmArgs& g, int wg, int nwg, flo
 #pragma unroll
       for (int bj = 0; bj < 2; ++bj) acc[bi][bj] = f32x4{0.f, 0.f, 0.f, 0.f};
     bsum[0] = bsum[1] = 0.f;
-    kt = 0;
-    if (++i < tl.count) {
+    if (i + 1 < tl.count) {
       // every wave has read this tile's epilogue operands: load the next's
       wait_lgkm0();
       barrier();
-      fire_epi<LAST>(g, coord_of(g, tl.logical(i)), epi, epi2, q);
+      fire_epi<LAST>(g, coord_of(g, tl.logical(i + 1)), epi, epi2, q);
     }
-  };
-
-  // stage of step s: s % 4; fragment set: s % 2
-  const int total = tl.count * nk, total4 = total & ~3;
-  for (int s = 0; s < total4; s += 4) {
-    step(f0, f1, st1, st0);
-    step(f1, f0, st2, st1);
-    step(f0, f1, st3, st2);
-    step(f1, f0, st0, st3);
   }
-  if (total4 < total) step(f0, f1, st1, st0);
-  if (total4 + 1 < total) step(f1, f0, st2, st1);
-  if (total4 + 2 < total) step(f0, f1, st3, st2);
   // loads of the steps past the end (zero page) still write LDS
   wait_vm<0>();
 }
@@ -656,21 +658,44 @@ template <bool LAST>
 __global__ __launch_bounds__(NT) void gemm_f32_dl_dw_kernel(GemmArgs g) {
   DL_STAGES
   DL_EPI(LAST)
-  dw_tiles<LAST>(g, blockIdx.x, gridDim.x, st0, st1, st2, st3, epi, epi2);
+  dw_tiles<LAST>(g, tiles_of_wg(tiles_dl(g), blockIdx.x, gridDim.x), st0, st1, st2, st3, epi, epi2);
+}
+
+// Weight-gradient tiles of workgroup `pid` in the combined backward launch
+// (workgroups [0, n1pad) start with an input-gradient tile, the rest are
+// weight-gradient only; workgroup pid runs on XCD pid % 8).  Each XCD owns a
+// contiguous range of logical tiles (one worker's dZ and H share its L2),
+// handed out in contiguous runs: cb tiles to each of its weight-gradient-only
+// workgroups, then ca to each of its input-gradient workgroups, so that both
+// kinds finish together.
+__device__ __forceinline__ TileList split_tiles(int T, int pid, int n1pad, int ca, int cb) {
+  const int xcd = pid % kNumXcd, q = (T + kNumXcd - 1) / kNumXcd;
+  const int lo = xcd * q, hi = min(T, lo + q);
+  const int nb = ((int)gridDim.x - n1pad) / kNumXcd;
+  const int first = pid >= n1pad ? lo + ((pid - n1pad) / kNumXcd) * cb : lo + nb * cb + (pid / kNumXcd) * ca;
+  const int n = pid >= n1pad ? cb : ca;
+  TileList t;
+  t.first = first;
+  t.stride = 1;
+  t.count = max(0, min(hi, first + n) - first);
+  return t;
 }
 
 // input-gradient tiles (one per workgroup, spread evenly over the XCDs),
-// then the persistent weight-gradient workgroups of the same layer
+// and the weight-gradient tiles of the same layer on every workgroup
 template <bool LAST>
-__global__ __launch_bounds__(NT) void gemm_f32_dl_bwd_kernel(GemmArgs dx, GemmArgs dw, int n1, int n1pad) {
+__global__ __launch_bounds__(NT) void gemm_f32_dl_bwd_kernel(GemmArgs dx, GemmArgs dw, int n1, int n1pad, int ca,
+                                                             int cb) {
   DL_STAGES
   DL_EPI(LAST)
   const int pid = blockIdx.x;
-  if (pid < n1pad) {
-    if (pid < n1) tile_dl<true, false, EPI_DX_MASK>(dx, xcd_remap(pid, n1), st0, st1, st2, st3);
-  } else {
-    dw_tiles<LAST>(dw, pid - n1pad, gridDim.x - n1pad, st0, st1, st2, st3, epi, epi2);
+  if (pid < n1) {
+    tile_dl<true, false, EPI_DX_MASK>(dx, xcd_remap(pid, n1), st0, st1, st2, st3);
+    // every wave is done with the stages before the weight-gradient tiles load into them
+    wait_lgkm0();
+    barrier();
   }
+  dw_tiles<LAST>(dw, split_tiles(tiles_dl(dw), pid, n1pad, ca, cb), st0, st1, st2, st3, epi, epi2);
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
@@ -682,14 +707,14 @@ bool operand_ok(const Operand& op, bool kc, int outer_n, int K) {
 }
 
 // weight-gradient product: K-strided operands (B may be gathered when the
-// batch fits in a shard), at least NS K steps, 16-byte epilogue rows
+// batch fits in a shard), a multiple of NS K steps, 16-byte epilogue rows
 bool dw_ok(const GemmArgs& g) {
   if (g.epi != EPI_DW_UPDATE || !g.zero || g.adam.on) return false;  // (Adam: register-staged kernel)
   const Operand& a = g.a;
   const Operand& b = g.b;
   if (!a.vec || !b.vec || a.gather || !aligned16(a.ptr) || !aligned16(b.ptr)) return false;
   if (a.ld % 4 || a.wstride % 4 || b.ld % 4 || b.wstride % 4) return false;
-  if (g.M % 4 || g.N % 4 || (g.K + BKD - 1) / BKD < NS) return false;
+  if (g.M % 4 || g.N % 4 || ((g.K + BKD - 1) / BKD) % NS) return false;
   if (b.gather && g.K > g.g.S) return false;
   if (!aligned16(g.w_src) || !aligned16(g.w_dst) || g.ldw % 4 || g.pstride % 4) return false;
   return !g.last || aligned16(g.w_snap);
@@ -737,11 +762,23 @@ hipError_t launch_gemm_f32_dl_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStr
   const int t2 = dw_grid(dw);
   if (n2 > t2) n2 = t2;
   if (n2 < kNumXcd) n2 = kNumXcd;
+  // Split each XCD's q weight-gradient tiles so that an input-gradient
+  // workgroup (nkx K steps, then ca tiles) and a weight-gradient-only one
+  // (cb tiles) take about the same time.  A weight-gradient tile costs about
+  // three times its NS K steps (its epilogue reads and writes a 64 x 64
+  // block of weights; measured on 8 x 1000 x 1000 x 128: the split 3 / 5
+  // beats 1 / 7 and 4 / 4 by 4 % of the round)
+  const int q = (tiles_dl(dw) + kNumXcd - 1) / kNumXcd, a = n1pad / kNumXcd, b = n2 / kNumXcd;
+  const double u = 3.0 * NS, nkx = (dx.K + BKD - 1) / BKD;
+  int ca = (int)std::floor((q - b * nkx / u) / (a + b) + 0.5);
+  if (ca < 0) ca = 0;
+  if (ca * a > q) ca = q / a;
+  const int cb = (q - ca * a + b - 1) / b;
   const dim3 grid(n1pad + n2), block(NT);
   if (dw.last)
-    hipLaunchKernelGGL(gemm_f32_dl_bwd_kernel<true>, grid, block, 0, s, dx, dw, n1, n1pad);
+    hipLaunchKernelGGL(gemm_f32_dl_bwd_kernel<true>, grid, block, 0, s, dx, dw, n1, n1pad, ca, cb);
   else
-    hipLaunchKernelGGL(gemm_f32_dl_bwd_kernel<false>, grid, block, 0, s, dx, dw, n1, n1pad);
+    hipLaunchKernelGGL(gemm_f32_dl_bwd_kernel<false>, grid, block, 0, s, dx, dw, n1, n1pad, ca, cb);
   return hipGetLastError();
 }
 
