@@ -114,6 +114,12 @@ struct DirectLoader {
   int64_t ld;
   int outer0, outer_n, K;
   const float* rowp[2];      // KC: the lane's two rows (null past the edge)
+  // steps whose loads all lie inside K ("full" steps) load from
+  // fast[u] + offset(k0): the lane's row (KC) or column chunk (KS) clamped
+  // into the matrix -- rows and columns past the edge feed only outputs
+  // that are never stored, so any data will do there
+  const float* fast[2];
+  int lk[2];                 // KC: the lane's k offset inside a step
 
   __device__ void init(const Operand& op, const Gather& g, const float* zp, int64_t w, int o0, int on, int k,
                        int wave, int lane) {
@@ -128,12 +134,25 @@ struct DirectLoader {
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
         const int r = 8 * (2 * wave + u) + lane / 8;
-        const int o = o0 + r;
-        int64_t ri = o;
-        if (op.gather && o < on) ri = batch_row(w, t, g.mb, g.S, o);
+        const int o = o0 + r, oc = o < on ? o : on - 1;
+        const int64_t ri = op.gather ? batch_row(w, t, g.mb, g.S, oc) : oc;
         rowp[u] = o < on ? base + ri * ld : nullptr;
+        fast[u] = base + ri * ld;
+        lk[u] = 4 * ((lane % 8) ^ kc_key(r));
+      }
+    } else {
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const int j = 2 * wave + u;
+        const int o = o0 + 4 * ks_chunk(j, lane);
+        fast[u] = base + (int64_t)ks_row(j, lane) * ld + (o < on ? o : on - 4);  // (on % 4 == 0)
       }
     }
+  }
+
+  // source for a full step (every k of the step below K)
+  __device__ const float* src_full(int k0, int u) const {
+    return KC ? fast[u] + (k0 + lk[u]) : fast[u] + (int64_t)k0 * ld;
   }
 
   // source of this lane's 16 bytes in load instruction u (0, 1) of the K
@@ -331,23 +350,41 @@ __device__ __forceinline__ void tile_dl(const GemmArgs& g, const int logical, fl
   Frags f0, f1;
   read_frags<A_KC, B_KC>(st0, q.wm, q.wn, q.li, q.lg, f0);
 
-  auto step = [&](int kt, const Frags& cur, Frags& nxt, const float* rd, float* wr) {
+  // step kt loads step kt + NS: from the precomputed full-step sources
+  // while that step lies inside K, else through the bounds checks
+  auto step = [&](auto full, int kt, const Frags& cur, Frags& nxt, const float* rd, float* wr) {
     const int k0 = (kt + NS) * BKD;
-    const float* const src[4] = {la.src(k0, 0, q.wave, q.lane), la.src(k0, 1, q.wave, q.lane),
-                                 lb.src(k0, 0, q.wave, q.lane), lb.src(k0, 1, q.wave, q.lane)};
-    k_step<A_KC, B_KC, 4 * (NS - 2)>(q, cur, nxt, rd, wr, src, acc, bsum);
+    if constexpr (decltype(full)::value) {
+      const float* const src[4] = {la.src_full(k0, 0), la.src_full(k0, 1), lb.src_full(k0, 0),
+                                   lb.src_full(k0, 1)};
+      k_step<A_KC, B_KC, 4 * (NS - 2)>(q, cur, nxt, rd, wr, src, acc, bsum);
+    } else {
+      const float* const src[4] = {la.src(k0, 0, q.wave, q.lane), la.src(k0, 1, q.wave, q.lane),
+                                   lb.src(k0, 0, q.wave, q.lane), lb.src(k0, 1, q.wave, q.lane)};
+      k_step<A_KC, B_KC, 4 * (NS - 2)>(q, cur, nxt, rd, wr, src, acc, bsum);
+    }
   };
+  using Full = std::true_type;
+  using Checked = std::false_type;
   // stage of step kt: kt % 4; fragment set: kt % 2
   const int nk4 = nk & ~3;
-  for (int kt = 0; kt < nk4; kt += 4) {
-    step(kt, f0, f1, st1, st0);
-    step(kt + 1, f1, f0, st2, st1);
-    step(kt + 2, f0, f1, st3, st2);
-    step(kt + 3, f1, f0, st0, st3);
+  const int nfast = (g.K / BKD - NS > 0 ? g.K / BKD - NS : 0) & ~3;  // steps kt whose step kt+NS is full
+  int kt = 0;
+  for (; kt < nfast && kt < nk4; kt += 4) {
+    step(Full{}, kt, f0, f1, st1, st0);
+    step(Full{}, kt + 1, f1, f0, st2, st1);
+    step(Full{}, kt + 2, f0, f1, st3, st2);
+    step(Full{}, kt + 3, f1, f0, st0, st3);
   }
-  if (nk4 < nk) step(nk4, f0, f1, st1, st0);
-  if (nk4 + 1 < nk) step(nk4 + 1, f1, f0, st2, st1);
-  if (nk4 + 2 < nk) step(nk4 + 2, f0, f1, st3, st2);
+  for (; kt < nk4; kt += 4) {
+    step(Checked{}, kt, f0, f1, st1, st0);
+    step(Checked{}, kt + 1, f1, f0, st2, st1);
+    step(Checked{}, kt + 2, f0, f1, st3, st2);
+    step(Checked{}, kt + 3, f1, f0, st0, st3);
+  }
+  if (nk4 < nk) step(Checked{}, nk4, f0, f1, st1, st0);
+  if (nk4 + 1 < nk) step(Checked{}, nk4 + 1, f1, f0, st2, st1);
+  if (nk4 + 2 < nk) step(Checked{}, nk4 + 2, f0, f1, st3, st2);
   // loads of the steps past the end (zero page) still write LDS
   wait_vm<0>();
   // the epilogue operands are in registers now (nothing is in flight): use
