@@ -460,6 +460,13 @@ struct DwLoads {
   int64_t a_off, b_off;  // worker offsets
   int m0, n0, worker;
   bool live;
+  // Sources of the tile's steps that lie inside K, at k0 = 0: the lane's k
+  // row and column chunk (clamped into the matrix: columns past the edge
+  // feed only outputs that are never stored); usable when the tile is live
+  // and its gathered rows do not wrap around the shard's end
+  const float* fa[2];
+  const float* fb[2];
+  bool fast;
 
   __device__ void set_tile(const GemmArgs& g, const TileList& tl, int i) {
     live = i < tl.count;
@@ -469,7 +476,17 @@ struct DwLoads {
     n0 = c.n0;
     a_off = (int64_t)worker * a_ws;
     b_off = (int64_t)worker * b_ws;
+    fast = live && (!b_gather || tb + K <= S);
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int oa = m0 + 4 * cc[u], ob = n0 + 4 * cc[u];  // (M, N multiples of 4)
+      fa[u] = a_base + a_off + (int64_t)kl[u] * a_ld + (oa < M ? oa : M - 4);
+      const int64_t rb = b_gather ? (int64_t)worker * S + tb + kl[u] : (int64_t)kl[u];
+      fb[u] = b_base + b_off + rb * b_ld + (ob < N ? ob : N - 4);
+    }
   }
+  __device__ const float* a_full(int k0, int u) const { return fa[u] + (int64_t)k0 * a_ld; }
+  __device__ const float* b_full(int k0, int u) const { return fb[u] + (int64_t)k0 * b_ld; }
   __device__ const float* a_src(int k0, int u) const {
     const int kk = k0 + kl[u], o = m0 + 4 * cc[u];
     if (!live || kk >= K || o >= M) return zero;
@@ -573,7 +590,18 @@ __device__ __forceinline__ void dw_tiles(const GemmArgs& g, const TileList tl, f
   // the loads NS steps ahead, run this step's MFMAs
   auto step = [&](auto vm, const Frags& cur, Frags& nxt, const float* rd, float* wr) {
     const int k0 = kt2 * BKD;
-    const float* const src[4] = {ld.a_src(k0, 0), ld.a_src(k0, 1), ld.b_src(k0, 0), ld.b_src(k0, 1)};
+    const float* src[4];
+    if (ld.fast && k0 + BKD <= g.K) {  // (uniform) every load of the step inside K
+      src[0] = ld.a_full(k0, 0);
+      src[1] = ld.a_full(k0, 1);
+      src[2] = ld.b_full(k0, 0);
+      src[3] = ld.b_full(k0, 1);
+    } else {
+      src[0] = ld.a_src(k0, 0);
+      src[1] = ld.a_src(k0, 1);
+      src[2] = ld.b_src(k0, 0);
+      src[3] = ld.b_src(k0, 1);
+    }
     k_step<false, false, decltype(vm)::value>(q, cur, nxt, rd, wr, src, acc, bsum);
     if (++kt2 == nk) {
       kt2 = 0;
