@@ -201,6 +201,8 @@ def main():
     ap.add_argument("--optimizer", choices=["sgd", "adam"], default="sgd",
                     help="local rule: plain SGD (the paper's Eq. 1) or Adam (beta 0.9/0.999, eps 1e-8)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-eval", action="store_true",
+                    help="skip the held-out evaluation (counter passes of the round's kernels alone)")
     ap.add_argument("--cpu-budget", type=float, default=12.0)
     ap.add_argument("--commit", choices=sorted(COMMIT_RULES), default="agn",
                     help="commit rule: agn (a / lambda, the default), accumulated (a), or either scaled by "
@@ -306,7 +308,7 @@ def main():
     torch.cuda.synchronize()
 
     # evaluation of the trained central variable on the held-out set
-    ev = measure_eval(agn, g, wl, xh, yh_d, Xh, yh, cpu=not args.no_cpu_baseline)
+    ev = None if args.no_eval else measure_eval(agn, g, wl, xh, yh_d, Xh, yh, cpu=not args.no_cpu_baseline)
 
     value = args.steps * wl.worker_samples_per_round / dt
     wd = work[dominant]
@@ -345,8 +347,9 @@ def main():
                             "traffic": stored_traffic(wl.name, "commit")},
         "round_mfma_util": round(wl.flops_per_round / (dt / args.steps) / 1e12 / PEAK_TFLOPS[wl.dtype], 4),
         "kernels": breakdown,
-        "eval": ev,
     }
+    if ev is not None:
+        out["eval"] = ev
     g.close()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, X, y, orders, budget_s=args.cpu_budget, adam=adam,
