@@ -19,22 +19,16 @@
 //            (W_new - W_pulled) / lambda is stored instead.  Epilogues go
 //            through LDS so that outputs, masks and master weights move in
 //            16-byte row chunks.
-#include "device_common.h"
+#include "bf16_epilogue.h"
 
 namespace agn {
 namespace {
 
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-
-constexpr int TB = 128;          // tile edge (M and N)
 constexpr int BKH = 32;          // k per step
 constexpr int LDK = BKH + 8;     // LDS row stride (bf16 elements) of a K-contiguous [outer][k] tile
 constexpr int LDS_KS = TB + 32;  // LDS row stride (bf16 elements) of a K-strided [k][outer] tile
 constexpr int TILE = TB * LDK;   // bf16 elements per operand tile (either layout)
 static_assert(BKH * LDS_KS <= TILE, "K-strided tile fits the tile buffer");
-constexpr int NT = 256;
-constexpr int EPI_LD = TB + 4;   // LDS row stride (floats) of the epilogue accumulator tile
 // LDS per workgroup: the two double-buffered operand tiles, or (after the
 // K loop) the 128x128 float32 accumulator tile of the epilogue
 constexpr int LDS_BYTES = (4 * TILE * 2 > TB * EPI_LD * 4) ? 4 * TILE * 2 : TB * EPI_LD * 4;
@@ -146,192 +140,6 @@ __device__ __forceinline__ bf16x8 frag(const uint16_t* lds, int outer, int k0, i
 
 __host__ __device__ inline int tiles_of(const GemmArgs& g) { return ((g.M + TB - 1) / TB) * ((g.N + TB - 1) / TB) * g.batch; }
 
-// Weight-gradient epilogue through LDS: the float32 accumulator tile is
-// written to LDS, then every thread streams 16-byte chunks of rows
-// (W_src read, W_dst and its bf16 shadow written, 16 chunks in flight), so
-// the master-weight traffic is coalesced.  Needs 16-byte rows.
-__device__ __forceinline__ bool dw_vec_ok(const GemmArgs& g) {
-  const uintptr_t p = (uintptr_t)g.w_src | (uintptr_t)g.w_dst | (g.last ? (uintptr_t)g.w_snap : 0);
-  return (p & 15) == 0 && ((uintptr_t)g.w_dst16 & 7) == 0 && g.ldw % 4 == 0 && g.pstride % 4 == 0 && g.N % 4 == 0;
-}
-
-__device__ __forceinline__ void dw_epilogue_lds(const GemmArgs& g, int worker, int m0, int n0, const f32x16 (&acc)[2][2],
-                                                float* et, const AdamCoef& ac) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1, li = lane & 31, lh = lane >> 5;
-#pragma unroll
-  for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-    for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        et[(wm * 64 + 32 * bi + 8 * (r >> 2) + 4 * lh + (r & 3)) * EPI_LD + wn * 64 + 32 * bj + li] = acc[bi][bj][r];
-  __syncthreads();
-  const int64_t wo = (int64_t)worker * g.pstride;
-  constexpr int CH = TB * TB / 4 / NT;  // 16-byte chunks per thread
-#pragma unroll
-  for (int half = 0; half < 2; ++half) {
-    float4 w[CH / 2], sn[CH / 2];
-    int64_t e[CH / 2];
-    bool ok[CH / 2];
-#pragma unroll
-    for (int u = 0; u < CH / 2; ++u) {
-      const int c = tid + NT * (u + half * CH / 2), row = c / (TB / 4), col = 4 * (c % (TB / 4));
-      ok[u] = m0 + row < g.M && n0 + col < g.N;
-      e[u] = wo + (int64_t)(m0 + row) * g.ldw + n0 + col;
-      // unconditional loads (index clamped into the matrix, N a multiple
-      // of 4): all in flight together, used after the last is issued
-      const int64_t el = wo + (int64_t)min(m0 + row, g.M - 1) * g.ldw + min(n0 + col, g.N - 4);
-      w[u] = *reinterpret_cast<const float4*>(g.w_src + el);
-      sn[u] = *reinterpret_cast<const float4*>(g.w_snap + el);
-    }
-#pragma unroll
-    for (int u = 0; u < CH / 2; ++u)
-      asm volatile("" ::"v"(w[u].x), "v"(w[u].w), "v"(sn[u].x), "v"(sn[u].w));
-#pragma unroll
-    for (int u = 0; u < CH / 2; ++u) {
-      const int c = tid + NT * (u + half * CH / 2), row = c / (TB / 4), col = 4 * (c % (TB / 4));
-      float4 a = *reinterpret_cast<const float4*>(et + row * EPI_LD + col);
-      if (!ok[u]) continue;
-      if (g.adam.on) {
-        a.x = adam_dir(a.x, g.adam.mw, g.adam.vw, e[u], g.adam, ac);
-        a.y = adam_dir(a.y, g.adam.mw, g.adam.vw, e[u] + 1, g.adam, ac);
-        a.z = adam_dir(a.z, g.adam.mw, g.adam.vw, e[u] + 2, g.adam, ac);
-        a.w = adam_dir(a.w, g.adam.mw, g.adam.vw, e[u] + 3, g.adam, ac);
-      }
-      float4 nw = make_float4(w[u].x - g.eta * a.x, w[u].y - g.eta * a.y, w[u].z - g.eta * a.z, w[u].w - g.eta * a.w);
-      if (g.last) {
-        nw = make_float4((nw.x - sn[u].x) / g.lam, (nw.y - sn[u].y) / g.lam, (nw.z - sn[u].z) / g.lam,
-                         (nw.w - sn[u].w) / g.lam);
-        *reinterpret_cast<float4*>(g.w_dst + e[u]) = nw;
-      } else {
-        *reinterpret_cast<float4*>(g.w_dst + e[u]) = nw;
-        uint2 h;
-        h.x = f32_to_bf16_rne(nw.x) | ((uint32_t)f32_to_bf16_rne(nw.y) << 16);
-        h.y = f32_to_bf16_rne(nw.z) | ((uint32_t)f32_to_bf16_rne(nw.w) << 16);
-        *reinterpret_cast<uint2*>(g.w_dst16 + e[u]) = h;
-      }
-    }
-  }
-}
-
-// Epilogue of the forward and input-gradient products through LDS: the
-// float32 accumulator tile goes to LDS, then each thread takes row chunks of
-// the output (8 bf16 or 4 float32 columns) with their operands (bias, ReLU
-// mask) loaded up front from indices clamped into the matrix, and stores
-// each chunk with one 16-byte store (element by element only where a chunk
-// crosses the matrix edge, so padding columns are never written).
-template <int EPI>
-__device__ __forceinline__ void out_epilogue_lds(const GemmArgs& g, int worker, int m0, int n0,
-                                                 const f32x16 (&acc)[2][2], float* et) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1, li = lane & 31, lh = lane >> 5;
-  constexpr bool F32 = EPI == EPI_FWD_LINEAR;
-  constexpr int CW = F32 ? 4 : 8;            // columns per chunk
-  constexpr int CPR = TB / CW;               // chunks per row
-  constexpr int NC = TB * CPR / NT;          // chunks per thread
-  const int colc = (tid % CPR) * CW;         // this thread's chunk column (the same for all its chunks)
-  const int cbase = n0 + colc;
-  // bias of the chunk's columns (forward)
-  float bv[CW];
-  if (EPI == EPI_FWD_RELU || EPI == EPI_FWD_LINEAR) {
-#pragma unroll
-    for (int j = 0; j < CW; ++j) bv[j] = g.bias[(int64_t)worker * g.bstride + min(cbase + j, g.N - 1)];
-  }
-  // mask rows of the chunks (input gradient): 8 bf16 at a clamped chunk start
-  uint4 mv[NC];
-  if (EPI == EPI_DX_MASK) {
-    const int cm = min(cbase, (g.N - 1) / 8 * 8);  // (rows of the mask are padded to 8)
-#pragma unroll
-    for (int u = 0; u < NC; ++u) {
-      const int row = min(m0 + (tid + NT * u) / CPR, g.M - 1);
-      mv[u] = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(g.mask) +
-                                              (int64_t)worker * g.mstride + (int64_t)row * g.ldm + cm);
-    }
-  }
-  // the accumulator tile to LDS while those loads are in flight
-#pragma unroll
-  for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-    for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        et[(wm * 64 + 32 * bi + 8 * (r >> 2) + 4 * lh + (r & 3)) * EPI_LD + wn * 64 + 32 * bj + li] = acc[bi][bj][r];
-  __syncthreads();
-  if (EPI == EPI_FWD_RELU || EPI == EPI_FWD_LINEAR) {
-#pragma unroll
-    for (int j = 0; j < CW; j += 2) asm volatile("" ::"v"(bv[j]), "v"(bv[j + 1]));
-  }
-  if (EPI == EPI_DX_MASK) {
-#pragma unroll
-    for (int u = 0; u < NC; ++u) asm volatile("" ::"v"(mv[u].x), "v"(mv[u].w));
-  }
-  if (cbase >= g.N) return;
-  const bool whole = cbase + CW <= g.N;
-#pragma unroll
-  for (int u = 0; u < NC; ++u) {
-    const int rl = (tid + NT * u) / CPR, row = m0 + rl;
-    if (row >= g.M) continue;
-    float v[CW];
-#pragma unroll
-    for (int j = 0; j < CW; j += 4) {
-      const float4 a = *reinterpret_cast<const float4*>(et + rl * EPI_LD + colc + j);
-      v[j] = a.x;
-      v[j + 1] = a.y;
-      v[j + 2] = a.z;
-      v[j + 3] = a.w;
-    }
-    const int64_t o = (int64_t)worker * g.ostride + (int64_t)row * g.ldo + cbase;
-    if (F32) {
-      float* out = reinterpret_cast<float*>(g.out) + o;
-#pragma unroll
-      for (int j = 0; j < CW; ++j) v[j] += bv[j];
-      if (whole) {
-        *reinterpret_cast<float4*>(out) = make_float4(v[0], v[1], v[2], v[3]);
-      } else {
-        for (int j = 0; j < CW && cbase + j < g.N; ++j) out[j] = v[j];
-      }
-    } else {
-      uint16_t hv[CW];
-      if (EPI == EPI_FWD_RELU) {
-#pragma unroll
-        for (int j = 0; j < CW; ++j) {
-          const float h = v[j] + bv[j];
-          hv[j] = f32_to_bf16_rne(h > 0.f ? h : 0.f);
-        }
-      } else {  // EPI_DX_MASK
-        const uint32_t mw[4] = {mv[u].x, mv[u].y, mv[u].z, mv[u].w};
-#pragma unroll
-        for (int j = 0; j < CW; ++j) {
-          const uint16_t m = (uint16_t)(mw[j / 2] >> (16 * (j % 2)));
-          hv[j] = f32_to_bf16_rne(bf16_to_f32(m) > 0.f ? v[j] : 0.f);
-        }
-      }
-      uint16_t* out = reinterpret_cast<uint16_t*>(g.out) + o;
-      if (whole) {
-        uint4 pk;
-        pk.x = (uint32_t)hv[0] | ((uint32_t)hv[1] << 16);
-        pk.y = (uint32_t)hv[2] | ((uint32_t)hv[3] << 16);
-        pk.z = (uint32_t)hv[4] | ((uint32_t)hv[5] << 16);
-        pk.w = (uint32_t)hv[6] | ((uint32_t)hv[7] << 16);
-        *reinterpret_cast<uint4*>(out) = pk;
-      } else {
-        for (int j = 0; j < CW && cbase + j < g.N; ++j) out[j] = hv[j];
-      }
-    }
-  }
-}
-
-// the output can take 16-byte chunk stores (and the mask 16-byte loads)
-__device__ __forceinline__ bool out_vec_ok(const GemmArgs& g) {
-  const bool f32 = g.epi == EPI_FWD_LINEAR;
-  const int cw = f32 ? 4 : 8;
-  bool ok = ((uintptr_t)g.out & 15) == 0 && g.ldo % cw == 0 && g.ostride % cw == 0;
-  if (g.epi == EPI_DX_MASK)
-    ok = ok && ((uintptr_t)g.mask & 15) == 0 && g.ldm % 8 == 0 && g.mstride % 8 == 0 && g.ldm >= (g.N + 7) / 8 * 8;
-  return ok;
-}
-
 // One 128x128 output tile (logical tile id `logical`) of one product.
 // lds: LDS_BYTES of LDS.
 template <bool A_KC, bool B_KC, int EPI>
@@ -409,7 +217,10 @@ __device__ __forceinline__ void gemm_tile16(const GemmArgs& g, const int logical
   const AdamCoef ac = (EPI == EPI_DW_UPDATE && g.adam.on) ? adam_coef(g.g, g.adam) : AdamCoef{1.f, 1.f};
   if (EPI == EPI_DW_UPDATE && dw_vec_ok(g)) {
     // (the K loop ended with a barrier: the operand tiles are free)
-    dw_epilogue_lds(g, worker, m0, n0, acc, reinterpret_cast<float*>(lds), ac);
+    if (g.last)
+      dw_epilogue_lds<true>(g, worker, m0, n0, acc, reinterpret_cast<float*>(lds), ac);
+    else
+      dw_epilogue_lds<false>(g, worker, m0, n0, acc, reinterpret_cast<float*>(lds), ac);
   } else if (EPI != EPI_DW_UPDATE && out_vec_ok(g)) {
     out_epilogue_lds<EPI>(g, worker, m0, n0, acc, reinterpret_cast<float*>(lds));
   } else {
@@ -493,12 +304,14 @@ hipError_t go(const GemmArgs& g, hipStream_t s) {
 
 hipError_t launch_gemm_bf16_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s) {
   if (dx.epi != EPI_DX_MASK || dw.epi != EPI_DW_UPDATE) return hipErrorInvalidValue;
+  if (gemm_bf16_dl_ok(1, 0, dx) && gemm_bf16_dl_ok(0, 0, dw)) return launch_gemm_bf16_dl_bwd(dx, dw, s);
   const int n1 = tiles_of(dx), n1pad = (n1 + kNumXcd - 1) / kNumXcd * kNumXcd;
   hipLaunchKernelGGL(gemm_bf16_bwd_kernel, dim3(n1pad + tiles_of(dw)), dim3(NT), 0, s, dx, dw, n1, n1pad);
   return hipGetLastError();
 }
 
 hipError_t launch_gemm_bf16(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s) {
+  if (gemm_bf16_dl_ok(a_kc, b_kc, g)) return launch_gemm_bf16_dl(a_kc, b_kc, g, s);
   if (a_kc && b_kc && g.epi == EPI_FWD_RELU) return go<true, true, EPI_FWD_RELU>(g, s);
   if (a_kc && b_kc && g.epi == EPI_FWD_LINEAR) return go<true, true, EPI_FWD_LINEAR>(g, s);
   if (a_kc && !b_kc && g.epi == EPI_DX_MASK) return go<true, false, EPI_DX_MASK>(g, s);

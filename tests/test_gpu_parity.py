@@ -57,6 +57,17 @@ SMALL = [
     # schedule needs K = m >= 97 (four K steps) and widths divisible by 4
     ("dl_ragged", (100, 200, 136, 10), 3, 3, 100, 0.05, 3, 650, "sparse_teacher2", "permutation", "fp32"),
     ("bf16_dl_ragged", (100, 200, 136, 10), 3, 3, 100, 0.05, 2, 650, "sparse_teacher2", "permutation", "bf16"),
+    # bf16 direct-load products on every layer but the output layer's
+    # backward: ragged 128-tiles, a K tail (m = 100), the first layer's
+    # weight gradient over gathered rows whose mini-batch wraps round the
+    # shard's end (S = 216: steps at offsets 0, 100, 200)
+    ("bf16_dl_gather", (136, 264, 200, 10), 3, 3, 100, 0.05, 2, 650, "sparse_teacher2", "permutation", "bf16"),
+    # (Adam through the same kernels, at small widths: Adam's first step is
+    # +-eta times the sign of the gradient, and on wider layers some
+    # component's gradient cancels to the rounding level, where even the
+    # oracle's float32 and float64 products disagree on its sign)
+    ("bf16_dl_adam", (40, 48, 16, 10), 3, 3, 100, 0.002, 2, 650, "gauss_linear", "permutation", "bf16",
+     True, ADAM),
     # without the normalization step (Section 2: DOWNPOUR with local
     # exploration): the committed delta is the accumulated update itself
     ("accumulated_ragged", (200, 130, 70, 10), 3, 3, 40, 0.02, 3, 650, "gauss_linear", "permutation", "fp32",
