@@ -20,9 +20,9 @@ constexpr int EPI_LD = TB + 4;   // LDS row stride (floats) of the epilogue accu
 constexpr int EPI_BYTES = TB * EPI_LD * 4;
 
 // Weight-gradient epilogue through LDS: the float32 accumulator tile is
-// written to LDS, then every thread streams 16-byte chunks of rows
-// (W_src read, W_dst and its bf16 shadow written, 16 chunks in flight), so
-// the master-weight traffic is coalesced.  Needs 16-byte rows.
+// written to LDS, then every thread streams 16-byte chunks of rows (W_src
+// read, W_dst and its bf16 shadow written), so the master-weight traffic is
+// coalesced.  Needs 16-byte rows.
 __host__ __device__ inline bool dw_vec_ok(const GemmArgs& g) {
   const uintptr_t p = (uintptr_t)g.w_src | (uintptr_t)g.w_dst | (g.last ? (uintptr_t)g.w_snap : 0);
   return (p & 15) == 0 && ((uintptr_t)g.w_dst16 & 7) == 0 && g.ldw % 4 == 0 && g.pstride % 4 == 0 && g.N % 4 == 0;
@@ -33,59 +33,65 @@ __device__ __forceinline__ void dw_epilogue_lds(const GemmArgs& g, int worker, i
                                                 float* et, const AdamCoef& ac) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1, li = lane & 31, lh = lane >> 5;
-#pragma unroll
-  for (int bi = 0; bi < 2; ++bi)
-#pragma unroll
-    for (int bj = 0; bj < 2; ++bj)
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        et[(wm * 64 + 32 * bi + 8 * (r >> 2) + 4 * lh + (r & 3)) * EPI_LD + wn * 64 + 32 * bj + li] = acc[bi][bj][r];
-  __syncthreads();
   const int64_t wo = (int64_t)worker * g.pstride;
-  constexpr int CH = TB * TB / 4 / NT;  // 16-byte chunks per thread
+  constexpr int CH = TB * TB / 4 / NT;  // 16-byte chunks per thread: chunk c = tid + NT*u
+  // the weight (and, on the last step, snapshot) loads of a pass first,
+  // all in flight together: unconditional, from indices clamped into the
+  // matrix (N a multiple of 4); values outside it are never stored.  One
+  // pass over the tile's 16 chunks per thread, two on the last step (the
+  // snapshot doubles the registers).  (Loads issued after a store wait for
+  // that store too: one counter for both.)
+  constexpr int NP = LAST ? 2 : 1, PER = CH / NP;
+  float4 w[PER], sn[LAST ? PER : 1];
 #pragma unroll
-  for (int half = 0; half < 2; ++half) {
-    float4 w[CH / 2], sn[CH / 2];
-    int64_t e[CH / 2];
-    bool ok[CH / 2];
+  for (int pass = 0; pass < NP; ++pass) {
 #pragma unroll
-    for (int u = 0; u < CH / 2; ++u) {
-      const int c = tid + NT * (u + half * CH / 2), row = c / (TB / 4), col = 4 * (c % (TB / 4));
-      ok[u] = m0 + row < g.M && n0 + col < g.N;
-      e[u] = wo + (int64_t)(m0 + row) * g.ldw + n0 + col;
-      // unconditional loads (index clamped into the matrix, N a multiple
-      // of 4): all in flight together, used after the last is issued
+    for (int v = 0; v < PER; ++v) {
+      const int c = tid + NT * (pass * PER + v), row = c / (TB / 4), col = 4 * (c % (TB / 4));
       const int64_t el = wo + (int64_t)min(m0 + row, g.M - 1) * g.ldw + min(n0 + col, g.N - 4);
-      w[u] = *reinterpret_cast<const float4*>(g.w_src + el);
-      if (LAST) sn[u] = *reinterpret_cast<const float4*>(g.w_snap + el);
+      w[v] = *reinterpret_cast<const float4*>(g.w_src + el);
+      if (LAST) sn[v] = *reinterpret_cast<const float4*>(g.w_snap + el);
+    }
+    if (pass == 0) {
+      // the accumulator tile to LDS while they are in flight
+#pragma unroll
+      for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            et[(wm * 64 + 32 * bi + 8 * (r >> 2) + 4 * lh + (r & 3)) * EPI_LD + wn * 64 + 32 * bj + li] = acc[bi][bj][r];
+      __syncthreads();
     }
 #pragma unroll
-    for (int u = 0; u < CH / 2; ++u) {
-      asm volatile("" ::"v"(w[u].x), "v"(w[u].w));
-      if (LAST) asm volatile("" ::"v"(sn[u].x), "v"(sn[u].w));
+    for (int v = 0; v < PER; ++v) {
+      asm volatile("" ::"v"(w[v].x), "v"(w[v].w));
+      if (LAST) asm volatile("" ::"v"(sn[v].x), "v"(sn[v].w));
     }
 #pragma unroll
-    for (int u = 0; u < CH / 2; ++u) {
-      const int c = tid + NT * (u + half * CH / 2), row = c / (TB / 4), col = 4 * (c % (TB / 4));
+    for (int v = 0; v < PER; ++v) {
+      const int c = tid + NT * (pass * PER + v), row = c / (TB / 4), col = 4 * (c % (TB / 4));
       float4 a = *reinterpret_cast<const float4*>(et + row * EPI_LD + col);
-      if (!ok[u]) continue;
+      if (m0 + row >= g.M || n0 + col >= g.N) continue;
+      const int64_t e = wo + (int64_t)(m0 + row) * g.ldw + n0 + col;
       if (g.adam.on) {
-        a.x = adam_dir(a.x, g.adam.mw, g.adam.vw, e[u], g.adam, ac);
-        a.y = adam_dir(a.y, g.adam.mw, g.adam.vw, e[u] + 1, g.adam, ac);
-        a.z = adam_dir(a.z, g.adam.mw, g.adam.vw, e[u] + 2, g.adam, ac);
-        a.w = adam_dir(a.w, g.adam.mw, g.adam.vw, e[u] + 3, g.adam, ac);
+        a.x = adam_dir(a.x, g.adam.mw, g.adam.vw, e, g.adam, ac);
+        a.y = adam_dir(a.y, g.adam.mw, g.adam.vw, e + 1, g.adam, ac);
+        a.z = adam_dir(a.z, g.adam.mw, g.adam.vw, e + 2, g.adam, ac);
+        a.w = adam_dir(a.w, g.adam.mw, g.adam.vw, e + 3, g.adam, ac);
       }
-      float4 nw = make_float4(w[u].x - g.eta * a.x, w[u].y - g.eta * a.y, w[u].z - g.eta * a.z, w[u].w - g.eta * a.w);
+      float4 nw = make_float4(w[v].x - g.eta * a.x, w[v].y - g.eta * a.y, w[v].z - g.eta * a.z,
+                              w[v].w - g.eta * a.w);
       if (LAST) {
-        nw = make_float4((nw.x - sn[u].x) / g.lam, (nw.y - sn[u].y) / g.lam, (nw.z - sn[u].z) / g.lam,
-                         (nw.w - sn[u].w) / g.lam);
-        *reinterpret_cast<float4*>(g.w_dst + e[u]) = nw;
+        nw = make_float4((nw.x - sn[v].x) / g.lam, (nw.y - sn[v].y) / g.lam, (nw.z - sn[v].z) / g.lam,
+                         (nw.w - sn[v].w) / g.lam);
+        *reinterpret_cast<float4*>(g.w_dst + e) = nw;
       } else {
-        *reinterpret_cast<float4*>(g.w_dst + e[u]) = nw;
+        *reinterpret_cast<float4*>(g.w_dst + e) = nw;
         uint2 h;
         h.x = f32_to_bf16_rne(nw.x) | ((uint32_t)f32_to_bf16_rne(nw.y) << 16);
         h.y = f32_to_bf16_rne(nw.z) | ((uint32_t)f32_to_bf16_rne(nw.w) << 16);
-        *reinterpret_cast<uint2*>(g.w_dst16 + e[u]) = h;
+        *reinterpret_cast<uint2*>(g.w_dst16 + e) = h;
       }
     }
   }

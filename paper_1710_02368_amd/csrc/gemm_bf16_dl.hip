@@ -45,36 +45,52 @@ typedef short i16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 
-constexpr int BK = 32, NS = 4;       // k per step, LDS stages
-constexpr int TILE_B = TB * BK * 2;  // bytes of one operand tile
-constexpr int STAGE_B = 2 * TILE_B;  // A and B
-constexpr int LDS_DL = NS * STAGE_B > EPI_BYTES ? NS * STAGE_B : EPI_BYTES;
+constexpr int BK = 32, NS = 4;  // k per step, LDS stages
+
+// Geometry of a TR x TR output tile (TR = 128 or 256): four waves of
+// TR/2 x TR/2, each as NB x NB blocks of 32 x 32.
+template <int TR>
+struct Geo {
+  static constexpr int NB = TR / 64;        // blocks per wave and dimension
+  static constexpr int IPW = TR / 64;       // load instructions per wave, operand and K step
+  static constexpr int TILE = TR * BK * 2;  // bytes of one operand tile
+  static constexpr int STAGE = 2 * TILE;    // A and B
+  static constexpr int CPK = TR / 8;        // 16-byte chunks per k row of a K-strided tile
+  static constexpr int RPI = 512 / TR;      // k rows per load instruction of a K-strided tile
+};
+constexpr int LDS_DL = NS * Geo<128>::STAGE > EPI_BYTES ? NS * Geo<128>::STAGE : EPI_BYTES;
+// 256 x 256 tiles: the epilogue stages 128 rows at a time
+constexpr int EPI_BIG_LD = 256 + 4;
+constexpr int EPI_BIG_BYTES = 128 * EPI_BIG_LD * 4;
+constexpr int LDS_BIG = NS * Geo<256>::STAGE > EPI_BIG_BYTES ? NS * Geo<256>::STAGE : EPI_BIG_BYTES;
 
 __device__ __forceinline__ int kc_key(int r) { return ((r >> 1) ^ (r >> 3)) & 3; }
 __device__ __forceinline__ int ks_key(int k) { return (0xAC60 >> (4 * (k & 3))) & 15; }
 __device__ __forceinline__ int kc_byte(int r, int q) { return (4 * r + (q ^ kc_key(r))) * 16; }
-__device__ __forceinline__ int ks_byte(int k, int c) { return (16 * k + (c ^ ks_key(k))) * 16; }
+template <int TR>
+__device__ __forceinline__ int ks_byte(int k, int c) { return (Geo<TR>::CPK * k + (c ^ ks_key(k))) * 16; }
 
-// Per-lane sources of one operand's two load instructions per K step
-// (instruction j = 2*wave + u, u = 0, 1; lane l fills chunk 64j + l):
+// Per-lane sources of one operand's IPW load instructions per K step
+// (instruction j = IPW*wave + u, u < IPW; lane l fills chunk 64j + l):
 //   K-contiguous: row r = 16j + l/4 (rows may be gathered data-set rows),
 //     k chunk (l%4) ^ key(r);
-//   K-strided: k row 4j + l/16, column chunk (l%16) ^ key(k) (k rows may be
-//     gathered data-set rows: batch index kk of worker w is row
+//   K-strided: k row RPI*j + l/CPK, column chunk (l%CPK) ^ key(k) (k rows
+//     may be gathered data-set rows: batch index kk of worker w is row
 //     w*S + (tb + kk) mod S, tb = t*m mod S, with K <= S).
-template <bool KC>
+template <bool KC, int TR>
 struct Loader {
+  static constexpr int IPW = Geo<TR>::IPW, CPK = Geo<TR>::CPK, RPI = Geo<TR>::RPI;
   const uint16_t* zero;
-  const uint16_t* row[2];   // KC: the lane's row; KS: its column chunk at k row 0 (null past the edge)
-  // steps whose loads all lie inside K ("full" steps) load from
-  // fast[u] + offset(k0): the lane's row or column chunk clamped into the
-  // matrix (rows and columns past the edge feed only outputs that are never
-  // stored, so any data will do there)
-  const uint16_t* fast[2];
-  int lk[2];                // KC: the lane's k offset in a step; KS: its k row in a step
-  int64_t ld, rbase, tb, S;
+  // the lane's source at k0 = 0 in instruction u: its row (KC) or column
+  // chunk (KS), clamped into the matrix -- rows and columns past the edge
+  // feed only outputs that are never stored, so steps whose loads all lie
+  // inside K ("full" steps) load from fast[u] + offset(k0) whatever the lane
+  const uint16_t* fast[IPW];
+  int lk[IPW];     // KC: the lane's k offset in a step; KS: its k row in a step
+  uint32_t valid;  // bit u: instruction u's row / column chunk lies inside the matrix
+  int64_t ld, tb, S;
   int K, gather;
-  bool full_ok;             // false: a gathered mini-batch wraps round the shard's end
+  bool full_ok;    // false: a gathered mini-batch wraps round the shard's end
 
   __device__ void init(const Operand& op, const Gather& g, const void* zp, int64_t w, int o0, int on, int k,
                        int wave, int lane) {
@@ -83,30 +99,31 @@ struct Loader {
     ld = op.ld;
     K = k;
     gather = op.gather;
+    valid = 0;
     if (KC) {
       const int64_t t = op.gather ? gather_step(g) : 0;
-      rbase = tb = S = 0;
+      tb = S = 0;
       full_ok = true;
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int r = 16 * (2 * wave + u) + lane / 4;
+      for (int u = 0; u < IPW; ++u) {
+        const int r = 16 * (IPW * wave + u) + lane / 4;
         const int o = o0 + r, oc = o < on ? o : on - 1;
         const int64_t ri = op.gather ? batch_row(w, t, g.mb, g.S, oc) : oc;
-        row[u] = o < on ? base + ri * ld : nullptr;
+        valid |= (o < on ? 1u : 0u) << u;
         fast[u] = base + ri * ld;
         lk[u] = 8 * ((lane % 4) ^ kc_key(r));
       }
     } else {
       S = g.S;
       tb = op.gather ? (gather_step(g) * g.mb) % g.S : 0;
-      rbase = op.gather ? w * g.S : 0;
+      const int64_t rbase = op.gather ? w * g.S + tb : 0;
       full_ok = !op.gather || tb + K <= S;
 #pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        const int kr = 4 * (2 * wave + u) + lane / 16;
-        const int o = o0 + 8 * ((lane % 16) ^ ks_key(kr));
-        row[u] = o < on ? base + o : nullptr;
-        fast[u] = base + (op.gather ? rbase + tb + kr : kr) * ld + (o < on ? o : on - 8);
+      for (int u = 0; u < IPW; ++u) {
+        const int kr = RPI * (IPW * wave + u) + lane / CPK;
+        const int o = o0 + 8 * ((lane % CPK) ^ ks_key(kr));
+        valid |= (o < on ? 1u : 0u) << u;
+        fast[u] = base + (rbase + kr) * ld + (o < on ? o : on - 8);
         lk[u] = kr;
       }
     }
@@ -118,30 +135,28 @@ struct Loader {
   }
 
   // source of this lane's 16 bytes in load instruction u of the K step
-  // starting at k0; the zero page past an edge (also for k0 >= K)
+  // starting at k0; the zero page past an edge (also for k0 >= K).  A
+  // gathered k row past the shard's end wraps round to its start.
   __device__ const uint16_t* src(int k0, int u) const {
     const int kk = k0 + lk[u];
-    if (!row[u] || kk >= K) return zero;
-    if (KC) return row[u] + kk;
-    int64_t r = kk;
-    if (gather) {
-      const int64_t x = tb + kk;
-      r = rbase + (x >= S ? x - S : x);
-    }
-    return row[u] + r * ld;
+    if (!((valid >> u) & 1u) || kk >= K) return zero;
+    if (KC) return fast[u] + kk;
+    return fast[u] + (int64_t)(gather && tb + kk >= S ? k0 - S : k0) * ld;
   }
 };
 
 // Fragments of one wave for one K step: a[b][s] / b[b][s] is the operand of
 // block b in slice s (k = 16s + 8*lh + 0..7 of the step).
+template <int TR>
 struct Frags {
-  bf16x8 a[2][2], b[2][2];
+  bf16x8 a[Geo<TR>::NB][2], b[Geo<TR>::NB][2];
 };
 
-template <bool KC>
-__device__ __forceinline__ void frag(const char* tile, int outer_off, int li, int lh, bf16x8 (&f)[2][2]) {
+template <bool KC, int TR>
+__device__ __forceinline__ void frag(const char* tile, int outer_off, int li, int lh,
+                                     bf16x8 (&f)[Geo<TR>::NB][2]) {
 #pragma unroll
-  for (int b = 0; b < 2; ++b)
+  for (int b = 0; b < Geo<TR>::NB; ++b)
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       if (KC) {
@@ -158,7 +173,7 @@ __device__ __forceinline__ void frag(const char* tile, int outer_off, int li, in
         for (int c = 0; c < 2; ++c) {
           const int k = 16 * s + 8 * lh + 4 * c + (li % 16) / 4;
           const i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (lds_i16x4*)(tile + ks_byte(k, col / 8) + 2 * (col % 8)));
+              (lds_i16x4*)(tile + ks_byte<TR>(k, col / 8) + 2 * (col % 8)));
           h[c] = __builtin_bit_cast(bf16x4, v);
         }
         f[b][s] = __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7);
@@ -170,10 +185,10 @@ struct Lanes {
   int wave, lane, wm, wn, li, lh;
 };
 
-template <bool A_KC, bool B_KC>
-__device__ __forceinline__ void read_frags(const char* stage, const Lanes& q, Frags& f) {
-  frag<A_KC>(stage, q.wm * 64, q.li, q.lh, f.a);
-  frag<B_KC>(stage + TILE_B, q.wn * 64, q.li, q.lh, f.b);
+template <bool A_KC, bool B_KC, int TR>
+__device__ __forceinline__ void read_frags(const char* stage, const Lanes& q, Frags<TR>& f) {
+  frag<A_KC, TR>(stage, q.wm * (TR / 2), q.li, q.lh, f.a);
+  frag<B_KC, TR>(stage + Geo<TR>::TILE, q.wn * (TR / 2), q.li, q.lh, f.b);
 }
 
 __device__ __forceinline__ float sum8(const bf16x8& v) {
@@ -187,114 +202,237 @@ __device__ __forceinline__ float sum8(const bf16x8& v) {
 
 // K step: the fragments of this step are in `cur`; the loads of the next
 // NS-1 steps are in flight.  Wait until every wave has read `cur`'s stage
-// and the next step's loads have landed (at most the 4*(NS-2) load
+// and the next step's loads have landed (at most the 2*IPW*(NS-2) load
 // instructions issued after the next step's may remain), start the loads
 // `src` of the step NS ahead into `wr` (the stage this step came from), read
 // the next step's fragments from `rd` into `nxt`, run this step's MFMAs.
 // Loads past the end of K read the zero page, so every step has the same
 // shape.  BSUM: add this step's A operands (dZ^T of the weight-gradient
-// product) to the lane's two bias-gradient partial sums.
-template <bool A_KC, bool B_KC, bool BSUM>
-__device__ __forceinline__ void k_step(const Lanes& q, const Frags& cur, Frags& nxt, const char* rd, char* wr,
-                                       const uint16_t* const (&src)[4], f32x16 (&acc)[2][2], float (&bsum)[2]) {
+// product) to the lane's bias-gradient partial sums.
+template <bool A_KC, bool B_KC, int TR, bool BSUM>
+__device__ __forceinline__ void k_step(const Lanes& q, const Frags<TR>& cur, Frags<TR>& nxt, const char* rd,
+                                       char* wr, const uint16_t* const (&src)[2 * Geo<TR>::IPW],
+                                       f32x16 (&acc)[Geo<TR>::NB][Geo<TR>::NB], float (&bsum)[Geo<TR>::NB]) {
+  constexpr int NB = Geo<TR>::NB, IPW = Geo<TR>::IPW;
   // the scheduler keeps each step's work between its waits: it would
   // otherwise pull the next step's MFMAs up against the reads they need
   __builtin_amdgcn_sched_barrier(0);
   wait_lgkm0();
-  wait_vm<4 * (NS - 2)>();
+  wait_vm<2 * IPW * (NS - 2)>();
   barrier();
-  const uint32_t wa = lds_off(wr) + 2048 * q.wave;
-  fire(src[0], wa);
-  fire(src[1], wa + 1024);
-  fire(src[2], wa + TILE_B);
-  fire(src[3], wa + TILE_B + 1024);
-  read_frags<A_KC, B_KC>(rd, q, nxt);
+  const uint32_t wa = lds_off(wr) + 1024 * IPW * q.wave;
+#pragma unroll
+  for (int u = 0; u < IPW; ++u) fire(src[u], wa + 1024 * u);
+#pragma unroll
+  for (int u = 0; u < IPW; ++u) fire(src[IPW + u], wa + Geo<TR>::TILE + 1024 * u);
+  read_frags<A_KC, B_KC, TR>(rd, q, nxt);
 #pragma unroll
   for (int s = 0; s < 2; ++s)
 #pragma unroll
-    for (int bi = 0; bi < 2; ++bi)
+    for (int bi = 0; bi < NB; ++bi)
 #pragma unroll
-      for (int bj = 0; bj < 2; ++bj)
+      for (int bj = 0; bj < NB; ++bj)
         acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(cur.a[bi][s], cur.b[bj][s], acc[bi][bj], 0, 0, 0);
   if (BSUM) {
 #pragma unroll
-    for (int b = 0; b < 2; ++b) bsum[b] += sum8(cur.a[b][0]) + sum8(cur.a[b][1]);
+    for (int b = 0; b < NB; ++b) bsum[b] += sum8(cur.a[b][0]) + sum8(cur.a[b][1]);
   }
   // issue order: the next step's LDS reads spread between the MFMAs
-  constexpr int NR = (A_KC ? 4 : 8) + (B_KC ? 4 : 8);  // LDS read instructions per step
+  constexpr int NR = NB * ((A_KC ? 2 : 4) + (B_KC ? 2 : 4));  // LDS read instructions per step
+  constexpr int NM = 2 * NB * NB;                               // MFMAs per step
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);       // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x008, NM / 8, 0);  // MFMA
     __builtin_amdgcn_sched_group_barrier(0x100, NR / 4, 0);  // LDS read
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);       // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x008, NM / 8, 0);  // MFMA
   }
   __builtin_amdgcn_sched_barrier(0);
 }
 
+template <int TR>
 __host__ __device__ inline int tiles16(const GemmArgs& g) {
-  return ((g.M + TB - 1) / TB) * ((g.N + TB - 1) / TB) * g.batch;
+  return ((g.M + TR - 1) / TR) * ((g.N + TR - 1) / TR) * g.batch;
 }
 
-// One 128x128 output tile (logical tile id `logical`) of one product;
-// lds: LDS_DL bytes.
-template <bool A_KC, bool B_KC, int EPI>
+// Epilogue of a 256 x 256 tile of the forward or input-gradient product:
+// two passes of 128 rows.  In pass h the two waves with wm == h stage
+// their accumulators in LDS, then every thread stores 16-byte row chunks
+// (8 bf16 or 4 float32 columns) with their operands (bias, ReLU mask)
+// loaded up front from indices clamped into the matrix (element by element
+// only where a chunk crosses the matrix edge).
+template <int EPI>
+__device__ __forceinline__ void out_epilogue_big(const GemmArgs& g, int worker, int m0, int n0,
+                                                 const f32x16 (&acc)[4][4], float* et) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1, li = lane & 31, lh = lane >> 5;
+  constexpr bool F32 = EPI == EPI_FWD_LINEAR;
+  constexpr int CW = F32 ? 4 : 8;     // columns per chunk
+  constexpr int CPR = 256 / CW;       // chunks per row
+  constexpr int NC = 128 * CPR / NT;  // chunks per thread and pass
+  const int colc = (tid % CPR) * CW;  // this thread's chunk column (the same for all its chunks)
+  const int cbase = n0 + colc;
+  float bv[CW];
+  if (EPI == EPI_FWD_RELU || EPI == EPI_FWD_LINEAR) {
+#pragma unroll
+    for (int j = 0; j < CW; ++j) bv[j] = g.bias[(int64_t)worker * g.bstride + min(cbase + j, g.N - 1)];
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    uint4 mv[NC];
+    if (EPI == EPI_DX_MASK) {
+      const int cm = min(cbase, (g.N - 1) / 8 * 8);  // (rows of the mask are padded to 8)
+#pragma unroll
+      for (int u = 0; u < NC; ++u) {
+        const int row = min(m0 + 128 * h + (tid + NT * u) / CPR, g.M - 1);
+        mv[u] = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(g.mask) +
+                                                (int64_t)worker * g.mstride + (int64_t)row * g.ldm + cm);
+      }
+    }
+    if (h == 1) __syncthreads();  // every thread is done reading pass 0's rows
+    if (wm == h) {
+#pragma unroll
+      for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < 4; ++bj)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            et[(32 * bi + 8 * (r >> 2) + 4 * lh + (r & 3)) * EPI_BIG_LD + wn * 128 + 32 * bj + li] = acc[bi][bj][r];
+    }
+    __syncthreads();
+    if (EPI == EPI_FWD_RELU || EPI == EPI_FWD_LINEAR) {
+#pragma unroll
+      for (int j = 0; j < CW; j += 2) asm volatile("" ::"v"(bv[j]), "v"(bv[j + 1]));
+    }
+    if (EPI == EPI_DX_MASK) {
+#pragma unroll
+      for (int u = 0; u < NC; ++u) asm volatile("" ::"v"(mv[u].x), "v"(mv[u].w));
+    }
+    if (cbase >= g.N) continue;
+    const bool whole = cbase + CW <= g.N;
+#pragma unroll
+    for (int u = 0; u < NC; ++u) {
+      const int rl = (tid + NT * u) / CPR, row = m0 + 128 * h + rl;
+      if (row >= g.M) continue;
+      float v[CW];
+#pragma unroll
+      for (int j = 0; j < CW; j += 4) {
+        const float4 a = *reinterpret_cast<const float4*>(et + rl * EPI_BIG_LD + colc + j);
+        v[j] = a.x;
+        v[j + 1] = a.y;
+        v[j + 2] = a.z;
+        v[j + 3] = a.w;
+      }
+      const int64_t o = (int64_t)worker * g.ostride + (int64_t)row * g.ldo + cbase;
+      if (F32) {
+        float* out = reinterpret_cast<float*>(g.out) + o;
+#pragma unroll
+        for (int j = 0; j < CW; ++j) v[j] += bv[j];
+        if (whole) {
+          *reinterpret_cast<float4*>(out) = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+          for (int j = 0; j < CW && cbase + j < g.N; ++j) out[j] = v[j];
+        }
+      } else {
+        uint16_t hv[CW];
+        if (EPI == EPI_FWD_RELU) {
+#pragma unroll
+          for (int j = 0; j < CW; ++j) {
+            const float z = v[j] + bv[j];
+            hv[j] = f32_to_bf16_rne(z > 0.f ? z : 0.f);
+          }
+        } else {  // EPI_DX_MASK
+          const uint32_t mw[4] = {mv[u].x, mv[u].y, mv[u].z, mv[u].w};
+#pragma unroll
+          for (int j = 0; j < CW; ++j) {
+            const uint16_t m = (uint16_t)(mw[j / 2] >> (16 * (j % 2)));
+            hv[j] = f32_to_bf16_rne(bf16_to_f32(m) > 0.f ? v[j] : 0.f);
+          }
+        }
+        uint16_t* out = reinterpret_cast<uint16_t*>(g.out) + o;
+        if (whole) {
+          uint4 pk;
+          pk.x = (uint32_t)hv[0] | ((uint32_t)hv[1] << 16);
+          pk.y = (uint32_t)hv[2] | ((uint32_t)hv[3] << 16);
+          pk.z = (uint32_t)hv[4] | ((uint32_t)hv[5] << 16);
+          pk.w = (uint32_t)hv[6] | ((uint32_t)hv[7] << 16);
+          *reinterpret_cast<uint4*>(out) = pk;
+        } else {
+          for (int j = 0; j < CW && cbase + j < g.N; ++j) out[j] = hv[j];
+        }
+      }
+    }
+  }
+}
+
+// One TR x TR output tile (logical tile id `logical`) of one product; lds:
+// LDS_DL (TR = 128) or LDS_BIG (TR = 256) bytes.  256 x 256 tiles serve the
+// forward and input-gradient products only.
+template <bool A_KC, bool B_KC, int EPI, int TR>
 __device__ __forceinline__ void tile_dl16(const GemmArgs& g, const int logical, char* lds) {
   constexpr bool DW = EPI == EPI_DW_UPDATE;
+  constexpr int NB = Geo<TR>::NB, IPW = Geo<TR>::IPW, STAGE = Geo<TR>::STAGE;
+  static_assert(TR == 128 || !DW, "weight-gradient tiles are 128 x 128");
   const int tid = threadIdx.x;
   const Lanes q{tid >> 6, tid & 63, (tid >> 6) >> 1, (tid >> 6) & 1, tid & 31, (tid & 63) >> 5};
-  const int tm = (g.M + TB - 1) / TB, tn = (g.N + TB - 1) / TB;
+  const int tm = (g.M + TR - 1) / TR, tn = (g.N + TR - 1) / TR;
   const int worker = logical / (tm * tn), rem = logical % (tm * tn);
-  const int tile_n = rem / tm, m0 = (rem % tm) * TB, n0 = tile_n * TB;
+  const int tile_n = rem / tm, m0 = (rem % tm) * TR, n0 = tile_n * TR;
   char* const st0 = lds;
-  char* const st1 = lds + STAGE_B;
-  char* const st2 = lds + 2 * STAGE_B;
-  char* const st3 = lds + 3 * STAGE_B;
+  char* const st1 = lds + STAGE;
+  char* const st2 = lds + 2 * STAGE;
+  char* const st3 = lds + 3 * STAGE;
 
-  Loader<A_KC> la;
-  Loader<B_KC> lb;
+  Loader<A_KC, TR> la;
+  Loader<B_KC, TR> lb;
   la.init(g.a, g.g, g.zero, worker, m0, g.M, g.K, q.wave, q.lane);
   lb.init(g.b, g.g, g.zero, worker, n0, g.N, g.K, q.wave, q.lane);
 
-  float bsum[2] = {0.f, 0.f};
-  f32x16 acc[2][2];
+  float bsum[NB];
+  f32x16 acc[NB][NB];
 #pragma unroll
-  for (int bi = 0; bi < 2; ++bi)
+  for (int bi = 0; bi < NB; ++bi) {
+    bsum[bi] = 0.f;
 #pragma unroll
-    for (int bj = 0; bj < 2; ++bj)
+    for (int bj = 0; bj < NB; ++bj)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[bi][bj][r] = 0.f;
+  }
 
   const int nk = (g.K + BK - 1) / BK;
-  // steps 0..NS-1 in flight (4 load instructions per wave per step), then
-  // the fragments of step 0
+  // steps 0..NS-1 in flight (2*IPW load instructions per wave per step),
+  // then the fragments of step 0
   {
     char* const stg[NS] = {st0, st1, st2, st3};
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      const uint32_t wa = lds_off(stg[s]) + 2048 * q.wave;
-      fire(la.src(s * BK, 0), wa);
-      fire(la.src(s * BK, 1), wa + 1024);
-      fire(lb.src(s * BK, 0), wa + TILE_B);
-      fire(lb.src(s * BK, 1), wa + TILE_B + 1024);
+      const uint32_t wa = lds_off(stg[s]) + 1024 * IPW * q.wave;
+#pragma unroll
+      for (int u = 0; u < IPW; ++u) fire(la.src(s * BK, u), wa + 1024 * u);
+#pragma unroll
+      for (int u = 0; u < IPW; ++u) fire(lb.src(s * BK, u), wa + Geo<TR>::TILE + 1024 * u);
     }
   }
-  wait_vm<4 * (NS - 1)>();
+  wait_vm<2 * IPW * (NS - 1)>();
   barrier();
-  Frags f0, f1;
-  read_frags<A_KC, B_KC>(st0, q, f0);
+  Frags<TR> f0, f1;
+  read_frags<A_KC, B_KC, TR>(st0, q, f0);
 
   // step kt loads step kt + NS: from the precomputed full-step sources
   // while that step lies inside K, else through the bounds checks
-  auto step = [&](auto full, const Frags& cur, Frags& nxt, const char* rd, char* wr, int kt) {
+  auto step = [&](auto full, const Frags<TR>& cur, Frags<TR>& nxt, const char* rd, char* wr, int kt) {
     const int k0 = (kt + NS) * BK;
-    if constexpr (decltype(full)::value) {
-      const uint16_t* const src[4] = {la.src_full(k0, 0), la.src_full(k0, 1), lb.src_full(k0, 0),
-                                      lb.src_full(k0, 1)};
-      k_step<A_KC, B_KC, DW>(q, cur, nxt, rd, wr, src, acc, bsum);
-    } else {
-      const uint16_t* const src[4] = {la.src(k0, 0), la.src(k0, 1), lb.src(k0, 0), lb.src(k0, 1)};
-      k_step<A_KC, B_KC, DW>(q, cur, nxt, rd, wr, src, acc, bsum);
+    const uint16_t* src[2 * IPW];
+#pragma unroll
+    for (int u = 0; u < IPW; ++u) {
+      if constexpr (decltype(full)::value) {
+        src[u] = la.src_full(k0, u);
+        src[IPW + u] = lb.src_full(k0, u);
+      } else {
+        src[u] = la.src(k0, u);
+        src[IPW + u] = lb.src(k0, u);
+      }
     }
+    k_step<A_KC, B_KC, TR, DW>(q, cur, nxt, rd, wr, src, acc, bsum);
   };
   using Full = std::true_type;
   using Checked = std::false_type;
@@ -324,7 +462,9 @@ __device__ __forceinline__ void tile_dl16(const GemmArgs& g, const int logical, 
   wait_lgkm0();
   barrier();
 
-  if constexpr (!DW) {
+  if constexpr (TR == 256) {
+    out_epilogue_big<EPI>(g, worker, m0, n0, acc, reinterpret_cast<float*>(lds));
+  } else if constexpr (!DW) {
     out_epilogue_lds<EPI>(g, worker, m0, n0, acc, reinterpret_cast<float*>(lds));
   } else {
     const AdamCoef ac = g.adam.on ? adam_coef(g.g, g.adam) : AdamCoef{1.f, 1.f};
@@ -337,7 +477,7 @@ __device__ __forceinline__ void tile_dl16(const GemmArgs& g, const int logical, 
     // of dZ (waves wn = 0 and 1 hold the same sums)
     if (tile_n == 0 && q.wn == 0) {
 #pragma unroll
-      for (int b = 0; b < 2; ++b) {
+      for (int b = 0; b < NB; ++b) {
         const float tot = bsum[b] + __shfl_xor(bsum[b], 32);
         const int o = m0 + q.wm * 64 + 32 * b + q.li;
         if (q.lh == 0 && o < g.M) {
@@ -354,7 +494,14 @@ __device__ __forceinline__ void tile_dl16(const GemmArgs& g, const int logical, 
 template <bool A_KC, bool B_KC, int EPI>
 __global__ __launch_bounds__(NT) void gemm_bf16_dl_kernel(GemmArgs g) {
   __shared__ __attribute__((aligned(16))) char lds[LDS_DL];
-  tile_dl16<A_KC, B_KC, EPI>(g, xcd_remap(blockIdx.x, tiles16(g)), lds);
+  tile_dl16<A_KC, B_KC, EPI, 128>(g, xcd_remap(blockIdx.x, tiles16<128>(g)), lds);
+}
+
+// 256 x 256 tiles, one workgroup per CU (LDS)
+template <bool A_KC, bool B_KC, int EPI>
+__global__ __launch_bounds__(NT) void gemm_bf16_dl_big_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) char lds[LDS_BIG];
+  tile_dl16<A_KC, B_KC, EPI, 256>(g, xcd_remap(blockIdx.x, tiles16<256>(g)), lds);
 }
 
 // The backward products of one layer in one launch: input-gradient tiles
@@ -366,9 +513,9 @@ __global__ __launch_bounds__(NT) void gemm_bf16_dl_bwd_kernel(GemmArgs dx, GemmA
   __shared__ __attribute__((aligned(16))) char lds[LDS_DL];
   const int pid = blockIdx.x;
   if (pid < n1pad) {
-    if (pid < n1) tile_dl16<true, false, EPI_DX_MASK>(dx, xcd_remap(pid, n1), lds);
+    if (pid < n1) tile_dl16<true, false, EPI_DX_MASK, 128>(dx, xcd_remap(pid, n1), lds);
   } else {
-    tile_dl16<false, false, EPI_DW_UPDATE>(dw, xcd_remap(pid - n1pad, tiles16(dw)), lds);
+    tile_dl16<false, false, EPI_DW_UPDATE, 128>(dw, xcd_remap(pid - n1pad, tiles16<128>(dw)), lds);
   }
 }
 
@@ -398,8 +545,23 @@ bool gemm_bf16_dl_ok(int a_kc, int b_kc, const GemmArgs& g) {
   return false;
 }
 
+// 256 x 256 tiles for the forward product where they fill the chip (the
+// workgroups hold a whole 256-row mini-batch: each weight tile is read once)
+static bool use_big(int a_kc, int b_kc, const GemmArgs& g) {
+  return a_kc && b_kc && g.M >= 256 && g.N >= 256 && tiles16<256>(g) >= 256;
+}
+
 hipError_t launch_gemm_bf16_dl(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s) {
-  const dim3 grid(tiles16(g)), block(NT);
+  const dim3 block(NT);
+  if (use_big(a_kc, b_kc, g)) {
+    const dim3 grid(tiles16<256>(g));
+    if (g.epi == EPI_FWD_RELU)
+      hipLaunchKernelGGL((gemm_bf16_dl_big_kernel<true, true, EPI_FWD_RELU>), grid, block, 0, s, g);
+    else
+      hipLaunchKernelGGL((gemm_bf16_dl_big_kernel<true, true, EPI_FWD_LINEAR>), grid, block, 0, s, g);
+    return hipGetLastError();
+  }
+  const dim3 grid(tiles16<128>(g));
   if (a_kc && b_kc && g.epi == EPI_FWD_RELU)
     hipLaunchKernelGGL((gemm_bf16_dl_kernel<true, true, EPI_FWD_RELU>), grid, block, 0, s, g);
   else if (a_kc && b_kc && g.epi == EPI_FWD_LINEAR)
@@ -414,8 +576,9 @@ hipError_t launch_gemm_bf16_dl(int a_kc, int b_kc, const GemmArgs& g, hipStream_
 }
 
 hipError_t launch_gemm_bf16_dl_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s) {
-  const int n1 = tiles16(dx), n1pad = (n1 + kNumXcd - 1) / kNumXcd * kNumXcd;
-  hipLaunchKernelGGL(gemm_bf16_dl_bwd_kernel, dim3(n1pad + tiles16(dw)), dim3(NT), 0, s, dx, dw, n1, n1pad);
+  const int n1 = tiles16<128>(dx), n1pad = (n1 + kNumXcd - 1) / kNumXcd * kNumXcd;
+  hipLaunchKernelGGL(gemm_bf16_dl_bwd_kernel, dim3(n1pad + tiles16<128>(dw)), dim3(NT), 0, s, dx, dw, n1,
+                     n1pad);
   return hipGetLastError();
 }
 

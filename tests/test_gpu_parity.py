@@ -62,6 +62,14 @@ SMALL = [
     # weight gradient over gathered rows whose mini-batch wraps round the
     # shard's end (S = 216: steps at offsets 0, 100, 200)
     ("bf16_dl_gather", (136, 264, 200, 10), 3, 3, 100, 0.05, 2, 650, "sparse_teacher2", "permutation", "bf16"),
+    # 256 x 256 forward tiles (a whole 256-row mini-batch per workgroup,
+    # used from 256 tiles on): a hidden layer with a K tail, and the logits.
+    # (Sparse inputs: with dense Gaussian ones some of the 16M hidden
+    # pre-activations sit within rounding distance of zero, and the ReLU
+    # mask they flip moves a committed delta by 2 % of its largest entry
+    # between the oracle's own float32 and float64 products.)
+    ("bf16_big_tiles", (520, 4096, 10), 16, 2, 256, 0.05, 1, 8192, "sparse_teacher2", "permutation", "bf16"),
+    ("bf16_big_logits", (64, 264, 4096), 16, 2, 256, 0.05, 1, 8192, "gauss_linear", "permutation", "bf16"),
     # (Adam through the same kernels, at small widths: Adam's first step is
     # +-eta times the sign of the gradient, and on wider layers some
     # component's gradient cancels to the rounding level, where even the
