@@ -192,6 +192,74 @@ def copy_calibration(nbytes=1 << 30, reps=5):
     print(json.dumps({"copy_bytes": nbytes, "reps": reps}))
 
 
+# rocprofv3 kernel names -> the kernel classes the library times
+def traffic_class(name):
+    if "commit_kernel" in name:
+        return "commit"
+    if "head_dw_kernel" in name:
+        return "output_dw"
+    if "head_kernel" in name or "softmax_ce" in name:
+        return "output"
+    if "_bwd_kernel" in name:
+        return "bwd"
+    if "gemm_f32_dl_dw_kernel" in name or "<false, false, 3>" in name:
+        return "dw_first"
+    if "<true, true" in name:
+        return "fwd"
+    return None
+
+
+def summarize_traffic(d, workload):
+    """FETCH_SIZE / WRITE_SIZE counter passes (rocprofv3 --pmc, csv output,
+    under d/{bench,copy}_{FETCH_SIZE,WRITE_SIZE}/) -> HBM bytes per launch
+    of each kernel class, scaled by what the same counter reads for the
+    1 GiB copy of --copy-calibration; written to profiles/traffic.json with
+    the digest of the kernel sources, and printed as a text summary."""
+    import collections
+    import csv
+
+    def rows(sub, counter):
+        with open(os.path.join(d, sub, "run_counter_collection.csv")) as fh:
+            return [r for r in csv.DictReader(fh) if r["Counter_Name"] == counter]
+
+    def factor(counter):
+        vals = [float(r["Counter_Value"]) for r in rows(f"copy_{counter}", counter)
+                if "copy" in r["Kernel_Name"].lower() or "elementwise" in r["Kernel_Name"].lower()]
+        kib = max(v for v in vals if v > 0)
+        return (1 << 30) / (kib * 1024.0), kib
+
+    out = {"workload": workload, "kernel_source_sha256": kernel_source_digest(), "classes": {}}
+    lines = []
+    per = {}
+    for counter in ("FETCH_SIZE", "WRITE_SIZE"):
+        f, kib = factor(counter)
+        lines.append(f"copy calibration (1 GiB device copy): {counter} {kib:.0f} KiB -> factor {f:.4f}")
+        cls, kern = collections.defaultdict(list), collections.defaultdict(list)
+        for r in rows(f"bench_{counter}", counter):
+            v = float(r["Counter_Value"]) * 1024 * f
+            kern[r["Kernel_Name"][:90]].append(v)
+            c = traffic_class(r["Kernel_Name"])
+            if c:
+                cls[c].append(v)
+        per[counter] = (cls, kern)
+    fcls, fkern = per["FETCH_SIZE"]
+    wcls, wkern = per["WRITE_SIZE"]
+    for c in sorted(fcls):
+        f = sum(fcls[c]) / len(fcls[c])
+        w = sum(wcls.get(c, [0.0])) / max(1, len(wcls.get(c, [0.0])))
+        out["classes"][c] = {"hbm_bytes_per_launch": f + w, "fetch_bytes_per_launch": f,
+                             "write_bytes_per_launch": w, "launches_sampled": len(fcls[c])}
+        lines.append(f"class {c:9s}: fetch {f / 1e6:9.2f} MB + write {w / 1e6:9.2f} MB per launch "
+                     f"({len(fcls[c])} launches)")
+    for k in sorted(fkern):
+        f = sum(fkern[k]) / len(fkern[k])
+        w = sum(wkern.get(k, [0.0])) / max(1, len(wkern.get(k, [0.0])))
+        lines.append(f"  {k[:80]:80s} fetch {f / 1e6:9.2f} MB write {w / 1e6:9.2f} MB")
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(out, fh, indent=1)
+    print("\n".join(lines))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -211,9 +279,15 @@ def main():
                     help="round: the AGN round (default line, with the evaluation); eval: evaluation only")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration)")
+    ap.add_argument("--summarize-traffic", metavar="DIR",
+                    help="turn the FETCH_SIZE / WRITE_SIZE counter passes under DIR into "
+                         "profiles/traffic.json for --workload (no GPU needed)")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.summarize_traffic:
+        summarize_traffic(args.summarize_traffic, args.workload)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the multi-GPU "
