@@ -919,7 +919,9 @@ int agn_kernel_class_work(agn_ctx* c, int32_t cls, double* flops, double* bytes)
       }
       break;
     case AGN_K_COMMIT:
-      b = 8.0 * (double)(c->n + 1) * c->P;  // central + n deltas in, n pulls + central out
+      // central + n deltas in, n pulls + central out (+ the bf16 copies of
+      // the pulls, the operands of each worker's next round)
+      b = (8.0 * (double)(c->n + 1) + (c->dtype == AGN_BF16 ? 2.0 * c->n : 0.0)) * c->P;
       break;
     case AGN_K_EVAL: {  // the last evaluation: inputs and weights read, logits written
       const double N = (double)c->eval_N;
