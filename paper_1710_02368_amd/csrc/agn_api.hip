@@ -67,6 +67,7 @@ struct agn_ctx {
   int64_t graph_n = -1;
   int device = 0;
   int use_head = 0;  // fused output-layer kernels (few classes)
+  int head_dw_folded = 0;  // the last round folded the output layer's update into the first layer's launch
   int normalize = 1; // commit a / lambda (AGN) or a (DOWNPOUR with local exploration)
   int staleness_scaling = 0;           // scale each commit by 1 / (tau + 1)
   float* commit_scale = nullptr;       // device, n factors of the current round
@@ -217,6 +218,37 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     return bf ? launch_gemm_bf16(a_kc, b_kc, g, c->ls) : launch_gemm_f32(a_kc, b_kc, g, c->ls);
   };
 
+  // dW_l = dZ_{l+1}^T H_l fused with the update of W_l and b_l
+  auto dw_args = [&](int l) {
+    const int64_t dz_ld = c->lda[l + 1], dz_st = (int64_t)m * c->lda[l + 1];
+    GemmArgs w{};
+    w.M = c->dims[l + 1];
+    w.N = c->dims[l];
+    w.K = m;
+    w.batch = n;
+    w.a = Operand{c->dZ[l + 1], dz_ld, dz_st, 0, 1};
+    w.b = l == 0 ? xop : Operand{c->H[l], c->lda[l], (int64_t)m * c->lda[l], 0, 1};
+    w.g = gath;
+    w.epi = EPI_DW_UPDATE;
+    w.w_src = src + c->woff[l];
+    w.w_dst = dst + c->woff[l];
+    w.w_snap = c->snap + c->woff[l];
+    w.b_src = src + c->boff[l];
+    w.b_dst = dst + c->boff[l];
+    w.b_snap = c->snap + c->boff[l];
+    w.w_dst16 = (bf && !last) ? dst16 + c->woff[l] : nullptr;
+    w.ldw = c->ldw[l];
+    w.pstride = ps;
+    w.eta = c->eta;
+    w.lam = c->normalize ? (float)c->lam : 1.f;  // divisor of the committed delta
+    w.last = last;
+    w.zero = c->zero;
+    w.adam = adam_args(c, l);
+    return w;
+  };
+  HeadDwArgs hdw{};
+  bool fold_head_dw = false;
+
   // forward: hidden layers with bias + ReLU, then the logits (unless the
   // fused output-layer kernel computes them)
   const int fwd_layers = c->use_head ? L - 1 : L;
@@ -268,7 +300,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     h.lam = c->lam;
     h.step = step;
     HIP_CHECK(c, timed(c, AGN_K_OUTPUT, [&] { return launch_head(h, c->ls); }));
-    HeadDwArgs w{};
+    HeadDwArgs& w = hdw;
     w.h = hin;
     w.ldh = ldh;
     w.hstride = hst;
@@ -293,7 +325,11 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     w.lam = c->normalize ? (float)c->lam : 1.f;  // divisor of the committed delta
     w.last = last;
     w.adam = adam_args(c, L - 1);
-    HIP_CHECK(c, timed(c, AGN_K_OUTPUT_DW, [&] { return launch_head_dw(w, c->ls); }));
+    // with a first-layer weight gradient on the direct-load path, the
+    // output layer's update rides in that launch (it touches nothing the
+    // layers in between read or write)
+    fold_head_dw = !bf && L >= 2 && gemm_f32_dl_dw_head_ok(dw_args(0), w);
+    if (!fold_head_dw) HIP_CHECK(c, timed(c, AGN_K_OUTPUT_DW, [&] { return launch_head_dw(w, c->ls); }));
   } else {
     // softmax cross-entropy: per-row loss and the output gradient dZ_L
     SoftmaxArgs s{};
@@ -320,29 +356,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
   // weight-gradient product fused with the update
   for (int l = c->use_head ? L - 2 : L - 1; l >= 0; --l) {
     const int64_t dz_ld = c->lda[l + 1], dz_st = (int64_t)m * c->lda[l + 1];
-    GemmArgs w{};  // dW_l = dZ_{l+1}^T H_l fused with the update of W_l and b_l
-    w.M = c->dims[l + 1];
-    w.N = c->dims[l];
-    w.K = m;
-    w.batch = n;
-    w.a = Operand{c->dZ[l + 1], dz_ld, dz_st, 0, 1};
-    w.b = l == 0 ? xop : Operand{c->H[l], c->lda[l], (int64_t)m * c->lda[l], 0, 1};
-    w.g = gath;
-    w.epi = EPI_DW_UPDATE;
-    w.w_src = src + c->woff[l];
-    w.w_dst = dst + c->woff[l];
-    w.w_snap = c->snap + c->woff[l];
-    w.b_src = src + c->boff[l];
-    w.b_dst = dst + c->boff[l];
-    w.b_snap = c->snap + c->boff[l];
-    w.w_dst16 = (bf && !last) ? dst16 + c->woff[l] : nullptr;
-    w.ldw = c->ldw[l];
-    w.pstride = ps;
-    w.eta = c->eta;
-    w.lam = c->normalize ? (float)c->lam : 1.f;  // divisor of the committed delta
-    w.last = last;
-    w.zero = c->zero;
-    w.adam = adam_args(c, l);
+    const GemmArgs w = dw_args(l);
     if (l >= 1) {  // dZ_l = (dZ_{l+1} W_l) * [H_l > 0]
       GemmArgs x{};
       x.M = m;
@@ -363,10 +377,13 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
       HIP_CHECK(c, timed(c, AGN_K_BWD, [&] {
         return bf ? launch_gemm_bf16_bwd(x, w, c->ls) : launch_gemm_f32_bwd(x, w, c->ls);
       }));
+    } else if (fold_head_dw) {
+      HIP_CHECK(c, timed(c, AGN_K_DW_FIRST, [&] { return launch_gemm_f32_dl_dw_head(w, hdw, c->ls); }));
     } else {
       HIP_CHECK(c, timed(c, AGN_K_DW_FIRST, [&] { return gemm(0, 0, w); }));
     }
   }
+  c->head_dw_folded = fold_head_dw;
   (void)dst16;
   return AGN_OK;
 }
@@ -901,7 +918,7 @@ int agn_kernel_class_work(agn_ctx* c, int32_t cls, double* flops, double* bytes)
       }
       break;
     case AGN_K_OUTPUT_DW:
-      if (c->use_head) {
+      if (c->use_head && !c->head_dw_folded) {
         f = 2.0 * mac(L - 1) * rows;
         b = upd * (mac(L - 1) + C);
       }
@@ -916,6 +933,10 @@ int agn_kernel_class_work(agn_ctx* c, int32_t cls, double* flops, double* bytes)
       if (!(c->use_head && L == 1)) {
         f = 2.0 * mac(0) * rows;
         b = upd * (mac(0) + c->dims[1]);
+      }
+      if (c->use_head && c->head_dw_folded) {  // (the output layer's update rides in this launch)
+        f += 2.0 * mac(L - 1) * rows;
+        b += upd * (mac(L - 1) + C);
       }
       break;
     case AGN_K_COMMIT:

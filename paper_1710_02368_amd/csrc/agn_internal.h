@@ -86,6 +86,11 @@ hipError_t launch_gemm_bf16_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStrea
 bool gemm_f32_dl_ok(int a_kc, int b_kc, const GemmArgs& g);
 hipError_t launch_gemm_f32_dl(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s);
 hipError_t launch_gemm_f32_dl_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s);
+struct HeadDwArgs;
+// the first layer's direct-load weight gradient with the output layer's
+// weight gradient + update (C <= 10) folded into the same launch
+bool gemm_f32_dl_dw_head_ok(const GemmArgs& g, const HeadDwArgs& h);
+hipError_t launch_gemm_f32_dl_dw_head(const GemmArgs& g, const HeadDwArgs& h, hipStream_t s);
 // direct global->LDS variants of the bf16 products (used when the operands
 // and outputs qualify, see gemm_bf16_dl_ok)
 bool gemm_bf16_dl_ok(int a_kc, int b_kc, const GemmArgs& g);

@@ -46,6 +46,7 @@
 #include <type_traits>
 
 #include "direct_load.h"
+#include "head_dw_unit.h"
 
 namespace agn {
 namespace {
@@ -687,10 +688,35 @@ __global__ __launch_bounds__(NT) void gemm_f32_dl_kernel(GemmArgs g) {
   tile_dl<A_KC, B_KC, EPI>(g, xcd_remap(blockIdx.x, tiles_dl(g)), st0, st1, st2, st3);
 }
 
-template <bool LAST>
-__global__ __launch_bounds__(NT) void gemm_f32_dl_dw_kernel(GemmArgs g) {
+// Rank of workgroup `wg` of `nwg` by its number of weight-gradient tiles
+// (tiles_of_wg: the high slots of each XCD hold one tile fewer): rank 0 is
+// the last slot of XCD 0, then the last slot of XCD 1, ...  A bijection on
+// [0, nwg).
+__device__ __forceinline__ int fewest_tiles_rank(int wg, int nwg) {
+  const int per = nwg / kNumXcd;
+  return (per - 1 - wg / kNumXcd) * kNumXcd + wg % kNumXcd;
+}
+
+// The first layer's weight gradient; with HCM > 0 (the class bound of the
+// fused output layer) also the output layer's weight-gradient units, which
+// neither read nor write what the first layer's tiles do: unit u goes to
+// the workgroup of rank u mod nwg, before its tiles (the stage buffers are
+// free then, and these workgroups hold a tile fewer).
+template <bool LAST, int HCM>
+__global__ __launch_bounds__(NT) void gemm_f32_dl_dw_kernel(GemmArgs g, HeadDwArgs h) {
   DL_STAGES
   DL_EPI(LAST)
+  if constexpr (HCM > 0) {
+    static_assert(hdw_smem_floats<HCM>() <= STAGE_F, "an output-layer unit fits one stage buffer");
+    const int units = hdw_units(h);
+    bool ran = false;
+    for (int u = fewest_tiles_rank(blockIdx.x, gridDim.x); u < units; u += gridDim.x) {
+      if (ran) __syncthreads();  // the previous unit's LDS reads are done
+      head_dw_unit<HCM>(h, u, st0);
+      ran = true;
+    }
+    if (ran) __syncthreads();    // before the tiles' loads land in the stages
+  }
   dw_tiles<LAST>(g, tiles_of_wg(tiles_dl(g), blockIdx.x, gridDim.x), st0, st1, st2, st3, epi, epi2);
 }
 
@@ -775,13 +801,27 @@ hipError_t launch_gemm_f32_dl(int a_kc, int b_kc, const GemmArgs& g, hipStream_t
   else if (a_kc && !b_kc && g.epi == EPI_DX_MASK)
     hipLaunchKernelGGL((gemm_f32_dl_kernel<true, false, EPI_DX_MASK>), grid, block, 0, s, g);
   else if (!a_kc && !b_kc && g.epi == EPI_DW_UPDATE) {
+    const HeadDwArgs none{};
     if (g.last)
-      hipLaunchKernelGGL(gemm_f32_dl_dw_kernel<true>, dim3(dw_grid(g)), block, 0, s, g);
+      hipLaunchKernelGGL((gemm_f32_dl_dw_kernel<true, 0>), dim3(dw_grid(g)), block, 0, s, g, none);
     else
-      hipLaunchKernelGGL(gemm_f32_dl_dw_kernel<false>, dim3(dw_grid(g)), block, 0, s, g);
+      hipLaunchKernelGGL((gemm_f32_dl_dw_kernel<false, 0>), dim3(dw_grid(g)), block, 0, s, g, none);
   } else {
     return hipErrorInvalidValue;
   }
+  return hipGetLastError();
+}
+
+bool gemm_f32_dl_dw_head_ok(const GemmArgs& g, const HeadDwArgs& h) {
+  return dw_ok(g) && h.C >= 1 && h.C <= 10 && h.n >= 1 && h.d >= 1;
+}
+
+hipError_t launch_gemm_f32_dl_dw_head(const GemmArgs& g, const HeadDwArgs& h, hipStream_t s) {
+  if (!gemm_f32_dl_dw_head_ok(g, h)) return hipErrorInvalidValue;
+  if (g.last)
+    hipLaunchKernelGGL((gemm_f32_dl_dw_kernel<true, 10>), dim3(dw_grid(g)), dim3(NT), 0, s, g, h);
+  else
+    hipLaunchKernelGGL((gemm_f32_dl_dw_kernel<false, 10>), dim3(dw_grid(g)), dim3(NT), 0, s, g, h);
   return hipGetLastError();
 }
 

@@ -362,6 +362,45 @@ def test_errors_leave_state_unchanged():
     g.close()
 
 
+@pytest.mark.parametrize("dims,folded", [((100, 200, 136, 10), True), ((100, 200, 136, 12), False),
+                                         ((100, 200, 10), True)])
+def test_output_layer_update_rides_in_first_layer_launch(dims, folded):
+    """With at most 10 classes and the first layer's weight gradient on the
+    direct-load path, the output layer's weight update runs inside that
+    launch (no launch of its own); the class accounting follows, and the
+    round still matches the oracle."""
+    agn = _agn()
+    wl = W.small_workload("fold", dims, 3, 2, 100, 0.05, 1, 650, data="sparse_teacher2", order="permutation")
+    X, y = W.make_data(wl)
+    xd, yd = to_device(X, y)
+    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed)
+    o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed)
+    for c in agn.KERNEL_CLASSES.values():
+        agn.agn_set_kernel_timing(g.ctx, c, True)
+    order = W.commit_orders(wl)[0]
+    g.round(xd, yd, order)
+    o.round(X, y, order)
+    _, n_out_dw = agn.agn_kernel_timing(g.ctx, agn.KERNEL_CLASSES["output_dw"])
+    _, n_first = agn.agn_kernel_timing(g.ctx, agn.KERNEL_CLASSES["dw_first"])
+    f_out_dw, _ = agn.agn_kernel_class_work(g.ctx, agn.KERNEL_CLASSES["output_dw"])
+    f_first, _ = agn.agn_kernel_class_work(g.ctx, agn.KERNEL_CLASSES["dw_first"])
+    mac = lambda l: dims[l] * dims[l + 1]
+    rows = wl.n * wl.lam * wl.m
+    assert n_first == wl.lam
+    if folded:
+        assert n_out_dw == 0 and f_out_dw == 0
+        assert f_first == 2.0 * (mac(0) + mac(len(dims) - 2)) * rows
+    else:
+        assert n_out_dw == wl.lam and f_out_dw == 2.0 * mac(len(dims) - 2) * rows
+        assert f_first == 2.0 * mac(0) * rows
+    err, where = rel_err(g.central().cpu().numpy(), o.central_flat(), wl.dims)
+    assert err <= FP32_TOL_1, (where, err)
+    for k in range(wl.n):
+        e, w = rel_err(g.worker_params(k).cpu().numpy(), o.worker_flat(k), wl.dims)
+        assert e <= FP32_TOL_1, (k, w, e)
+    g.close()
+
+
 def test_graph_replay_and_eager_launches_agree():
     """Rounds run eagerly (kernel timing on) and rounds replayed from the
     captured graph launch the same kernels: results are bitwise equal; the
