@@ -67,7 +67,7 @@ struct agn_ctx {
   int64_t graph_n = -1;
   int device = 0;
   int use_head = 0;  // fused output-layer kernels (few classes)
-  int head_dw_folded = 0;  // the last round folded the output layer's update into the first layer's launch
+  int head_dw_folded = 0;  // local steps of the last round that folded the output layer's update into the first layer's launch
   int normalize = 1; // commit a / lambda (AGN) or a (DOWNPOUR with local exploration)
   int staleness_scaling = 0;           // scale each commit by 1 / (tau + 1)
   float* commit_scale = nullptr;       // device, n factors of the current round
@@ -328,7 +328,9 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     // with a first-layer weight gradient on the direct-load path, the
     // output layer's update rides in that launch (it touches nothing the
     // layers in between read or write)
-    fold_head_dw = !bf && L >= 2 && gemm_f32_dl_dw_head_ok(dw_args(0), w);
+    // (not on a round's last step: its first-layer launch runs one
+    // workgroup per CU, and the folded units would lengthen it)
+    fold_head_dw = !bf && !last && L >= 2 && gemm_f32_dl_dw_head_ok(dw_args(0), w);
     if (!fold_head_dw) HIP_CHECK(c, timed(c, AGN_K_OUTPUT_DW, [&] { return launch_head_dw(w, c->ls); }));
   } else {
     // softmax cross-entropy: per-row loss and the output gradient dZ_L
@@ -383,7 +385,8 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
       HIP_CHECK(c, timed(c, AGN_K_DW_FIRST, [&] { return gemm(0, 0, w); }));
     }
   }
-  c->head_dw_folded = fold_head_dw;
+  if (step == 0) c->head_dw_folded = 0;
+  c->head_dw_folded += fold_head_dw ? 1 : 0;
   (void)dst16;
   return AGN_OK;
 }
@@ -918,9 +921,10 @@ int agn_kernel_class_work(agn_ctx* c, int32_t cls, double* flops, double* bytes)
       }
       break;
     case AGN_K_OUTPUT_DW:
-      if (c->use_head && !c->head_dw_folded) {
-        f = 2.0 * mac(L - 1) * rows;
-        b = upd * (mac(L - 1) + C);
+      if (c->use_head) {  // (steps that folded it into the first layer's launch count there)
+        const double own = 1.0 - (double)c->head_dw_folded / c->lam;
+        f = 2.0 * mac(L - 1) * rows * own;
+        b = upd * (mac(L - 1) + C) * own;
       }
       break;
     case AGN_K_BWD:  // hidden layers not done in the output kernels
@@ -934,9 +938,10 @@ int agn_kernel_class_work(agn_ctx* c, int32_t cls, double* flops, double* bytes)
         f = 2.0 * mac(0) * rows;
         b = upd * (mac(0) + c->dims[1]);
       }
-      if (c->use_head && c->head_dw_folded) {  // (the output layer's update rides in this launch)
-        f += 2.0 * mac(L - 1) * rows;
-        b += upd * (mac(L - 1) + C);
+      if (c->use_head && c->head_dw_folded) {  // steps where the output layer's update rides in this launch
+        const double folded = (double)c->head_dw_folded / c->lam;
+        f += 2.0 * mac(L - 1) * rows * folded;
+        b += upd * (mac(L - 1) + C) * folded;
       }
       break;
     case AGN_K_COMMIT:
