@@ -96,6 +96,10 @@ struct agn_ctx {
 
 static std::string g_create_err;
 
+namespace agn {
+thread_local LaunchEvents g_launch_events{nullptr, nullptr};
+}
+
 namespace {
 
 inline int64_t round_up(int64_t v, int64_t a) { return (v + a - 1) / a * a; }
@@ -163,13 +167,15 @@ hipError_t timed(agn_ctx* c, int cls, F&& launch) {
       t.ev.push_back(e);
     }
   }
-  hipError_t r = hipEventRecord(t.ev[2 * t.used], c->stream);
+  // the class's one kernel records the events at its own start and end
+  g_launch_events = LaunchEvents{t.ev[2 * t.used], t.ev[2 * t.used + 1]};
+  hipError_t r = launch();
+  const bool taken = g_launch_events.start == nullptr;
+  g_launch_events = LaunchEvents{nullptr, nullptr};
   if (r != hipSuccess) return r;
-  r = launch();
-  if (r != hipSuccess) return r;
-  r = hipEventRecord(t.ev[2 * t.used + 1], c->stream);
+  if (!taken) return hipErrorInvalidValue;  // (every timed class launches a kernel)
   ++t.used;
-  return r;
+  return hipSuccess;
 }
 
 int check_ctx(agn_ctx* c) {

@@ -1,10 +1,31 @@
 // Internal declarations shared by the host code and the kernels of libagn.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace agn {
+
+// Kernel timing: while set, the next kernel launched on this thread records
+// these two events at its own start and end (hipExtLaunchKernel), so that a
+// timed launch measures the kernel and not the gaps around it.  Set by the
+// timing bracket of the host API, taken (and cleared) by AGN_LAUNCH.
+struct LaunchEvents {
+  hipEvent_t start, stop;
+};
+extern thread_local LaunchEvents g_launch_events;
+
+#define AGN_LAUNCH(kernel, grid, block, shmem, stream, ...)                                              \
+  do {                                                                                                  \
+    if (::agn::g_launch_events.start) {                                                                 \
+      const ::agn::LaunchEvents ev_ = ::agn::g_launch_events;                                           \
+      ::agn::g_launch_events = ::agn::LaunchEvents{nullptr, nullptr};                                   \
+      hipExtLaunchKernelGGL(kernel, grid, block, shmem, stream, ev_.start, ev_.stop, 0, __VA_ARGS__);  \
+    } else {                                                                                            \
+      hipLaunchKernelGGL(kernel, grid, block, shmem, stream, __VA_ARGS__);                              \
+    }                                                                                                   \
+  } while (0)
 
 // An operand of a batched product, as the matrix is stored in memory.
 struct Operand {

@@ -274,34 +274,34 @@ inline unsigned blocks_for(int64_t n, int per) { return (unsigned)((n + per - 1)
 
 hipError_t launch_softmax_ce(const SoftmaxArgs& a, hipStream_t s) {
   const int64_t rows = (int64_t)a.n * a.m;
-  hipLaunchKernelGGL(softmax_ce_kernel, dim3(blocks_for(rows, 4)), dim3(256), 0, s, a);
+  AGN_LAUNCH(softmax_ce_kernel, dim3(blocks_for(rows, 4)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_commit(const CommitArgs& a, hipStream_t s) {
   const int64_t n4 = a.count / 4;
   if (a.scale)
-    hipLaunchKernelGGL(commit_kernel<true>, dim3(blocks_for(n4 > 0 ? n4 : 1, 256)), dim3(256), 0, s, a);
+    AGN_LAUNCH(commit_kernel<true>, dim3(blocks_for(n4 > 0 ? n4 : 1, 256)), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(commit_kernel<false>, dim3(blocks_for(n4 > 0 ? n4 : 1, 256)), dim3(256), 0, s, a);
+    AGN_LAUNCH(commit_kernel<false>, dim3(blocks_for(n4 > 0 ? n4 : 1, 256)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_pack(const PackArgs& pa, const float* padded, float* packed, hipStream_t s) {
-  hipLaunchKernelGGL(pack_kernel, dim3(blocks_for(pa.P, 256)), dim3(256), 0, s, pa, padded, packed);
+  AGN_LAUNCH(pack_kernel, dim3(blocks_for(pa.P, 256)), dim3(256), 0, s, pa, padded, packed);
   return hipGetLastError();
 }
 
 hipError_t launch_unpack(const PackArgs& pa, const float* packed, float* padded, uint16_t* padded16,
                          int32_t copies, int64_t pstride, hipStream_t s) {
-  hipLaunchKernelGGL(unpack_kernel, dim3(blocks_for(pa.P, 256)), dim3(256), 0, s, pa, packed, padded,
+  AGN_LAUNCH(unpack_kernel, dim3(blocks_for(pa.P, 256)), dim3(256), 0, s, pa, packed, padded,
                      padded16, copies, pstride);
   return hipGetLastError();
 }
 
 hipError_t launch_loss_reduce(const float* loss, int32_t n, int64_t per_worker, float* out,
                               hipStream_t s) {
-  hipLaunchKernelGGL(loss_reduce_kernel, dim3(n), dim3(256), 0, s, loss, per_worker, out);
+  AGN_LAUNCH(loss_reduce_kernel, dim3(n), dim3(256), 0, s, loss, per_worker, out);
   return hipGetLastError();
 }
 
@@ -312,14 +312,14 @@ hipError_t launch_set_order(const int32_t* host_order, const float* host_scale, 
     o.v[j] = j < n ? host_order[j] : 0;
     o.sc[j] = (j < n && host_scale) ? host_scale[j] : 1.f;
   }
-  hipLaunchKernelGGL(set_order_kernel, dim3(1), dim3(256), 0, s, o, n, dev_order,
+  AGN_LAUNCH(set_order_kernel, dim3(1), dim3(256), 0, s, o, n, dev_order,
                      host_scale ? dev_scale : nullptr);
   return hipGetLastError();
 }
 
 hipError_t launch_batch_indices(int32_t worker, int64_t t, int32_t mb, int64_t S, int64_t* out,
                                 hipStream_t s) {
-  hipLaunchKernelGGL(batch_indices_kernel, dim3(blocks_for(mb, 256)), dim3(256), 0, s, worker, t, mb,
+  AGN_LAUNCH(batch_indices_kernel, dim3(blocks_for(mb, 256)), dim3(256), 0, s, worker, t, mb,
                      S, out);
   return hipGetLastError();
 }
@@ -327,18 +327,18 @@ hipError_t launch_batch_indices(int32_t worker, int64_t t, int32_t mb, int64_t S
 int64_t eval_blocks(int64_t rows) { return (rows + EVAL_ROWS_PER_BLOCK - 1) / EVAL_ROWS_PER_BLOCK; }
 
 hipError_t launch_eval_rows(const EvalArgs& a, hipStream_t s) {
-  hipLaunchKernelGGL(eval_rows_kernel, dim3((unsigned)eval_blocks(a.rows)), dim3(256), 0, s, a);
+  AGN_LAUNCH(eval_rows_kernel, dim3((unsigned)eval_blocks(a.rows)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_eval_reduce(const double* part, int64_t blocks, double* acc, int32_t first,
                               hipStream_t s) {
-  hipLaunchKernelGGL(eval_reduce_kernel, dim3(1), dim3(256), 0, s, part, blocks, acc, first);
+  AGN_LAUNCH(eval_reduce_kernel, dim3(1), dim3(256), 0, s, part, blocks, acc, first);
   return hipGetLastError();
 }
 
 hipError_t launch_copy_bf16(const float* src, uint16_t* dst, int64_t count, hipStream_t s) {
-  hipLaunchKernelGGL(copy_bf16_kernel, dim3(blocks_for(count, 256)), dim3(256), 0, s, src, dst, count);
+  AGN_LAUNCH(copy_bf16_kernel, dim3(blocks_for(count, 256)), dim3(256), 0, s, src, dst, count);
   return hipGetLastError();
 }
 

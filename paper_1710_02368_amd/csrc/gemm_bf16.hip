@@ -296,7 +296,7 @@ __global__ __launch_bounds__(NT) void gemm_bf16_bwd_kernel(GemmArgs dx, GemmArgs
 
 template <bool A_KC, bool B_KC, int EPI>
 hipError_t go(const GemmArgs& g, hipStream_t s) {
-  hipLaunchKernelGGL((gemm_bf16_kernel<A_KC, B_KC, EPI>), dim3(tiles_of(g)), dim3(NT), 0, s, g);
+  AGN_LAUNCH((gemm_bf16_kernel<A_KC, B_KC, EPI>), dim3(tiles_of(g)), dim3(NT), 0, s, g);
   return hipGetLastError();
 }
 
@@ -306,7 +306,7 @@ hipError_t launch_gemm_bf16_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStrea
   if (dx.epi != EPI_DX_MASK || dw.epi != EPI_DW_UPDATE) return hipErrorInvalidValue;
   if (gemm_bf16_dl_ok(1, 0, dx) && gemm_bf16_dl_ok(0, 0, dw)) return launch_gemm_bf16_dl_bwd(dx, dw, s);
   const int n1 = tiles_of(dx), n1pad = (n1 + kNumXcd - 1) / kNumXcd * kNumXcd;
-  hipLaunchKernelGGL(gemm_bf16_bwd_kernel, dim3(n1pad + tiles_of(dw)), dim3(NT), 0, s, dx, dw, n1, n1pad);
+  AGN_LAUNCH(gemm_bf16_bwd_kernel, dim3(n1pad + tiles_of(dw)), dim3(NT), 0, s, dx, dw, n1, n1pad);
   return hipGetLastError();
 }
 

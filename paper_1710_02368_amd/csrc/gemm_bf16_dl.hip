@@ -556,20 +556,20 @@ hipError_t launch_gemm_bf16_dl(int a_kc, int b_kc, const GemmArgs& g, hipStream_
   if (use_big(a_kc, b_kc, g)) {
     const dim3 grid(tiles16<256>(g));
     if (g.epi == EPI_FWD_RELU)
-      hipLaunchKernelGGL((gemm_bf16_dl_big_kernel<true, true, EPI_FWD_RELU>), grid, block, 0, s, g);
+      AGN_LAUNCH((gemm_bf16_dl_big_kernel<true, true, EPI_FWD_RELU>), grid, block, 0, s, g);
     else
-      hipLaunchKernelGGL((gemm_bf16_dl_big_kernel<true, true, EPI_FWD_LINEAR>), grid, block, 0, s, g);
+      AGN_LAUNCH((gemm_bf16_dl_big_kernel<true, true, EPI_FWD_LINEAR>), grid, block, 0, s, g);
     return hipGetLastError();
   }
   const dim3 grid(tiles16<128>(g));
   if (a_kc && b_kc && g.epi == EPI_FWD_RELU)
-    hipLaunchKernelGGL((gemm_bf16_dl_kernel<true, true, EPI_FWD_RELU>), grid, block, 0, s, g);
+    AGN_LAUNCH((gemm_bf16_dl_kernel<true, true, EPI_FWD_RELU>), grid, block, 0, s, g);
   else if (a_kc && b_kc && g.epi == EPI_FWD_LINEAR)
-    hipLaunchKernelGGL((gemm_bf16_dl_kernel<true, true, EPI_FWD_LINEAR>), grid, block, 0, s, g);
+    AGN_LAUNCH((gemm_bf16_dl_kernel<true, true, EPI_FWD_LINEAR>), grid, block, 0, s, g);
   else if (a_kc && !b_kc && g.epi == EPI_DX_MASK)
-    hipLaunchKernelGGL((gemm_bf16_dl_kernel<true, false, EPI_DX_MASK>), grid, block, 0, s, g);
+    AGN_LAUNCH((gemm_bf16_dl_kernel<true, false, EPI_DX_MASK>), grid, block, 0, s, g);
   else if (!a_kc && !b_kc && g.epi == EPI_DW_UPDATE)
-    hipLaunchKernelGGL((gemm_bf16_dl_kernel<false, false, EPI_DW_UPDATE>), grid, block, 0, s, g);
+    AGN_LAUNCH((gemm_bf16_dl_kernel<false, false, EPI_DW_UPDATE>), grid, block, 0, s, g);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
@@ -577,7 +577,7 @@ hipError_t launch_gemm_bf16_dl(int a_kc, int b_kc, const GemmArgs& g, hipStream_
 
 hipError_t launch_gemm_bf16_dl_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s) {
   const int n1 = tiles16<128>(dx), n1pad = (n1 + kNumXcd - 1) / kNumXcd * kNumXcd;
-  hipLaunchKernelGGL(gemm_bf16_dl_bwd_kernel, dim3(n1pad + tiles16<128>(dw)), dim3(NT), 0, s, dx, dw, n1,
+  AGN_LAUNCH(gemm_bf16_dl_bwd_kernel, dim3(n1pad + tiles16<128>(dw)), dim3(NT), 0, s, dx, dw, n1,
                      n1pad);
   return hipGetLastError();
 }

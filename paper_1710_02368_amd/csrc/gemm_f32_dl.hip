@@ -795,17 +795,17 @@ bool gemm_f32_dl_ok(int a_kc, int b_kc, const GemmArgs& g) {
 hipError_t launch_gemm_f32_dl(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s) {
   const dim3 grid(tiles_dl(g)), block(NT);
   if (a_kc && b_kc && g.epi == EPI_FWD_RELU)
-    hipLaunchKernelGGL((gemm_f32_dl_kernel<true, true, EPI_FWD_RELU>), grid, block, 0, s, g);
+    AGN_LAUNCH((gemm_f32_dl_kernel<true, true, EPI_FWD_RELU>), grid, block, 0, s, g);
   else if (a_kc && b_kc && g.epi == EPI_FWD_LINEAR)
-    hipLaunchKernelGGL((gemm_f32_dl_kernel<true, true, EPI_FWD_LINEAR>), grid, block, 0, s, g);
+    AGN_LAUNCH((gemm_f32_dl_kernel<true, true, EPI_FWD_LINEAR>), grid, block, 0, s, g);
   else if (a_kc && !b_kc && g.epi == EPI_DX_MASK)
-    hipLaunchKernelGGL((gemm_f32_dl_kernel<true, false, EPI_DX_MASK>), grid, block, 0, s, g);
+    AGN_LAUNCH((gemm_f32_dl_kernel<true, false, EPI_DX_MASK>), grid, block, 0, s, g);
   else if (!a_kc && !b_kc && g.epi == EPI_DW_UPDATE) {
     const HeadDwArgs none{};
     if (g.last)
-      hipLaunchKernelGGL((gemm_f32_dl_dw_kernel<true, 0>), dim3(dw_grid(g)), block, 0, s, g, none);
+      AGN_LAUNCH((gemm_f32_dl_dw_kernel<true, 0>), dim3(dw_grid(g)), block, 0, s, g, none);
     else
-      hipLaunchKernelGGL((gemm_f32_dl_dw_kernel<false, 0>), dim3(dw_grid(g)), block, 0, s, g, none);
+      AGN_LAUNCH((gemm_f32_dl_dw_kernel<false, 0>), dim3(dw_grid(g)), block, 0, s, g, none);
   } else {
     return hipErrorInvalidValue;
   }
@@ -819,9 +819,9 @@ bool gemm_f32_dl_dw_head_ok(const GemmArgs& g, const HeadDwArgs& h) {
 hipError_t launch_gemm_f32_dl_dw_head(const GemmArgs& g, const HeadDwArgs& h, hipStream_t s) {
   if (!gemm_f32_dl_dw_head_ok(g, h)) return hipErrorInvalidValue;
   if (g.last)
-    hipLaunchKernelGGL((gemm_f32_dl_dw_kernel<true, 10>), dim3(dw_grid(g)), dim3(NT), 0, s, g, h);
+    AGN_LAUNCH((gemm_f32_dl_dw_kernel<true, 10>), dim3(dw_grid(g)), dim3(NT), 0, s, g, h);
   else
-    hipLaunchKernelGGL((gemm_f32_dl_dw_kernel<false, 10>), dim3(dw_grid(g)), dim3(NT), 0, s, g, h);
+    AGN_LAUNCH((gemm_f32_dl_dw_kernel<false, 10>), dim3(dw_grid(g)), dim3(NT), 0, s, g, h);
   return hipGetLastError();
 }
 
@@ -849,9 +849,9 @@ hipError_t launch_gemm_f32_dl_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStr
   const int cb = (q - ca * a + b - 1) / b;
   const dim3 grid(n1pad + n2), block(NT);
   if (dw.last)
-    hipLaunchKernelGGL(gemm_f32_dl_bwd_kernel<true>, grid, block, 0, s, dx, dw, n1, n1pad, ca, cb);
+    AGN_LAUNCH(gemm_f32_dl_bwd_kernel<true>, grid, block, 0, s, dx, dw, n1, n1pad, ca, cb);
   else
-    hipLaunchKernelGGL(gemm_f32_dl_bwd_kernel<false>, grid, block, 0, s, dx, dw, n1, n1pad, ca, cb);
+    AGN_LAUNCH(gemm_f32_dl_bwd_kernel<false>, grid, block, 0, s, dx, dw, n1, n1pad, ca, cb);
   return hipGetLastError();
 }
 

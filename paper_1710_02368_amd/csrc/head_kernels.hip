@@ -265,7 +265,7 @@ static hipError_t head_go(const HeadArgs& a, hipStream_t s, bool prepare) {
                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   }
   const int blocks = a.n * ((a.m + head_rows(EVAL) - 1) / head_rows(EVAL));
-  hipLaunchKernelGGL((head_kernel<CM, QM, EVAL>), dim3(blocks), dim3(256), lds, s, a);
+  AGN_LAUNCH((head_kernel<CM, QM, EVAL>), dim3(blocks), dim3(256), lds, s, a);
   return hipGetLastError();
 }
 
@@ -310,9 +310,9 @@ hipError_t launch_head_eval(const HeadArgs& a, hipStream_t s) { return head_disp
 hipError_t launch_head_dw(const HeadDwArgs& a, hipStream_t s) {
   const int blocks = hdw_units(a);
   switch (head_cmax(a.C)) {
-    case 10: hipLaunchKernelGGL(head_dw_kernel<10>, dim3(blocks), dim3(64 * HDW_WAVES), 0, s, a); break;
-    case 16: hipLaunchKernelGGL(head_dw_kernel<16>, dim3(blocks), dim3(64 * HDW_WAVES), 0, s, a); break;
-    default: hipLaunchKernelGGL(head_dw_kernel<32>, dim3(blocks), dim3(64 * HDW_WAVES), 0, s, a); break;
+    case 10: AGN_LAUNCH(head_dw_kernel<10>, dim3(blocks), dim3(64 * HDW_WAVES), 0, s, a); break;
+    case 16: AGN_LAUNCH(head_dw_kernel<16>, dim3(blocks), dim3(64 * HDW_WAVES), 0, s, a); break;
+    default: AGN_LAUNCH(head_dw_kernel<32>, dim3(blocks), dim3(64 * HDW_WAVES), 0, s, a); break;
   }
   return hipGetLastError();
 }
