@@ -242,13 +242,15 @@ int agn_debug_batch_indices(agn_ctx* ctx, int32_t worker, int64_t step_t,
                              gradient; with few classes also the logits and
                              the output layer's input gradient, fused        */
 #define AGN_K_OUTPUT_DW 2 /* fused output layer only: its weight gradient
-                             with the SGD update                             */
+                             with the SGD update (float32 with at most 10
+                             classes: carried by the AGN_K_DW_FIRST launch on
+                             every local step but a round's last)            */
 #define AGN_K_BWD 3       /* hidden layers l >= 1, one launch per layer: the
                              input-gradient product and the weight-gradient
                              product fused with the SGD update               */
 #define AGN_K_DW_FIRST 4  /* first layer: weight-gradient product (rows
                              gathered from the data set) fused with the SGD
-                             update                                          */
+                             update (and the output layer's, see above)      */
 #define AGN_K_COMMIT 5    /* normalize + commit + pull                       */
 #define AGN_K_EVAL 6      /* agn_evaluate's forward products (not part of a
                              round)                                          */
@@ -257,19 +259,24 @@ int agn_debug_batch_indices(agn_ctx* ctx, int32_t worker, int64_t step_t,
 /* Algorithmic work of one round attributed to a kernel class, as this
  * context launches it: flops = 2 * multiply-adds of the class's matrix
  * products; bytes = the memory traffic the class cannot avoid (for the
- * commit: central + n deltas read, n pulled copies + central written;
+ * commit: central + n deltas read, n pulled copies + central written,
+ * plus the bf16 copies of the pulls in bf16 mode;
  * for the classes with the update: the parameters they update read and
  * written once per local step, plus their bf16 shadow written in bf16
  * mode and Adam's two moment estimates read and written; for the output
  * layer: its activations read and gradients written).  AGN_K_EVAL: the
  * work of the last agn_evaluate call instead (its rows' inputs and the
  * weights read once, the logits written once), zero before the first.
+ * Work carried by another class's launch counts there (AGN_K_OUTPUT_DW).
  * HOST outputs. */
 int agn_kernel_class_work(agn_ctx* ctx, int32_t kernel_class, double* flops,
                           double* bytes);
 
-/* When enabled, every launch of the given class is bracketed by HIP events
- * on the context's stream.  Enabling resets the counters. */
+/* When enabled, every launch of the given class records a pair of HIP
+ * events at its kernel's start and end (the dispatch records them, so the
+ * time is the kernel's own), and rounds run their launches eagerly on the
+ * context's stream instead of replaying the captured graph.  Enabling
+ * resets the counters. */
 int agn_set_kernel_timing(agn_ctx* ctx, int32_t kernel_class, int32_t enable);
 
 /* Total milliseconds and number of launches of the class since timing was
