@@ -4,22 +4,24 @@
 // three K steps ahead of their use, and the fragments of the next K step
 // are read from LDS while the MFMAs of the current one run.
 //
-// Tile: 128x128 outputs per workgroup of 4 waves; wave (wm, wn) owns a
-// 64x64 quarter as 2x2 blocks of v_mfma_f32_32x32x16_bf16; K in steps of 32
-// (two MFMA slices of 16).  In one MFMA, lane (li = l%32, lh = l/32)
-// supplies A[i = li][k = 8*lh .. 8*lh+7] and B[k = 8*lh .. 8*lh+7][j = li],
-// 16 bytes each; the accumulators are laid out as the shared epilogues
+// Tile: TR x TR outputs per workgroup of 4 waves, TR = 128 (two workgroups
+// per CU) or 256 (forward products with a whole 256-row mini-batch per
+// tile, one workgroup per CU); wave (wm, wn) owns a TR/2 x TR/2 quarter as
+// blocks of v_mfma_f32_32x32x16_bf16; K in steps of 32 (two MFMA slices of
+// 16).  In one MFMA, lane (li = l%32, lh = l/32) supplies
+// A[i = li][k = 8*lh .. 8*lh+7] and B[k = 8*lh .. 8*lh+7][j = li], 16 bytes
+// each; the 128-tile accumulators are laid out as the shared epilogues
 // expect.
 //
-// LDS layout of one operand tile (128 x 32 bf16 = 512 chunks of 16 bytes; a
+// LDS layout of one operand tile (TR x 32 bf16 = TR*4 chunks of 16 bytes; a
 // wave's load instruction fills 64 consecutive chunks, lane l chunk l):
 //   K-contiguous (rows = outer index, 4 chunks of 8 k per row): chunk
 //     (r, q) at 4r + (q ^ key(r)), key(r) = ((r >> 1) ^ (r >> 3)) & 3.  A
 //     fragment is one 16-byte read; the rows of 8 consecutive lanes land in
 //     8 distinct 16-byte bank groups modulo 128 bytes, those of 16
 //     consecutive lanes in 16 distinct groups modulo 256 bytes.
-//   K-strided (rows = k, 16 chunks of 8 outer per row): chunk (k, c) at
-//     16k + (c ^ key(k)), key(k) = 0, 6, 12, 10 for k % 4 = 0, 1, 2, 3.  A
+//   K-strided (rows = k, TR/8 chunks of 8 outer per row): chunk (k, c) at
+//     (TR/8)k + (c ^ key(k)), key(k) = 0, 6, 12, 10 for k % 4 = 0..3.  A
 //     fragment is two transposing 8-byte reads (ds_read_b64_tr_b16), each
 //     over four consecutive k rows; the key puts those rows in distinct
 //     bank windows (32 bytes modulo 128, 64 bytes modulo 256).
