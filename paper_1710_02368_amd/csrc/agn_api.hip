@@ -371,7 +371,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
       x.N = c->dims[l];
       x.K = c->dims[l + 1];
       x.batch = n;
-      x.a = Operand{c->dZ[l + 1], dz_ld, dz_st, 0, 1};
+      x.a = Operand{c->dZ[l + 1], dz_ld, dz_st, 0, 1, 1};  // (gradient rows: zero padding, never written)
       x.b = bf ? Operand{src16 + c->woff[l], c->ldw[l], ps, 0, 1} : Operand{src + c->woff[l], c->ldw[l], ps, 0, 1};
       x.g = gath;
       x.epi = EPI_DX_MASK;
@@ -646,6 +646,13 @@ int agn_create(const agn_shapes* shapes, int32_t n, int32_t lambda, float eta, u
   if (e == hipSuccess) e = hipMemset(c->round_dev, 0, 8);
   if (e == hipSuccess) e = hipMemset(c->zero, 0, 1024 * sizeof(float));
   if (e == hipSuccess) e = hipMemset(c->loss, 0, (size_t)n * lambda * c->m * 4);
+  // activations and gradients: their row padding stays zero (no kernel
+  // writes it; the bf16 products read it as a zero K tail)
+  for (int l = 1; e == hipSuccess && l <= L; ++l) {
+    const size_t bytes = (size_t)n * c->m * c->lda[l] * act;
+    if (l < L) e = hipMemset(c->H[l], 0, bytes);
+    if (e == hipSuccess) e = hipMemset(c->dZ[l], 0, bytes);
+  }
   if (e != hipSuccess) return bail(AGN_EHIP, std::string("hipMemset: ") + hipGetErrorString(e));
 
   std::vector<float> init(P);

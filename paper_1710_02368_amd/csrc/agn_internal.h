@@ -34,6 +34,7 @@ struct Operand {
   int64_t wstride;  // elements between consecutive workers' matrices (0: shared)
   int32_t gather;   // 1: stored rows are data-set rows picked by the batch index
   int32_t vec;      // 1: ld % 4 == 0 and ptr 16-byte aligned (vector loads allowed)
+  int32_t padded = 0;  // 1: the elements between a row's last column and ld are zero
 };
 
 // Batch index of a gathered operand: worker k, local step t = round*lam + step,

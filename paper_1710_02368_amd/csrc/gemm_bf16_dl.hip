@@ -523,21 +523,25 @@ __global__ __launch_bounds__(NT) void gemm_bf16_dl_bwd_kernel(GemmArgs dx, GemmA
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
-// the operand can be staged in 16-byte chunks (8 bf16) that never straddle
-// an edge; a K-strided operand may be gathered only where the caller says so
+// the operand can be staged in 16-byte chunks (8 bf16).  A chunk may cross
+// an edge only inside the row's padding: past K of a K-contiguous operand
+// when that padding is zero (it meets the other operand's zero-page rows,
+// so it adds nothing), past the outer size of a K-strided one in any case
+// (those columns feed only outputs that are never stored).  A K-strided
+// operand may be gathered only where the caller says so.
 bool operand_ok(const Operand& op, bool kc, int outer_n, int K, bool gather_ok) {
   if (!op.vec || !aligned16(op.ptr) || op.ld % 8 || op.wstride % 8) return false;
-  if (kc) return K % 8 == 0;
-  return outer_n % 8 == 0 && (!op.gather || gather_ok);
+  if (kc) return K % 8 == 0 || (op.padded && op.ld >= (K + 7) / 8 * 8);
+  return (outer_n % 8 == 0 || op.ld >= (outer_n + 7) / 8 * 8) && (!op.gather || gather_ok);
 }
 
 }  // namespace
 
 bool gemm_bf16_dl_ok(int a_kc, int b_kc, const GemmArgs& g) {
   if (!g.zero || g.M <= 0 || g.N <= 0 || g.K <= 0) return false;
-  if (a_kc && b_kc)
-    return (g.epi == EPI_FWD_RELU || g.epi == EPI_FWD_LINEAR) && operand_ok(g.a, true, g.M, g.K, false) &&
-           operand_ok(g.b, true, g.N, g.K, false) && out_vec_ok(g);
+  if (a_kc && b_kc)  // (both K-contiguous: no chunk past K, it would meet the other's padding)
+    return (g.epi == EPI_FWD_RELU || g.epi == EPI_FWD_LINEAR) && g.K % 8 == 0 &&
+           operand_ok(g.a, true, g.M, g.K, false) && operand_ok(g.b, true, g.N, g.K, false) && out_vec_ok(g);
   if (a_kc && !b_kc)
     return g.epi == EPI_DX_MASK && operand_ok(g.a, true, g.M, g.K, false) &&
            operand_ok(g.b, false, g.N, g.K, false) && out_vec_ok(g);
