@@ -349,8 +349,10 @@ def main():
         e = {"ms_per_round": round(per_round_s * 1e3, 4), "launches_per_round": cnt // prof_rounds}
         if work[c]["flops"] > 0:
             e["TFLOP/s"] = round(work[c]["flops"] / per_round_s / 1e12, 2)
+            e["mfma_frac"] = round(work[c]["flops"] / per_round_s / 1e12 / PEAK_TFLOPS[wl.dtype], 4)
         if work[c]["bytes"] > 0:
             e["GB/s"] = round(work[c]["bytes"] / per_round_s / 1e9, 1)
+            e["hbm_frac"] = round(work[c]["bytes"] / per_round_s / 1e9 / PEAK_HBM_GBS, 4)
         breakdown[c] = e
     dominant = max(breakdown, key=lambda c: breakdown[c]["ms_per_round"])
 
