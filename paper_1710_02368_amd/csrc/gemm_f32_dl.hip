@@ -389,6 +389,183 @@ __device__ __forceinline__ void tile_dl(const GemmArgs& g, const int logical, fl
 }
 
 // ---------------------------------------------------------------------------
+// Forward product with eight waves (two per SIMD) splitting each K step:
+// waves 0-3 take MFMA slices 0-3 of the step, waves 4-7 slices 4-7, each
+// wave with the accumulators of its 32 x 32 block (wm, wn).  A wave waiting
+// at a barrier or on its LDS reads leaves the matrix core to the other wave
+// of its SIMD.  The halves are added (waves 4-7 through LDS) before the
+// epilogue.  Tiles, LDS layout and loads as in the four-wave schedule; each
+// wave issues one load instruction per operand and step (j = wave).
+constexpr int NT8 = 512;
+
+struct Loader1 {  // K-contiguous operand, one load instruction per wave and step
+  const float* zero;
+  const float* fast;  // the lane's row (clamped into the matrix)
+  int lk;             // its k offset inside a step
+  bool valid;         // the row lies inside the matrix
+  int K;
+
+  __device__ void init(const Operand& op, const Gather& g, const float* zp, int64_t w, int o0, int on, int k,
+                       int wave, int lane) {
+    const float* base = reinterpret_cast<const float*>(op.ptr) + w * op.wstride;
+    const int r = 8 * wave + lane / 8;
+    const int o = o0 + r, oc = o < on ? o : on - 1;
+    const int64_t t = op.gather ? gather_step(g) : 0;
+    const int64_t ri = op.gather ? batch_row(w, t, g.mb, g.S, oc) : oc;
+    zero = zp;
+    K = k;
+    valid = o < on;
+    fast = base + ri * op.ld;
+    lk = 4 * ((lane % 8) ^ kc_key(r));
+  }
+  __device__ const float* src_full(int k0) const { return fast + (k0 + lk); }
+  __device__ const float* src(int k0) const {
+    const int k = k0 + lk;
+    return (valid && k < K) ? fast + k : zero;
+  }
+};
+
+// this wave's half of a K step's fragments: slices 4*kh .. 4*kh+3, i.e. the
+// lane's 16-byte chunk 2*lg + kh of its row
+__device__ __forceinline__ void frag_half(const float* tile, int outer_off, int li, int lg, int kh, f32x4 (&f)[2]) {
+#pragma unroll
+  for (int b = 0; b < 2; ++b)
+    f[b] = *reinterpret_cast<const f32x4*>(tile + 4 * kc_slot(outer_off + 16 * b + li, 2 * lg + kh));
+}
+
+struct FragsH {
+  f32x4 a[2], b[2];
+};
+
+__device__ __forceinline__ void k_step8(int wave, int wm, int wn, int li, int lg, int kh, const FragsH& cur,
+                                        FragsH& nxt, const float* rd, float* wr, const float* sa, const float* sb,
+                                        f32x4 (&acc)[2][2]) {
+  wait_lgkm0();
+  wait_vm<2 * (NS - 2)>();
+  barrier();
+  frag_half(rd, wm * 32, li, lg, kh, nxt.a);
+  frag_half(rd + TILE_F, wn * 32, li, lg, kh, nxt.b);
+  const uint32_t wa = lds_off(wr) + 4 * 256 * wave;
+  fire(sa, wa);
+  fire(sb, wa + 4 * TILE_F);
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int bj = 0; bj < 2; ++bj)
+        acc[bi][bj] = __builtin_amdgcn_mfma_f32_16x16x4f32(cur.a[bi][s], cur.b[bj][s], acc[bi][bj], 0, 0, 0);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS read
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);  // MFMA
+  }
+}
+
+template <int EPI>
+__device__ __forceinline__ void tile_fwd8(const GemmArgs& g, const int logical, float* st0, float* st1, float* st2,
+                                          float* st3) {
+  static_assert(EPI == EPI_FWD_RELU || EPI == EPI_FWD_LINEAR, "forward products only");
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int kh = wave >> 2, wm = (wave & 3) >> 1, wn = wave & 1, li = lane & 15, lg = lane >> 4;
+  const TileCoord c = coord_of(g, logical);
+  const int worker = c.worker, m0 = c.m0, n0 = c.n0;
+  const int rbase = m0 + wm * 32, cbase = n0 + wn * 32;
+  // accumulator (bi, bj, r) sits at row rbase + 16*bi + 4*lg + r, column
+  // cbase + 16*bj + li; the bias of this lane's two columns first (clamped,
+  // unconditional, oldest in the memory queue)
+  float bpre[2];
+#pragma unroll
+  for (int bj = 0; bj < 2; ++bj) bpre[bj] = g.bias[(int64_t)worker * g.bstride + min(cbase + 16 * bj + li, g.N - 1)];
+
+  Loader1 la, lb;
+  la.init(g.a, g.g, g.zero, worker, m0, g.M, g.K, wave, lane);
+  lb.init(g.b, g.g, g.zero, worker, n0, g.N, g.K, wave, lane);
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj) acc[bi][bj] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int nk = (g.K + BKD - 1) / BKD;
+  {
+    float* stg[NS] = {st0, st1, st2, st3};
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const uint32_t wa = lds_off(stg[s]) + 4 * 256 * wave;
+      fire(la.src(s * BKD), wa);
+      fire(lb.src(s * BKD), wa + 4 * TILE_F);
+    }
+  }
+  wait_vm<2 * (NS - 1)>();
+  barrier();
+  FragsH f0, f1;
+  frag_half(st0, wm * 32, li, lg, kh, f0.a);
+  frag_half(st0 + TILE_F, wn * 32, li, lg, kh, f0.b);
+
+  auto step = [&](auto full, const FragsH& cur, FragsH& nxt, const float* rd, float* wr, int kt) {
+    const int k0 = (kt + NS) * BKD;
+    if constexpr (decltype(full)::value)
+      k_step8(wave, wm, wn, li, lg, kh, cur, nxt, rd, wr, la.src_full(k0), lb.src_full(k0), acc);
+    else
+      k_step8(wave, wm, wn, li, lg, kh, cur, nxt, rd, wr, la.src(k0), lb.src(k0), acc);
+  };
+  using Full = std::true_type;
+  using Checked = std::false_type;
+  const int nk4 = nk & ~3;
+  const int nfast = (g.K / BKD - NS > 0 ? g.K / BKD - NS : 0) & ~3;  // steps kt whose step kt+NS is full
+  int kt = 0;
+  for (; kt < nfast && kt < nk4; kt += 4) {
+    step(Full{}, f0, f1, st1, st0, kt);
+    step(Full{}, f1, f0, st2, st1, kt + 1);
+    step(Full{}, f0, f1, st3, st2, kt + 2);
+    step(Full{}, f1, f0, st0, st3, kt + 3);
+  }
+  for (; kt < nk4; kt += 4) {
+    step(Checked{}, f0, f1, st1, st0, kt);
+    step(Checked{}, f1, f0, st2, st1, kt + 1);
+    step(Checked{}, f0, f1, st3, st2, kt + 2);
+    step(Checked{}, f1, f0, st0, st3, kt + 3);
+  }
+  if (nk4 < nk) step(Checked{}, f0, f1, st1, st0, nk4);
+  if (nk4 + 1 < nk) step(Checked{}, f1, f0, st2, st1, nk4 + 1);
+  if (nk4 + 2 < nk) step(Checked{}, f0, f1, st3, st2, nk4 + 2);
+  // every load (also those of the steps past the end) has landed and every
+  // wave is done reading the stages: waves 4-7 hand their sums over in LDS
+  wait_vm<0>();
+  wait_lgkm0();
+  barrier();
+  f32x4* xfer = reinterpret_cast<f32x4*>(st0) + ((wave & 3) * 64 + lane) * 4;
+  if (kh == 1) {
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int bj = 0; bj < 2; ++bj) xfer[2 * bi + bj] = acc[bi][bj];
+  }
+  __syncthreads();
+  if (kh == 1) return;
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj) acc[bi][bj] += xfer[2 * bi + bj];
+  asm volatile("" ::"v"(bpre[0]), "v"(bpre[1]));
+  float* out = reinterpret_cast<float*>(g.out) + (int64_t)worker * g.ostride;
+#pragma unroll
+  for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int bj = 0; bj < 2; ++bj) {
+        const int row = rbase + 16 * bi + 4 * lg + r, col = cbase + 16 * bj + li;
+        if (row >= g.M || col >= g.N) continue;
+        float z = acc[bi][bj][r] + bpre[bj];
+        if (EPI == EPI_FWD_RELU) z = z > 0.f ? z : 0.f;
+        out[(int64_t)row * g.ldo + col] = z;
+      }
+}
+
+// ---------------------------------------------------------------------------
 // Persistent schedule of the weight-gradient product
 //   dW = dZ^T H (A = dZ [K][M] and B = H [K][N], both K-strided; for the
 //   first layer H is the gathered data rows),
@@ -682,6 +859,13 @@ __device__ __forceinline__ void dw_tiles(const GemmArgs& g, const TileList tl, f
   __shared__ __attribute__((aligned(16))) float epi[(LAST ? 2 : 1) * EPI_F]; \
   float* epi2 = epi + (LAST ? EPI_F : 0);  /* (snapshot tile: last step only) */
 
+// forward products, eight waves splitting each K step
+template <int EPI>
+__global__ __launch_bounds__(NT8) void gemm_f32_dl_fwd8_kernel(GemmArgs g) {
+  DL_STAGES
+  tile_fwd8<EPI>(g, xcd_remap(blockIdx.x, tiles_dl(g)), st0, st1, st2, st3);
+}
+
 template <bool A_KC, bool B_KC, int EPI>
 __global__ __launch_bounds__(NT) void gemm_f32_dl_kernel(GemmArgs g) {
   DL_STAGES
@@ -795,9 +979,9 @@ bool gemm_f32_dl_ok(int a_kc, int b_kc, const GemmArgs& g) {
 hipError_t launch_gemm_f32_dl(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s) {
   const dim3 grid(tiles_dl(g)), block(NT);
   if (a_kc && b_kc && g.epi == EPI_FWD_RELU)
-    AGN_LAUNCH((gemm_f32_dl_kernel<true, true, EPI_FWD_RELU>), grid, block, 0, s, g);
+    AGN_LAUNCH((gemm_f32_dl_fwd8_kernel<EPI_FWD_RELU>), grid, dim3(NT8), 0, s, g);
   else if (a_kc && b_kc && g.epi == EPI_FWD_LINEAR)
-    AGN_LAUNCH((gemm_f32_dl_kernel<true, true, EPI_FWD_LINEAR>), grid, block, 0, s, g);
+    AGN_LAUNCH((gemm_f32_dl_fwd8_kernel<EPI_FWD_LINEAR>), grid, dim3(NT8), 0, s, g);
   else if (a_kc && !b_kc && g.epi == EPI_DX_MASK)
     AGN_LAUNCH((gemm_f32_dl_kernel<true, false, EPI_DX_MASK>), grid, block, 0, s, g);
   else if (!a_kc && !b_kc && g.epi == EPI_DW_UPDATE) {
