@@ -51,6 +51,7 @@ def test_traffic_classes():
     assert bench.traffic_class("void agn::(anonymous namespace)::gemm_bf16_dl_kernel<false, false, 3>(x)") == "dw_first"
     assert bench.traffic_class("void agn::(anonymous namespace)::gemm_f32_dl_dw_kernel<true>(x)") == "dw_first"
     assert bench.traffic_class("void agn::(anonymous namespace)::gemm_bf16_dl_big_kernel<true, true, 0>(x)") == "fwd"
+    assert bench.traffic_class("void agn::(anonymous namespace)::gemm_f32_dl_fwd8_kernel<0>(agn::GemmArgs)") == "fwd"
     assert bench.traffic_class("void agn::(anonymous namespace)::head_dw_kernel<10>(x)") == "output_dw"
     assert bench.traffic_class("void agn::(anonymous namespace)::head_kernel<10, 16, false>(x)") == "output"
     assert bench.traffic_class("__amd_rocclr_fillBufferAligned") is None
