@@ -34,7 +34,8 @@
 //
 // Two schedules:
 //   * forward and input-gradient products (K = layer width, tens of K
-//     steps): one output tile per workgroup;
+//     steps): one output tile per workgroup (the forward with eight waves
+//     that split each K step between two waves per block);
 //   * weight-gradient products (K = mini-batch, a few K steps per tile):
 //     persistent workgroups walk a list of tiles and the operand loads run
 //     on across tile boundaries, so a tile's first steps load while the
