@@ -77,6 +77,8 @@ EVAL_CASES = [
     ("two_chunks_single_layer", (33, 7), 2, 16, 8193, "gauss_linear", "fp32"),
     ("two_chunks_many_classes", (60, 50, 40), 3, 24, 9000, "gauss_linear", "fp32"),
     ("bf16_two_chunks", (200, 130, 70, 10), 3, 40, 8192 + 555, "gauss_linear", "bf16"),
+    # a full 8192-row chunk of a 2048-wide layer: 256 x 256 forward tiles
+    ("bf16_big_tiles", (64, 2048, 10), 2, 16, 8192 + 300, "gauss_linear", "bf16"),
 ]
 
 
