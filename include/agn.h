@@ -243,8 +243,7 @@ int agn_debug_batch_indices(agn_ctx* ctx, int32_t worker, int64_t step_t,
                              the output layer's input gradient, fused        */
 #define AGN_K_OUTPUT_DW 2 /* fused output layer only: its weight gradient
                              with the SGD update (float32 with at most 10
-                             classes: carried by the AGN_K_DW_FIRST launch on
-                             every local step but a round's last)            */
+                             classes: carried by the AGN_K_DW_FIRST launch)  */
 #define AGN_K_BWD 3       /* hidden layers l >= 1, one launch per layer: the
                              input-gradient product and the weight-gradient
                              product fused with the SGD update               */

@@ -334,9 +334,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     // with a first-layer weight gradient on the direct-load path, the
     // output layer's update rides in that launch (it touches nothing the
     // layers in between read or write)
-    // (not on a round's last step: its first-layer launch runs one
-    // workgroup per CU, and the folded units would lengthen it)
-    fold_head_dw = !bf && !last && L >= 2 && gemm_f32_dl_dw_head_ok(dw_args(0), w);
+    fold_head_dw = !bf && L >= 2 && gemm_f32_dl_dw_head_ok(dw_args(0), w);
     if (!fold_head_dw) HIP_CHECK(c, timed(c, AGN_K_OUTPUT_DW, [&] { return launch_head_dw(w, c->ls); }));
   } else {
     // softmax cross-entropy: per-row loss and the output gradient dZ_L

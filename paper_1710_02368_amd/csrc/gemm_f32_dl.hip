@@ -651,11 +651,16 @@ struct DwLoads {
   }
 };
 
-// Epilogue operand tile(s) of tile `c` into LDS: rows m0.., columns n0..
-// of W_src (and W_snap), row-major 64 x 64.  This wave: rows 4j .. 4j+3 for
-// j = 4*wave .. 4*wave+3, lane l row 4j + l/16, columns 4*(l%16) .. +3.
+// Epilogue operands of tile `c`: W_src into LDS (rows m0.., columns n0..,
+// row-major 64 x 64; this wave: rows 4j .. 4j+3 for j = 4*wave .. 4*wave+3,
+// lane l row 4j + l/16, columns 4*(l%16) .. +3), and on a round's last step
+// the lane's own W_snap pairs straight into registers (rows and columns as
+// its accumulators; clamped into the matrix, never stored outside it).  The
+// snapshot's loads are ordinary loads, so the compiler waits for them where
+// the epilogue reads them; in LDS it would take a second tile buffer, and
+// with it the second workgroup of each CU.
 template <bool LAST>
-__device__ __forceinline__ void fire_epi(const GemmArgs& g, const TileCoord& c, float* epi, float* epi2,
+__device__ __forceinline__ void fire_epi(const GemmArgs& g, const TileCoord& c, float* epi, float2 (&snap)[2][4],
                                          const Lanes& q) {
   const int64_t wo = (int64_t)c.worker * g.pstride;
 #pragma unroll
@@ -665,14 +670,23 @@ __device__ __forceinline__ void fire_epi(const GemmArgs& g, const TileCoord& c, 
     const bool ok = row < g.M && col < g.N;
     const int64_t e = wo + (int64_t)row * g.ldw + col;
     fire(ok ? g.w_src + e : g.zero, lds_off(epi) + 4 * 256 * j);
-    if (LAST) fire(ok ? g.w_snap + e : g.zero, lds_off(epi2) + 4 * 256 * j);
+  }
+  if constexpr (LAST) {
+#pragma unroll
+    for (int bi = 0; bi < 2; ++bi)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = min(c.m0 + q.wm * 32 + 2 * (4 * q.lg + r) + bi, g.M - 1);
+        const int col = min(c.n0 + q.wn * 32 + 2 * q.li, g.N - 2);  // (N even)
+        snap[bi][r] = *reinterpret_cast<const float2*>(g.w_snap + wo + (int64_t)row * g.ldw + col);
+      }
   }
 }
 
 template <bool LAST>
 __device__ __forceinline__ void dw_tiles(const GemmArgs& g, const TileList tl, float* st0, float* st1, float* st2,
-                                         float* st3, float* epi, float* epi2) {
-  constexpr int EPN = LAST ? 8 : 4;  // epilogue load instructions per wave and tile
+                                         float* st3, float* epi) {
+  constexpr int EPN = LAST ? 4 + 8 : 4;  // epilogue load instructions per wave and tile
   if (tl.count == 0) return;
   const int tid = threadIdx.x;
   const Lanes q{tid >> 6, tid & 63, (tid >> 6) >> 1, (tid >> 6) & 1, tid & 15, (tid & 63) >> 4};
@@ -712,7 +726,8 @@ __device__ __forceinline__ void dw_tiles(const GemmArgs& g, const TileList tl, f
       fire(ld.b_src(s * BKD, 1), wa + 4 * (TILE_F + 256));
     }
   }
-  fire_epi<LAST>(g, coord_of(g, tl.logical(0)), epi, epi2, q);
+  float2 snap[2][4];
+  fire_epi<LAST>(g, coord_of(g, tl.logical(0)), epi, snap, q);
   wait_vm<4 * (NS - 1) + EPN>();
   barrier();
   Frags f0, f1;
@@ -787,9 +802,8 @@ __device__ __forceinline__ void dw_tiles(const GemmArgs& g, const TileList tl, f
         const float2 ws = *reinterpret_cast<const float2*>(epi + tr * TM + tc);
         float2 v{ws.x - g.eta * acc[bi][0][r], ws.y - g.eta * acc[bi][1][r]};
         if (LAST) {
-          const float2 sn = *reinterpret_cast<const float2*>(epi2 + tr * TM + tc);
-          v.x = (v.x - sn.x) / g.lam;
-          v.y = (v.y - sn.y) / g.lam;
+          v.x = (v.x - snap[bi][r].x) / g.lam;
+          v.y = (v.y - snap[bi][r].y) / g.lam;
         }
         nw[bi][r] = v;
       }
@@ -842,7 +856,7 @@ __device__ __forceinline__ void dw_tiles(const GemmArgs& g, const TileList tl, f
       // every wave has read this tile's epilogue operands: load the next's
       wait_lgkm0();
       barrier();
-      fire_epi<LAST>(g, coord_of(g, tl.logical(i + 1)), epi, epi2, q);
+      fire_epi<LAST>(g, coord_of(g, tl.logical(i + 1)), epi, snap, q);
     }
   }
   // loads of the steps past the end (zero page) still write LDS
@@ -856,9 +870,7 @@ __device__ __forceinline__ void dw_tiles(const GemmArgs& g, const TileList tl, f
   __shared__ __attribute__((aligned(16))) float st1[STAGE_F];     \
   __shared__ __attribute__((aligned(16))) float st2[STAGE_F];     \
   __shared__ __attribute__((aligned(16))) float st3[STAGE_F];
-#define DL_EPI(LAST)                                                  \
-  __shared__ __attribute__((aligned(16))) float epi[(LAST ? 2 : 1) * EPI_F]; \
-  float* epi2 = epi + (LAST ? EPI_F : 0);  /* (snapshot tile: last step only) */
+#define DL_EPI __shared__ __attribute__((aligned(16))) float epi[EPI_F];
 
 // forward products, eight waves splitting each K step
 template <int EPI>
@@ -890,7 +902,7 @@ __device__ __forceinline__ int fewest_tiles_rank(int wg, int nwg) {
 template <bool LAST, int HCM>
 __global__ __launch_bounds__(NT) void gemm_f32_dl_dw_kernel(GemmArgs g, HeadDwArgs h) {
   DL_STAGES
-  DL_EPI(LAST)
+  DL_EPI
   if constexpr (HCM > 0) {
     static_assert(hdw_smem_floats<HCM>() <= STAGE_F, "an output-layer unit fits one stage buffer");
     const int units = hdw_units(h);
@@ -902,7 +914,7 @@ __global__ __launch_bounds__(NT) void gemm_f32_dl_dw_kernel(GemmArgs g, HeadDwAr
     }
     if (ran) __syncthreads();    // before the tiles' loads land in the stages
   }
-  dw_tiles<LAST>(g, tiles_of_wg(tiles_dl(g), blockIdx.x, gridDim.x), st0, st1, st2, st3, epi, epi2);
+  dw_tiles<LAST>(g, tiles_of_wg(tiles_dl(g), blockIdx.x, gridDim.x), st0, st1, st2, st3, epi);
 }
 
 // Weight-gradient tiles of workgroup `pid` in the combined backward launch
@@ -931,7 +943,7 @@ template <bool LAST>
 __global__ __launch_bounds__(NT) void gemm_f32_dl_bwd_kernel(GemmArgs dx, GemmArgs dw, int n1, int n1pad, int ca,
                                                              int cb) {
   DL_STAGES
-  DL_EPI(LAST)
+  DL_EPI
   const int pid = blockIdx.x;
   if (pid < n1) {
     tile_dl<true, false, EPI_DX_MASK>(dx, xcd_remap(pid, n1), st0, st1, st2, st3);
@@ -939,7 +951,7 @@ __global__ __launch_bounds__(NT) void gemm_f32_dl_bwd_kernel(GemmArgs dx, GemmAr
     wait_lgkm0();
     barrier();
   }
-  dw_tiles<LAST>(dw, split_tiles(tiles_dl(dw), pid, n1pad, ca, cb), st0, st1, st2, st3, epi, epi2);
+  dw_tiles<LAST>(dw, split_tiles(tiles_dl(dw), pid, n1pad, ca, cb), st0, st1, st2, st3, epi);
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }

@@ -367,8 +367,9 @@ def test_errors_leave_state_unchanged():
 def test_output_layer_update_rides_in_first_layer_launch(dims, folded):
     """With at most 10 classes and the first layer's weight gradient on the
     direct-load path, the output layer's weight update runs inside that
-    launch on every local step but a round's last; the class accounting
-    follows, and the round still matches the oracle."""
+    launch on every local step (the round's last one included, where it
+    stores the normalized displacement); the class accounting follows, and
+    the round still matches the oracle."""
     agn = _agn()
     wl = W.small_workload("fold", dims, 3, 2, 100, 0.05, 1, 650, data="sparse_teacher2", order="permutation")
     X, y = W.make_data(wl)
@@ -387,11 +388,9 @@ def test_output_layer_update_rides_in_first_layer_launch(dims, folded):
     mac = lambda l: dims[l] * dims[l + 1]
     rows = wl.n * wl.lam * wl.m
     assert n_first == wl.lam
-    if folded:   # (every local step but the round's last)
-        assert n_out_dw == 1
-        assert f_out_dw == pytest.approx(2.0 * mac(len(dims) - 2) * rows / wl.lam, rel=1e-12)
-        assert f_first == pytest.approx(2.0 * (mac(0) + mac(len(dims) - 2) * (wl.lam - 1) / wl.lam) * rows,
-                                        rel=1e-12)
+    if folded:
+        assert n_out_dw == 0 and f_out_dw == 0.0
+        assert f_first == pytest.approx(2.0 * (mac(0) + mac(len(dims) - 2)) * rows, rel=1e-12)
     else:
         assert n_out_dw == wl.lam and f_out_dw == pytest.approx(2.0 * mac(len(dims) - 2) * rows, rel=1e-12)
         assert f_first == pytest.approx(2.0 * mac(0) * rows, rel=1e-12)
