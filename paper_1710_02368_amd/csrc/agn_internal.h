@@ -154,6 +154,7 @@ struct HeadArgs {
   float* row_loss;         // [m] or null
   int32_t* row_pred;       // [m] or null
   double* part;            // [2 * head_eval_blocks(m)]
+  int32_t vec;             // (set by the launch: rows of h and dprev allow 16-byte accesses)
 };
 struct HeadDwArgs {        // output-layer weight gradient + update (M = C <= 32)
   const float* h;

@@ -22,13 +22,30 @@
 namespace agn {
 namespace {
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 constexpr int HEAD_WAVE_ROWS = 1;                  // rows a wave processes together
 constexpr int HEAD_DMAX = 2048;                     // hidden width limit
 
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float lane_value(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+
+// Sum over the wave (every lane active), the same value in every lane and
+// on every call: within each row of 16 lanes by data-parallel moves (quad
+// pairs 1<->0, 3<->2, then 2<->0, 3<->1; then the two quads of each half
+// row, i <-> 7-i; then the two halves, i <-> 15-i), then the four row sums
+// in row order.
 __device__ __forceinline__ float wsum(float v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
+  v += dpp<0xB1>(v);   // quad_perm(1, 0, 3, 2)
+  v += dpp<0x4E>(v);   // quad_perm(2, 3, 0, 1)
+  v += dpp<0x141>(v);  // row_half_mirror
+  v += dpp<0x140>(v);  // row_mirror
+  return ((lane_value(v, 0) + lane_value(v, 16)) + lane_value(v, 32)) + lane_value(v, 48);
 }
 
 // Argmax order of the evaluation: a NaN beats any number, a larger value a
@@ -42,19 +59,29 @@ __device__ __forceinline__ bool beats_h(float v, int i, float bv, int bi) {
 
 constexpr int EVAL_WAVE_ROWS = 4;                   // rows per wave in the evaluation variant
 __host__ __device__ constexpr int head_rows(bool eval) { return 4 * (eval ? EVAL_WAVE_ROWS : HEAD_WAVE_ROWS); }
+// Waves per row: the training variant splits each row's columns over two
+// waves when each lane holds at least two groups of them (its latency is
+// one row per wave; the evaluation variant runs many rows per wave instead)
+__host__ __device__ constexpr int head_split(int q4, bool eval) { return !eval && q4 >= 2 ? 2 : 1; }
 
-// LDS: W padded to CMAX rows x 64*QMAX columns (zeros outside C x d), then b.
-// Each wave keeps its rows of H in registers (QMAX per lane per row, all
-// loaded at once); padding rows and columns are zero, so the loops are
-// static and branch-free.
-template <int CMAX, int QMAX, bool EVAL>
-__global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
+// LDS: W padded to CMAX rows x 256*Q4 columns (zeros outside C x d), then b.
+// Lane l owns the columns 4l + 256q .. +3 of every row, for the groups q of
+// its wave's share (all Q4 of them, or half when SP = 2 waves share a row):
+// it keeps them of its wave's rows of H in registers (all loaded at once,
+// 16 bytes at a time when the rows allow it) and reads W and writes the
+// input gradient 16 bytes at a time.  Padding rows and columns are zero, so
+// the loops are static and branch-free.
+template <int CMAX, int Q4, bool EVAL>
+__global__ __launch_bounds__(256 * head_split(Q4, EVAL)) void head_kernel(HeadArgs a) {
   extern __shared__ float smem[];
   __shared__ double epart[EVAL ? 8 : 1];
-  constexpr int LW = 64 * QMAX;
+  constexpr int SP = head_split(Q4, EVAL), QH = Q4 / SP, NTH = 256 * SP;
+  __shared__ float xch[SP > 1 ? 4 * SP * CMAX : 1];  // the halves' logits
+  constexpr int LW = 256 * Q4;
   constexpr int WR = EVAL ? EVAL_WAVE_ROWS : HEAD_WAVE_ROWS;  // rows per wave
   constexpr int RB = 4 * WR;                                     // rows per workgroup
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = (tid >> 6) / SP, half = (tid >> 6) % SP;
+  const int qb = QH * half;  // this wave's first column group
   const int blocks_per_worker = (a.m + RB - 1) / RB;
   const int k = blockIdx.x / blocks_per_worker;
   const int r0 = (blockIdx.x % blocks_per_worker) * RB;
@@ -70,7 +97,7 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
   int jr[WR];
   int label[WR];
   const float* hp[WR];
-  float hv[WR][QMAX];
+  f32x4 hv[WR][QH];
 #pragma unroll
   for (int r = 0; r < WR; ++r) {
     jr[r] = r0 + wave * WR + r;
@@ -79,27 +106,32 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
     hp[r] = a.gather ? a.h + batch_row(k, t, a.g.mb, a.g.S, j) * a.ldh
                      : a.h + (int64_t)k * a.hstride + (int64_t)j * a.ldh;
 #pragma unroll
-    for (int q = 0; q < QMAX; ++q) {
-      const int i = lane + 64 * q;
-      hv[r][q] = hp[r][i < d ? i : d - 1];
+    for (int q = 0; q < QH; ++q) {
+      const int i = 4 * lane + 256 * (qb + q);
+      if (a.vec) {  // (d a multiple of 4: a group lies inside the row or past it)
+        hv[r][q] = *reinterpret_cast<const f32x4*>(hp[r] + (i < d ? i : d - 4));
+      } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) hv[r][q][e] = hp[r][i + e < d ? i + e : d - 1];
+      }
     }
   }
   // W and b into LDS, float4 at a time (W rows are 16-byte aligned).  All
   // loads first, unconditionally (row and column clamped into the padded W:
   // rows are ldw >= d floats, ldw a multiple of 8), then the LDS writes with
   // the parts outside C x d zeroed: the loads are in flight together
-  constexpr int NW4 = CMAX * LW / 4, WIT = (NW4 + 255) / 256;
+  constexpr int NW4 = CMAX * LW / 4, WIT = (NW4 + NTH - 1) / NTH;
   float4 wv[WIT];
 #pragma unroll
   for (int it = 0; it < WIT; ++it) {
-    const int e4 = min(tid + 256 * it, NW4 - 1);
+    const int e4 = min(tid + NTH * it, NW4 - 1);
     const int c = min(e4 / (LW / 4), C - 1), i = min(4 * (e4 % (LW / 4)), (int)a.ldw - 4);
     wv[it] = *reinterpret_cast<const float4*>(W + (int64_t)c * a.ldw + i);
   }
 #pragma unroll
   for (int it = 0; it < WIT; ++it) {
-    const int e4 = tid + 256 * it;
-    if (NW4 % 256 != 0 && e4 >= NW4) break;
+    const int e4 = tid + NTH * it;
+    if (NW4 % NTH != 0 && e4 >= NW4) break;
     const int c = e4 / (LW / 4), i = 4 * (e4 % (LW / 4));
     float4 v = wv[it];
     if (c >= C || i >= d) v = make_float4(0.f, 0.f, 0.f, 0.f);
@@ -115,7 +147,9 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
 #pragma unroll
   for (int r = 0; r < WR; ++r)
 #pragma unroll
-    for (int q = 0; q < QMAX; ++q) hv[r][q] = lane + 64 * q < d ? hv[r][q] : 0.f;
+    for (int q = 0; q < QH; ++q)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) hv[r][q][e] = 4 * lane + 256 * (qb + q) + e < d ? hv[r][q][e] : 0.f;
   __syncthreads();
 
   // logits: lane-partial dot products, then one wave reduction per (row, class)
@@ -125,18 +159,42 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
 #pragma unroll
     for (int c = 0; c < CMAX; ++c) p[r][c] = 0.f;
 #pragma unroll
-  for (int q = 0; q < QMAX; ++q) {
+  for (int q = 0; q < QH; ++q) {
 #pragma unroll
     for (int c = 0; c < CMAX; ++c) {
-      const float w = Ws[c * LW + lane + 64 * q];
+      const f32x4 w = *reinterpret_cast<const f32x4*>(Ws + c * LW + 4 * lane + 256 * (qb + q));
 #pragma unroll
-      for (int r = 0; r < WR; ++r) p[r][c] += hv[r][q] * w;
+      for (int r = 0; r < WR; ++r)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) p[r][c] += hv[r][q][e] * w[e];
     }
   }
+  if constexpr (SP == 1) {
 #pragma unroll
-  for (int r = 0; r < WR; ++r)
+    for (int r = 0; r < WR; ++r)
 #pragma unroll
-    for (int c = 0; c < CMAX; ++c) p[r][c] = wsum(p[r][c]) + bs[c];
+      for (int c = 0; c < CMAX; ++c) p[r][c] = wsum(p[r][c]) + bs[c];
+  } else {
+    // each wave's partial logits to LDS; then both waves of a row add the
+    // halves in the same order and hold the same logits
+    static_assert(WR == 1, "one row per wave pair");
+#pragma unroll
+    for (int c = 0; c < CMAX; ++c) p[0][c] = wsum(p[0][c]);
+    if (lane < CMAX) {
+      float mine = 0.f;
+#pragma unroll
+      for (int c = 0; c < CMAX; ++c) mine = lane == c ? p[0][c] : mine;
+      xch[(wave * SP + half) * CMAX + lane] = mine;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int c = 0; c < CMAX; ++c) {
+      float z = xch[wave * SP * CMAX + c];
+#pragma unroll
+      for (int h = 1; h < SP; ++h) z += xch[(wave * SP + h) * CMAX + c];
+      p[0][c] = z + bs[c];
+    }
+  }
 
   if constexpr (EVAL) {
     // loss, predicted class and the block's partial sums (fixed order)
@@ -204,7 +262,7 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
 #pragma unroll
     for (int c = 0; c < CMAX; ++c)
       p[r][c] = c < C ? (p[r][c] * inv_s - (c == lb ? 1.f : 0.f)) * inv_m : 0.f;
-    if (jr[r] < a.m) {
+    if (jr[r] < a.m && half == 0) {
       float* dzo = a.dz + (int64_t)k * a.dzstride + (int64_t)jr[r] * a.lddz;
       float mine = 0.f;
 #pragma unroll
@@ -217,22 +275,33 @@ __global__ __launch_bounds__(256) void head_kernel(HeadArgs a) {
   // input gradient of the output layer, masked by the ReLU of H_{L-1}
   if (a.dprev) {
 #pragma unroll
-    for (int q = 0; q < QMAX; ++q) {
-      const int i = lane + 64 * q;
-      float acc[WR];
+    for (int q = 0; q < QH; ++q) {
+      const int i = 4 * lane + 256 * (qb + q);
+      f32x4 acc[WR];
 #pragma unroll
-      for (int r = 0; r < WR; ++r) acc[r] = 0.f;
+      for (int r = 0; r < WR; ++r) acc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int c = 0; c < CMAX; ++c) {
-        const float w = Ws[c * LW + i];
+        const f32x4 w = *reinterpret_cast<const f32x4*>(Ws + c * LW + i);
 #pragma unroll
-        for (int r = 0; r < WR; ++r) acc[r] += p[r][c] * w;
+        for (int r = 0; r < WR; ++r)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[r][e] += p[r][c] * w[e];
       }
 #pragma unroll
       for (int r = 0; r < WR; ++r) {
         if (jr[r] < a.m && i < d) {
           float* dp = a.dprev + (int64_t)k * a.hstride + (int64_t)jr[r] * a.ldh;
-          dp[i] = hv[r][q] > 0.f ? acc[r] : 0.f;
+          f32x4 v;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = hv[r][q][e] > 0.f ? acc[r][e] : 0.f;
+          if (a.vec) {
+            *reinterpret_cast<f32x4*>(dp + i) = v;
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              if (i + e < d) dp[i + e] = v[e];
+          }
         }
       }
     }
@@ -249,11 +318,19 @@ __global__ __launch_bounds__(64 * HDW_WAVES) void head_dw_kernel(HeadDwArgs a) {
 }  // namespace
 
 static int head_cmax(int C) { return C <= 10 ? 10 : C <= 16 ? 16 : 32; }
-static int head_qmax(int d) { return d <= 128 ? 2 : d <= 512 ? 8 : d <= 1024 ? 16 : 32; }
+static int head_q4(int d) { return d <= 256 ? 1 : d <= 512 ? 2 : d <= 1024 ? 4 : 8; }
 
 size_t head_lds_bytes(int C, int d) {
   const int cm = head_cmax(C);
-  return ((size_t)cm * 64 * head_qmax(d) + cm) * sizeof(float);
+  return ((size_t)cm * 256 * head_q4(d) + cm) * sizeof(float);
+}
+
+// 16-byte accesses to the rows of H (and of the input gradient): d and the
+// row pitches multiples of 4 floats, the bases 16-byte aligned
+static bool head_vec(const HeadArgs& a) {
+  const auto al = [](const void* p) { return ((uintptr_t)p & 15) == 0; };
+  return a.d % 4 == 0 && a.ldh % 4 == 0 && (a.gather || a.hstride % 4 == 0) && al(a.h) &&
+         (!a.dprev || al(a.dprev));
 }
 
 template <int CM, int QM, bool EVAL>
@@ -265,17 +342,19 @@ static hipError_t head_go(const HeadArgs& a, hipStream_t s, bool prepare) {
                                hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   }
   const int blocks = a.n * ((a.m + head_rows(EVAL) - 1) / head_rows(EVAL));
-  AGN_LAUNCH((head_kernel<CM, QM, EVAL>), dim3(blocks), dim3(256), lds, s, a);
+  HeadArgs v = a;
+  v.vec = head_vec(a);
+  AGN_LAUNCH((head_kernel<CM, QM, EVAL>), dim3(blocks), dim3(256 * head_split(QM, EVAL)), lds, s, v);
   return hipGetLastError();
 }
 
 template <int CM, bool EVAL>
 static hipError_t head_dispatch_q(const HeadArgs& a, hipStream_t s, bool prepare) {
-  switch (head_qmax(a.d)) {
+  switch (head_q4(a.d)) {
+    case 1: return head_go<CM, 1, EVAL>(a, s, prepare);
     case 2: return head_go<CM, 2, EVAL>(a, s, prepare);
-    case 8: return head_go<CM, 8, EVAL>(a, s, prepare);
-    case 16: return head_go<CM, 16, EVAL>(a, s, prepare);
-    default: return head_go<CM, 32, EVAL>(a, s, prepare);
+    case 4: return head_go<CM, 4, EVAL>(a, s, prepare);
+    default: return head_go<CM, 8, EVAL>(a, s, prepare);
   }
 }
 
@@ -293,7 +372,7 @@ static hipError_t head_dispatch(const HeadArgs& a, hipStream_t s, bool prepare) 
 // on gfx950; beyond 64 KB the kernel's dynamic-LDS limit is raised first).
 bool head_prepare(int C, int d) {
   if (C > 32 || d > HEAD_DMAX) return false;
-  if (head_lds_bytes(C, d) > 160 * 1024 - 1024) return false;
+  if (head_lds_bytes(C, d) > 160 * 1024 - 2048) return false;  // (+ the kernel's static LDS)
   HeadArgs a{};
   a.C = C;
   a.d = d;

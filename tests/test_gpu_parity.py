@@ -48,6 +48,12 @@ SMALL = [
     ("many_classes", (60, 50, 40), 3, 2, 24, 0.1, 2, 300, "gauss_linear", "permutation", "fp32"),
     ("wide_hidden", (30, 2100, 10), 2, 2, 8, 0.02, 2, 64, "gauss_linear", "permutation", "fp32"),
     ("big_head_lds", (50, 2000, 12), 2, 2, 16, 0.02, 2, 96, "gauss_linear", "permutation", "fp32"),
+    # the fused output layer with each row's columns split over two waves
+    # (width > 256): rows that do not allow 16-byte accesses, and the output
+    # layer fed by the gathered data rows directly (with and without them)
+    ("head_split_unaligned", (45, 301, 10), 3, 2, 20, 0.05, 2, 200, "gauss_linear", "permutation", "fp32"),
+    ("head_split_gather", (301, 10), 2, 3, 16, 0.05, 2, 150, "gauss_linear", "permutation", "fp32"),
+    ("head_split_gather_vec", (300, 7), 2, 3, 16, 0.05, 2, 150, "sparse_teacher2", "permutation", "fp32"),
     # bf16 products (bf16 operands, float32 accumulation and master weights)
     ("bf16_ragged", (200, 130, 70, 10), 3, 3, 40, 0.05, 3, 650, "gauss_linear", "permutation", "bf16"),
     ("bf16_many_classes", (256, 300, 300, 100), 4, 2, 70, 0.01, 2, 1000, "gauss_linear", "permutation", "bf16"),
