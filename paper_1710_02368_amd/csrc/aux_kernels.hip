@@ -11,17 +11,6 @@ namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
-  return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
-  return v;
-}
-
 // Softmax cross-entropy of one mini-batch row per wave (the loss of Eq. 1).
 // loss_j = logsumexp(z_j) - z_{j,y_j};  dZ_j = (softmax(z_j) - onehot(y_j)) / m,
 // the gradient of the batch-mean loss with respect to the logits.

@@ -20,6 +20,35 @@ __device__ __forceinline__ int xcd_remap(int pid, int nblk) {
   return xcd < rem ? xcd * (q + 1) + local : rem * (q + 1) + (xcd - rem) * q + local;
 }
 
+// A data-parallel (DPP) move within each row of 16 lanes.
+template <int CTRL>
+__device__ __forceinline__ float dpp_move(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float lane_value(float v, int l) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+}
+
+// Reduction over the wave with a commutative op (every lane active): within
+// each row of 16 lanes by DPP moves (quad pairs 1<->0, 3<->2, then 2<->0,
+// 3<->1; then the two quads of each half row, i <-> 7-i; then the two
+// halves, i <-> 15-i), then the four row results in row order.  The same
+// value in every lane and on every call.
+template <typename Op>
+__device__ __forceinline__ float wave_reduce(float v, Op op) {
+  v = op(v, dpp_move<0xB1>(v));   // quad_perm(1, 0, 3, 2)
+  v = op(v, dpp_move<0x4E>(v));   // quad_perm(2, 3, 0, 1)
+  v = op(v, dpp_move<0x141>(v));  // row_half_mirror
+  v = op(v, dpp_move<0x140>(v));  // row_mirror
+  return op(op(op(lane_value(v, 0), lane_value(v, 16)), lane_value(v, 32)), lane_value(v, 48));
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  return wave_reduce(v, [](float a, float b) { return a + b; });
+}
+__device__ __forceinline__ float wave_max(float v) {
+  return wave_reduce(v, [](float a, float b) { return fmaxf(a, b); });
+}
+
 // Data-set row of row j of worker k's mini-batch at local step t.
 __device__ __forceinline__ int64_t batch_row(int64_t k, int64_t t, int64_t mb, int64_t S, int64_t j) {
   return k * S + (t * mb + j) % S;

@@ -27,27 +27,6 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int HEAD_WAVE_ROWS = 1;                  // rows a wave processes together
 constexpr int HEAD_DMAX = 2048;                     // hidden width limit
 
-template <int CTRL>
-__device__ __forceinline__ float dpp(float v) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
-}
-__device__ __forceinline__ float lane_value(float v, int l) {
-  return __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
-}
-
-// Sum over the wave (every lane active), the same value in every lane and
-// on every call: within each row of 16 lanes by data-parallel moves (quad
-// pairs 1<->0, 3<->2, then 2<->0, 3<->1; then the two quads of each half
-// row, i <-> 7-i; then the two halves, i <-> 15-i), then the four row sums
-// in row order.
-__device__ __forceinline__ float wsum(float v) {
-  v += dpp<0xB1>(v);   // quad_perm(1, 0, 3, 2)
-  v += dpp<0x4E>(v);   // quad_perm(2, 3, 0, 1)
-  v += dpp<0x141>(v);  // row_half_mirror
-  v += dpp<0x140>(v);  // row_mirror
-  return ((lane_value(v, 0) + lane_value(v, 16)) + lane_value(v, 32)) + lane_value(v, 48);
-}
-
 // Argmax order of the evaluation: a NaN beats any number, a larger value a
 // smaller one, and among equals (or NaNs) the lower class index wins.
 __device__ __forceinline__ bool beats_h(float v, int i, float bv, int bi) {
@@ -173,13 +152,13 @@ __global__ __launch_bounds__(256 * head_split(Q4, EVAL)) void head_kernel(HeadAr
 #pragma unroll
     for (int r = 0; r < WR; ++r)
 #pragma unroll
-      for (int c = 0; c < CMAX; ++c) p[r][c] = wsum(p[r][c]) + bs[c];
+      for (int c = 0; c < CMAX; ++c) p[r][c] = wave_sum(p[r][c]) + bs[c];
   } else {
     // each wave's partial logits to LDS; then both waves of a row add the
     // halves in the same order and hold the same logits
     static_assert(WR == 1, "one row per wave pair");
 #pragma unroll
-    for (int c = 0; c < CMAX; ++c) p[0][c] = wsum(p[0][c]);
+    for (int c = 0; c < CMAX; ++c) p[0][c] = wave_sum(p[0][c]);
     if (lane < CMAX) {
       float mine = 0.f;
 #pragma unroll
