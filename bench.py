@@ -70,29 +70,71 @@ COMMIT_RULES = {"agn": (True, False), "accumulated": (False, False), "agn_scaled
                 "dynsgd": (False, True)}
 
 
-def cpu_baseline(wl, X, y, orders, budget_s=12.0, adam=None, normalize=True, scaled=False):
-    """The oracle as it stands, on the host cores, over whole rounds until
-    about budget_s seconds have passed (at least one round)."""
-    from oracle import AGNOracle
+def host_cores():
+    """Cores this process may run on, and the BLAS thread count the oracle's
+    products use (set to match the cores)."""
+    cores = len(os.sched_getaffinity(0))
+    blas = None
     try:
-        from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        from threadpoolctl import threadpool_info, threadpool_limits
+        threadpool_limits(limits=cores)
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
-        threads = len(os.sched_getaffinity(0))
+        pass
+    return cores, blas
+
+
+def cpu_baseline(wl, X, y, orders, budget_s=20.0, adam=None, normalize=True, scaled=False, full=False):
+    """The oracle as it stands, on the host cores, timed on a bounded sample
+    of the workload: whole rounds while they fit in about budget_s seconds
+    (always with full=True, at least one); when one round would take longer,
+    the first workers of round 1, each running its lambda local steps, until
+    about budget_s seconds have passed (the server's commits, n float32
+    vector additions, are under 1% of an oracle round and are left out)."""
+    from oracle import AGNOracle
+    cores, blas = host_cores()
     o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, bf16=wl.dtype == "bf16", adam=adam,
                   normalize=normalize, staleness_scaled=scaled)
+    Xo = X
+    if X.dtype == np.uint16:
+        import workloads as W
+        Xo = W.f32_from_bf16_bits(X)
+    S = wl.N // wl.n
+    # one worker's local steps first: they tell whether a whole round fits
     t0 = time.perf_counter()
-    rounds = 0
-    while True:
-        o.round(X, y, orders[rounds % len(orders)])
-        rounds += 1
-        if time.perf_counter() - t0 >= budget_s:
-            break
-    dt = time.perf_counter() - t0
-    return {"value": rounds * wl.worker_samples_per_round / dt, "unit": "worker-samples/s",
-            "cores": int(threads), "kind": "oracle",
-            "sample": f"{rounds} full round(s) of {wl.name} ({rounds * wl.worker_samples_per_round} "
-                      f"worker-samples) in {dt:.1f} s, float32 storage / float64 accumulation"}
+    o._worker_round(0, Xo, y, S)
+    t1 = time.perf_counter() - t0
+    per = wl.lam * wl.m
+    if full or t1 * wl.n <= budget_s:
+        o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, bf16=wl.dtype == "bf16",
+                      adam=adam, normalize=normalize, staleness_scaled=scaled)
+        t0 = time.perf_counter()
+        rounds = 0
+        while True:
+            o.round(X, y, orders[rounds % len(orders)])
+            rounds += 1
+            if time.perf_counter() - t0 >= budget_s:
+                break
+        dt = time.perf_counter() - t0
+        samples = rounds * wl.worker_samples_per_round
+        sample = (f"{rounds} full round(s) of {wl.name} ({samples} worker-samples) in {dt:.1f} s, "
+                  "float32 storage / float64 accumulation")
+    else:
+        k, dt = 1, t1
+        while k < wl.n and dt + t1 <= budget_s:
+            t0 = time.perf_counter()
+            o._worker_round(k, Xo, y, S)
+            dt += time.perf_counter() - t0
+            k += 1
+        samples = k * per
+        sample = (f"workers 0..{k - 1} of round 1 of {wl.name}, {wl.lam} local steps each ({samples} "
+                  f"worker-samples of the round's {wl.worker_samples_per_round}) in {dt:.1f} s; float32 "
+                  "storage / float64 accumulation; the commits (under 1% of an oracle round) not timed")
+    out = {"value": samples / dt, "unit": "worker-samples/s", "cores": int(cores), "kind": "oracle",
+           "sample": sample}
+    if blas is not None:
+        out["blas_threads"] = int(blas)
+    return out
 
 
 def measure_eval(agn, g, wl, xh, yh, Xh, yh_host, reps=20, cpu=True):
@@ -132,20 +174,21 @@ def measure_eval(agn, g, wl, xh, yh, Xh, yh_host, reps=20, cpu=True):
                         "algorithmic_per_eval": flops}}
     if cpu:
         from oracle import evaluate
-        try:
-            from threadpoolctl import threadpool_info
-            threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-        except Exception:
-            threads = len(os.sched_getaffinity(0))
-        # the initial model's parameters (the library draws the same ones)
+        cores, blas = host_cores()
+        # the oracle evaluates the initial model (the library's initial
+        # parameters come from the same generator); the cost of an
+        # evaluation does not depend on the parameter values
         from oracle import he_normal_init
         params = he_normal_init(wl.dims, wl.seed)
         t0 = time.perf_counter()
         evaluate(params, Xh, yh_host, bf16=dtype == "bf16")
         ct = time.perf_counter() - t0
-        out["cpu_baseline"] = {"value": round(rows / ct, 1), "unit": "rows/s", "cores": int(threads),
+        out["cpu_baseline"] = {"value": round(rows / ct, 1), "unit": "rows/s", "cores": int(cores),
                                "kind": "oracle",
-                               "sample": f"{rows} held-out rows evaluated once in {ct:.2f} s"}
+                               "sample": f"{rows} held-out rows evaluated once in {ct:.2f} s, at the "
+                                         "initial model's parameters"}
+        if blas is not None:
+            out["cpu_baseline"]["blas_threads"] = int(blas)
     return out
 
 
@@ -260,18 +303,91 @@ def summarize_traffic(d, workload):
     print("\n".join(lines))
 
 
+MFMA_FILE = os.path.join(ROOT, "profiles", "mfma_{}.json")
+
+
+def summarize_mfma(d, workload, dtype):
+    """MFMA counter pass (rocprofv3 --pmc MfmaUtil MfmaFlopsF32 (or BF16)
+    GRBM_GUI_ACTIVE, csv output under d/) -> per kernel class: the MFMA busy
+    fraction (MfmaUtil: busy cycles of the matrix units over the dispatch's
+    active cycles times the SIMD count, averaged over the class's launches
+    weighted by their active cycles) and the MFMA flops the counters saw per
+    launch; written to profiles/mfma_<workload>.json with the digest of the
+    kernel sources, and printed as a text summary."""
+    import collections
+    import csv
+    flops_name = "MfmaFlopsBF16" if dtype == "bf16" else "MfmaFlopsF32"
+    per = collections.defaultdict(dict)
+    names = {}
+    with open(os.path.join(d, "run_counter_collection.csv")) as fh:
+        for r in csv.DictReader(fh):
+            k = r["Dispatch_Id"]
+            per[k][r["Counter_Name"]] = per[k].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+            names[k] = r["Kernel_Name"]
+    cls = collections.defaultdict(lambda: {"busy_w": 0.0, "active": 0.0, "flops": 0.0, "launches": 0})
+    kern = collections.defaultdict(lambda: {"busy_w": 0.0, "active": 0.0, "flops": 0.0, "launches": 0})
+    for k, v in per.items():
+        if "MfmaUtil" not in v or "GRBM_GUI_ACTIVE" not in v:
+            continue
+        for key, table in ((traffic_class(names[k]), cls), (names[k][:90], kern)):
+            if key is None:
+                continue
+            e = table[key]
+            e["busy_w"] += v["MfmaUtil"] / 100.0 * v["GRBM_GUI_ACTIVE"]
+            e["active"] += v["GRBM_GUI_ACTIVE"]
+            e["flops"] += v.get(flops_name, 0.0)
+            e["launches"] += 1
+    out = {"workload": workload, "kernel_source_sha256": kernel_source_digest(), "counter_flops": flops_name,
+           "classes": {}}
+    lines = [f"MFMA counters ({flops_name}, MfmaUtil = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE x SIMDs))"]
+    for c in sorted(cls):
+        e = cls[c]
+        if e["active"] <= 0:
+            continue
+        util = e["busy_w"] / e["active"]
+        fl = e["flops"] / e["launches"]
+        out["classes"][c] = {"mfma_busy": util, "mfma_flops_per_launch": fl, "launches_sampled": e["launches"]}
+        lines.append(f"class {c:9s}: MFMA busy {100 * util:6.2f} %   MFMA flops per launch {fl / 1e9:10.3f} G "
+                     f"({e['launches']} launches)")
+    for k in sorted(kern, key=lambda k: -kern[k]["active"]):
+        e = kern[k]
+        if e["active"] <= 0:
+            continue
+        lines.append(f"  {k[:80]:80s} busy {100 * e['busy_w'] / e['active']:6.2f} %  "
+                     f"{e['flops'] / e['launches'] / 1e9:9.3f} GFLOP/launch  ({e['launches']})")
+    with open(MFMA_FILE.format(workload), "w") as fh:
+        json.dump(out, fh, indent=1)
+    print("\n".join(lines))
+
+
+def stored_mfma(workload, kernel_class):
+    """The MFMA busy fraction of a kernel class from the committed counter
+    pass, or None when it was taken on other kernel sources."""
+    try:
+        with open(MFMA_FILE.format(workload)) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256") != kernel_source_digest():
+        return None
+    c = t.get("classes", {}).get(kernel_class)
+    return None if c is None else round(c["mfma_busy"], 4)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="mlp1000_n8")
+    ap.add_argument("--workload", default="mlp2000_n40")
     ap.add_argument("--optimizer", choices=["sgd", "adam"], default="sgd",
                     help="local rule: plain SGD (the paper's Eq. 1) or Adam (beta 0.9/0.999, eps 1e-8)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-eval", action="store_true",
                     help="skip the held-out evaluation (counter passes of the round's kernels alone)")
-    ap.add_argument("--cpu-budget", type=float, default=12.0)
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
+    ap.add_argument("--cpu-full-round", action="store_true",
+                    help="time the oracle over at least one whole round, however long it takes")
     ap.add_argument("--commit", choices=sorted(COMMIT_RULES), default="agn",
                     help="commit rule: agn (a / lambda, the default), accumulated (a), or either scaled by "
                          "1 / (staleness + 1) (agn_scaled, dynsgd)")
@@ -279,6 +395,9 @@ def main():
                     help="round: the AGN round (default line, with the evaluation); eval: evaluation only")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (counter calibration)")
+    ap.add_argument("--summarize-mfma", metavar="DIR",
+                    help="turn the MFMA counter pass under DIR into profiles/mfma_<workload>.json "
+                         "for --workload (no GPU needed)")
     ap.add_argument("--summarize-traffic", metavar="DIR",
                     help="turn the FETCH_SIZE / WRITE_SIZE counter passes under DIR into "
                          "profiles/traffic.json for --workload (no GPU needed)")
@@ -288,6 +407,10 @@ def main():
         return
     if args.summarize_traffic:
         summarize_traffic(args.summarize_traffic, args.workload)
+        return
+    if args.summarize_mfma:
+        import workloads as W
+        summarize_mfma(args.summarize_mfma, args.workload, W.workload(args.workload).dtype)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the multi-GPU "
@@ -401,7 +524,8 @@ def main():
         achieved = per_launch / avg_s / 1e9
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                 "frac": round(achieved / PEAK_HBM_GBS, 4)}
-    roof.update({"traffic": stored_traffic(wl.name, dominant), "kernel_class": dominant,
+    roof.update({"traffic": stored_traffic(wl.name, dominant), "counter_mfma_busy": stored_mfma(wl.name, dominant),
+                 "kernel_class": dominant,
                  "avg_launch_us": round(avg_s * 1e6, 2), "algorithmic_per_launch": per_launch,
                  "launches": dom_cnt})
     c_avg = c_ms * 1e-3 / max(c_cnt, 1)
@@ -429,7 +553,7 @@ def main():
     g.close()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, X, y, orders, budget_s=args.cpu_budget, adam=adam,
-                                           normalize=normalize, scaled=scaled)
+                                           normalize=normalize, scaled=scaled, full=args.cpu_full_round)
     print(json.dumps(out), flush=True)
 
 

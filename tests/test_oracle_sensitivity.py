@@ -56,3 +56,50 @@ def test_bf16_spread_exceeds_fp32_at_the_same_shape():
     a32, b32 = spread(dims, 128, 1, 0.005, "fp32")
     a16, b16 = spread(dims, 128, 1, 0.005, "bf16")
     assert rel_fro(b16, a16, dims)[0] > 10 * rel_fro(b32, a32, dims)[0]
+
+
+def test_fp32_round1_spread_at_784_1000_1000_10():
+    """One round of the 784-1000-1000-10 workload (n = 8, lambda = 15,
+    m = 128, its seeded data and commit order), the oracle against itself
+    with its start perturbed by 1e-7 (relative, every weight).
+
+    Measured: the central variable's weight tensors agree to about 1e-6
+    (max-norm), its two hidden bias tensors differ by 2.5e-4 and 4.0e-4 --
+    above the 1e-4 bound, below ten times it; one worker's delta (the
+    displacement (theta_lambda - theta_0) / lambda) differs by up to 8e-3 in
+    max-norm and 1.0e-3 in Frobenius norm, where a flipped ReLU derivative
+    sits undiluted.  These are the floors the full-size GPU gates on biases
+    and per-worker deltas are set against."""
+    wl = W.workload("mlp1000_n8")
+    X, y = W.make_data(wl)
+    order = W.commit_orders(wl)[0]
+    runs = []
+    for p in (0.0, 1e-7):
+        o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed)
+        if p:
+            rng = np.random.default_rng(3)
+            c = [(Wt * (1 + p * rng.standard_normal(Wt.shape)).astype(np.float32), b) for Wt, b in o.central]
+            o.central = c
+            o.workers = [[(a.copy(), b.copy()) for a, b in c] for _ in range(o.n)]
+        start = o.central_flat().astype(np.float64)
+        o.round(X, y, order)
+        disp = [(flat_params(f).astype(np.float64) - start) / wl.lam for f in o.last_finals]
+        runs.append((o.central_flat().astype(np.float64), disp))
+    (c0, d0), (c1, d1) = runs
+    w_spread, b_spread = 0.0, 0.0
+    for name, a, b in tensor_slices(wl.dims):
+        e = np.max(np.abs(c1[a:b] - c0[a:b])) / np.max(np.abs(c0[a:b]))
+        if name[0] == "W":
+            w_spread = max(w_spread, e)
+        else:
+            b_spread = max(b_spread, e)
+    assert w_spread < 1e-5, w_spread
+    assert 1e-4 < b_spread < 1e-3, b_spread
+    dmax = dfro = 0.0
+    for k in range(wl.n):
+        for name, a, b in tensor_slices(wl.dims):
+            diff = d1[k][a:b] - d0[k][a:b]
+            dmax = max(dmax, np.max(np.abs(diff)) / np.max(np.abs(d0[k][a:b])))
+            dfro = max(dfro, np.linalg.norm(diff) / np.linalg.norm(d0[k][a:b]))
+    assert 1e-3 < dmax < 5e-2, dmax
+    assert 1e-4 < dfro < 1e-2, dfro
