@@ -189,6 +189,36 @@ typedef struct {
 int agn_evaluate(agn_ctx* ctx, const agn_data* data, float* row_loss, int32_t* row_pred,
                  agn_eval_result* out);
 
+/* Allocation-free variant of agn_evaluate, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Same arguments, same results:
+ * row_loss, row_pred and the correct count as agn_evaluate gives them; the
+ * float64 mean loss may differ in its last bits when the rows are taken
+ * in smaller groups (below).  It allocates nothing, on the device or the
+ * host, and launches nothing but its kernels (no memset, no event).
+ *
+ * Its workspace is a file-scope device array of AGN_NOALLOC_SCRATCH_BYTES
+ * (16 MiB) that every device the library runs on holds until the process
+ * ends (its device address is looked up once per device by agn_create).
+ * The rows go through the forward pass as many at a time as fit in it (a
+ * multiple of 64, at most 8192): activations of the widest hidden layer
+ * twice, the logits when the output layer is not fused (C > 32 or bf16),
+ * and per-block partial sums.  AGN_EINVAL (nothing enqueued) when not even
+ * 64 rows fit, i.e. a hidden layer wider than about 32,000 units (float32)
+ * or 64,000 (bf16).  In AGN_BF16 contexts the bf16 operands of the central
+ * variable are the copy the last commit wrote for its worker's pull, so no
+ * conversion buffer is needed.
+ *
+ * Every call on one device shares that device's array and leaves its
+ * contents behind (each call overwrites what it reads): calls that overlap
+ * in time on one device -- from several contexts, streams or host threads
+ * -- race and give wrong results; serialize them.  With out == NULL the
+ * call returns after enqueueing (capturable); with out != NULL it waits for
+ * the stream and copies the totals to the host. */
+#define AGN_NOALLOC_SCRATCH_BYTES (16u << 20)
+int agn_evaluate_noalloc(agn_ctx* ctx, const agn_data* data, float* row_loss, int32_t* row_pred,
+                         agn_eval_result* out);
+
 /* Temporal efficiency E(a, b) of Eq. 4 (Section 4): the area under
  * performance curve f_a over the area under f_b, both over [0, tm] with tm
  * the minimal shared training time, min(last time of a, last time of b).

@@ -29,7 +29,7 @@ EXPORTED = [
     "agn_worker_params", "agn_debug_batch_indices", "agn_set_kernel_timing",
     "agn_kernel_timing", "agn_kernel_class_work", "agn_debug_delta", "agn_set_normalization",
     "agn_set_optimizer", "agn_evaluate", "agn_temporal_efficiency", "agn_set_staleness_scaling",
-    "agn_staleness",
+    "agn_staleness", "agn_evaluate_noalloc",
 ]
 
 
@@ -77,6 +77,7 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "agn_set_optimizer": (i32, [vp, i32, ctypes.c_float, ctypes.c_float, ctypes.c_float]),
         "agn_round": (i32, [vp, ctypes.POINTER(agn_data), ctypes.POINTER(ctypes.c_int32)]),
         "agn_evaluate": (i32, [vp, ctypes.POINTER(agn_data), vp, vp, ctypes.POINTER(agn_eval_result)]),
+        "agn_evaluate_noalloc": (i32, [vp, ctypes.POINTER(agn_data), vp, vp, ctypes.POINTER(agn_eval_result)]),
         "agn_temporal_efficiency": (i32, [ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), i64,
                                           ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), i64,
                                           ctypes.POINTER(ctypes.c_double)]),
@@ -176,6 +177,20 @@ def agn_evaluate(ctx, x, y, num_samples: int, x_dtype: int = AGN_FP32, row_loss=
     data = agn_data(x.data_ptr(), y.data_ptr(), int(num_samples), int(x_dtype))
     res = agn_eval_result()
     _check(load_library().agn_evaluate(
+        ctx, ctypes.byref(data),
+        ctypes.c_void_p(row_loss.data_ptr()) if row_loss is not None else None,
+        ctypes.c_void_p(row_pred.data_ptr()) if row_pred is not None else None,
+        ctypes.byref(res) if want_result else None), ctx)
+    return (res.mean_loss, res.accuracy, res.correct) if want_result else None
+
+
+def agn_evaluate_noalloc(ctx, x, y, num_samples: int, x_dtype: int = AGN_FP32, row_loss=None, row_pred=None,
+                         want_result: bool = True):
+    """agn_evaluate without device allocation (its workspace is the
+    library's per-device scratch array); same return convention."""
+    data = agn_data(x.data_ptr(), y.data_ptr(), int(num_samples), int(x_dtype))
+    res = agn_eval_result()
+    _check(load_library().agn_evaluate_noalloc(
         ctx, ctypes.byref(data),
         ctypes.c_void_p(row_loss.data_ptr()) if row_loss is not None else None,
         ctypes.c_void_p(row_pred.data_ptr()) if row_pred is not None else None,

@@ -22,6 +22,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -29,6 +30,12 @@
 #include "../../include/agn.h"
 
 using namespace agn;
+
+// Workspace of agn_evaluate_noalloc: one array per device, held until the
+// process ends.  In host code its name stands for a host-side shadow, not a
+// device address: every host use goes through the address that
+// hipGetSymbolAddress returns for the current device (scratch_address).
+static __device__ __align__(256) unsigned char scratch[AGN_NOALLOC_SCRATCH_BYTES];
 
 struct TimingSlot {
   int enabled = 0;
@@ -85,7 +92,10 @@ struct agn_ctx {
   double* ev_part = nullptr;           // per-block partial sums of one chunk
   double* ev_acc = nullptr;            // loss sum and correct count over all rows
   int64_t eval_N = 0;                  // rows of the last agn_evaluate call
+  unsigned char* scratch = nullptr;    // this device's scratch array (agn_evaluate_noalloc)
+  int last_committer = 0;              // worker that committed last (its pulled copy is the central variable)
   int capturing = 0;
+  int untimed = 0;                     // launch without timing events (agn_evaluate_noalloc)
   hipStream_t ls = nullptr;           // stream the launch sequence is enqueued on
   int poisoned = 0;
   std::string err;
@@ -154,7 +164,7 @@ hipError_t dalloc(agn_ctx* c, T** p, int64_t count) {
 template <class F>
 hipError_t timed(agn_ctx* c, int cls, F&& launch) {
   TimingSlot& t = c->timing[cls];
-  if (!t.enabled || c->capturing) return launch();
+  if (!t.enabled || c->capturing || c->untimed) return launch();
   if (t.used >= (1u << 15)) {
     ++t.dropped;
     return launch();
@@ -187,6 +197,26 @@ int check_ctx(agn_ctx* c) {
 int set_device(agn_ctx* c) {
   HIP_CHECK(c, hipSetDevice(c->device));
   return AGN_OK;
+}
+
+// The device address of `scratch` on device `dev` (current), looked up once
+// per device: each device holds its own copy of the array.
+std::mutex g_scratch_mu;
+std::vector<std::pair<int, unsigned char*>> g_scratch_addr;
+
+hipError_t scratch_address(int dev, unsigned char** out) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  for (const auto& e : g_scratch_addr)
+    if (e.first == dev) {
+      *out = e.second;
+      return hipSuccess;
+    }
+  void* ptr = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return e;
+  g_scratch_addr.emplace_back(dev, static_cast<unsigned char*>(ptr));
+  *out = static_cast<unsigned char*>(ptr);
+  return hipSuccess;
 }
 
 // One local step of every worker: forward, softmax cross-entropy, backward
@@ -444,21 +474,64 @@ int eval_alloc(agn_ctx* c) {
   return AGN_OK;
 }
 
-// The central variable's forward pass over data->x, EVAL_CHUNK rows at a
+// Buffers of one evaluation: activations of `chunk` rows (ping-pong, the
+// widest hidden layer), their logits (unfused output layer), the bf16
+// operands of the central variable (bf16 contexts), per-block partial sums
+// of one chunk and the float64 totals.
+struct EvalSpace {
+  void* h[2];
+  float* z;
+  const uint16_t* w16;
+  double* part;
+  double* acc;
+  int64_t chunk;
+};
+
+// Bytes of an EvalSpace for `rows` rows (each buffer 256-byte aligned), and
+// the buffers when base != nullptr.
+int64_t eval_space_bytes(const agn_ctx* c, int64_t rows, unsigned char* base, EvalSpace* ws) {
+  const bool bf = c->dtype == AGN_BF16;
+  int64_t wmax = 0;
+  for (int l = 1; l < c->L; ++l) wmax = std::max(wmax, c->lda[l]);
+  const int64_t act = bf ? 2 : 4;
+  const int64_t blocks = std::max(eval_blocks(rows), head_eval_blocks(rows));
+  int64_t off = 0;
+  auto take = [&](int64_t bytes) {
+    const int64_t at = off;
+    off += round_up(std::max<int64_t>(bytes, 1), 256);
+    return base ? base + at : nullptr;
+  };
+  unsigned char* acc = take(2 * sizeof(double));
+  unsigned char* part = take(2 * blocks * sizeof(double));
+  unsigned char* h0 = wmax > 0 ? take(rows * wmax * act) : nullptr;
+  unsigned char* h1 = wmax > 0 ? take(rows * wmax * act) : nullptr;
+  unsigned char* z = c->use_head ? nullptr : take(rows * c->lda[c->L] * 4);
+  if (ws) {
+    ws->h[0] = h0;
+    ws->h[1] = h1;
+    ws->z = reinterpret_cast<float*>(z);
+    ws->part = reinterpret_cast<double*>(part);
+    ws->acc = reinterpret_cast<double*>(acc);
+    ws->chunk = rows;
+    ws->w16 = nullptr;
+  }
+  return off;
+}
+
+// The central variable's forward pass over data->x, ws.chunk rows at a
 // time: the hidden layers' products (bias + ReLU), then either the fused
 // output-layer kernel (logits, loss, prediction) or the logits product and
-// the per-row kernel; per-chunk partial sums are folded into ev_acc in row
+// the per-row kernel; per-chunk partial sums are folded into ws.acc in row
 // order.
-int enqueue_eval(agn_ctx* c, const agn_data* d, float* row_loss, int32_t* row_pred) {
+int enqueue_eval(agn_ctx* c, const agn_data* d, float* row_loss, int32_t* row_pred, const EvalSpace& ws) {
   const int L = c->L;
   const bool bf = c->dtype == AGN_BF16;
   const int64_t N = d->num_samples, d0 = c->dims[0];
   const int64_t xes = bf ? 2 : 4;
-  if (bf) HIP_CHECK(c, launch_copy_bf16(c->central, c->ev_w16, c->P_pad, c->ls));
   const Gather rows_as_stored{c->round_dev, c->lam, 0, c->m, 1};  // (no gathered operand)
   const int products = c->use_head ? L - 1 : L;
-  for (int64_t r0 = 0; r0 < N; r0 += EVAL_CHUNK) {
-    const int32_t rows = (int32_t)std::min(EVAL_CHUNK, N - r0);
+  for (int64_t r0 = 0; r0 < N; r0 += ws.chunk) {
+    const int32_t rows = (int32_t)std::min(ws.chunk, N - r0);
     const void* x = static_cast<const char*>(d->x) + r0 * d0 * xes;
     const int x_vec = (d0 % (bf ? 8 : 4) == 0) && ((uintptr_t)x % 16 == 0);
     for (int l = 0; l < products; ++l) {
@@ -467,12 +540,12 @@ int enqueue_eval(agn_ctx* c, const agn_data* d, float* row_loss, int32_t* row_pr
       g.N = c->dims[l + 1];
       g.K = c->dims[l];
       g.batch = 1;
-      g.a = l == 0 ? Operand{x, d0, 0, 0, x_vec} : Operand{c->ev_h[(l - 1) & 1], c->lda[l], 0, 0, 1};
-      g.b = bf ? Operand{c->ev_w16 + c->woff[l], c->ldw[l], 0, 0, 1}
+      g.a = l == 0 ? Operand{x, d0, 0, 0, x_vec} : Operand{ws.h[(l - 1) & 1], c->lda[l], 0, 0, 1};
+      g.b = bf ? Operand{ws.w16 + c->woff[l], c->ldw[l], 0, 0, 1}
                : Operand{c->central + c->woff[l], c->ldw[l], 0, 0, 1};
       g.g = rows_as_stored;
       g.epi = l < L - 1 ? EPI_FWD_RELU : EPI_FWD_LINEAR;
-      g.out = l < L - 1 ? c->ev_h[l & 1] : (void*)c->ev_z;
+      g.out = l < L - 1 ? ws.h[l & 1] : (void*)ws.z;
       g.ldo = c->lda[l + 1];
       g.ostride = 0;
       g.bias = c->central + c->boff[l];
@@ -485,7 +558,7 @@ int enqueue_eval(agn_ctx* c, const agn_data* d, float* row_loss, int32_t* row_pr
     int64_t blocks = 0;
     if (c->use_head) {  // fused output layer (float32, few classes)
       HeadArgs h{};
-      h.h = L == 1 ? static_cast<const float*>(x) : static_cast<const float*>(c->ev_h[(L - 2) & 1]);
+      h.h = L == 1 ? static_cast<const float*>(x) : static_cast<const float*>(ws.h[(L - 2) & 1]);
       h.ldh = L == 1 ? d0 : c->lda[L - 1];
       h.hstride = 0;
       h.gather = 0;
@@ -501,23 +574,23 @@ int enqueue_eval(agn_ctx* c, const agn_data* d, float* row_loss, int32_t* row_pr
       h.C = c->dims[L];
       h.row_loss = row_loss ? row_loss + r0 : nullptr;
       h.row_pred = row_pred ? row_pred + r0 : nullptr;
-      h.part = c->ev_part;
+      h.part = ws.part;
       HIP_CHECK(c, timed(c, AGN_K_EVAL, [&] { return launch_head_eval(h, c->ls); }));
       blocks = head_eval_blocks(rows);
     } else {
       EvalArgs e{};
-      e.z = c->ev_z;
+      e.z = ws.z;
       e.ldz = c->lda[L];
       e.y = d->y + r0;
       e.rows = rows;
       e.C = c->dims[L];
       e.row_loss = row_loss ? row_loss + r0 : nullptr;
       e.row_pred = row_pred ? row_pred + r0 : nullptr;
-      e.part = c->ev_part;
+      e.part = ws.part;
       HIP_CHECK(c, launch_eval_rows(e, c->ls));
       blocks = eval_blocks(rows);
     }
-    HIP_CHECK(c, launch_eval_reduce(c->ev_part, blocks, c->ev_acc, r0 == 0, c->ls));
+    HIP_CHECK(c, launch_eval_reduce(ws.part, blocks, ws.acc, r0 == 0, c->ls));
   }
   return AGN_OK;
 }
@@ -531,6 +604,21 @@ bool te_curve_ok(const double* t, const double* f, int64_t n) {
     if (!std::isfinite(t[i]) || !std::isfinite(f[i]) || (i > 0 && !(t[i] > t[i - 1]))) return false;
   return true;
 }
+
+// Copy an evaluation's totals to the host (when out is not NULL).
+int eval_result(agn_ctx* c, const EvalSpace& ws, int64_t N, agn_eval_result* out) {
+  if (!out) return AGN_OK;
+  double acc[2] = {0.0, 0.0};
+  HIP_CHECK(c, hipMemcpyAsync(acc, ws.acc, sizeof acc, hipMemcpyDeviceToHost, c->stream));
+  HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  out->mean_loss = acc[0] / (double)N;
+  out->correct = (int64_t)acc[1];
+  out->accuracy = (double)out->correct / (double)N;
+  return AGN_OK;
+}
+
+// agn_evaluate_noalloc evaluates at least this many rows per forward pass
+constexpr int64_t NOALLOC_MIN_ROWS = 64;
 
 double te_area(const double* t, const double* f, int64_t n, double tm) {
   double area = 0.0;
@@ -607,6 +695,11 @@ int agn_create(const agn_shapes* shapes, int32_t n, int32_t lambda, float eta, u
     return fail(nullptr, code, msg);
   };
   if (hipGetDevice(&c->device) != hipSuccess) return bail(AGN_EHIP, "no HIP device");
+  {
+    const hipError_t e = scratch_address(c->device, &c->scratch);
+    if (e != hipSuccess)
+      return bail(AGN_EHIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+  }
   c->use_head = c->dtype == AGN_FP32 && head_prepare(c->dims[L], c->dims[L - 1]);
   if (hipStreamCreateWithFlags(&c->cap_stream, hipStreamNonBlocking) != hipSuccess)
     return bail(AGN_EHIP, "hipStreamCreate failed");
@@ -786,6 +879,7 @@ int agn_round(agn_ctx* c, const agn_data* d, const int32_t* order) {
     HIP_CHECK(c, hipGraphLaunch(c->graph_exec, c->stream));
   }
   c->N_fixed = d->num_samples;
+  c->last_committer = order[c->n - 1];
   ++c->rounds;
   for (int j = 0; j < c->n; ++j) c->pulled_version[order[j]] = c->version + j + 1;
   c->version += c->n;
@@ -822,17 +916,43 @@ int agn_evaluate(agn_ctx* c, const agn_data* d, float* row_loss, int32_t* row_pr
   if (int r = set_device(c)) return r;
   if (int r = eval_alloc(c)) return r;
   c->ls = c->stream;
-  if (int r = enqueue_eval(c, d, row_loss, row_pred)) return r;
+  const EvalSpace ws{{c->ev_h[0], c->ev_h[1]}, c->ev_z, c->ev_w16, c->ev_part, c->ev_acc, EVAL_CHUNK};
+  if (c->dtype == AGN_BF16) HIP_CHECK(c, launch_copy_bf16(c->central, c->ev_w16, c->P_pad, c->ls));
+  if (int r = enqueue_eval(c, d, row_loss, row_pred, ws)) return r;
   c->eval_N = d->num_samples;
-  if (out) {
-    double acc[2] = {0.0, 0.0};
-    HIP_CHECK(c, hipMemcpyAsync(acc, c->ev_acc, sizeof acc, hipMemcpyDeviceToHost, c->stream));
-    HIP_CHECK(c, hipStreamSynchronize(c->stream));
-    out->mean_loss = acc[0] / (double)d->num_samples;
-    out->correct = (int64_t)acc[1];
-    out->accuracy = (double)out->correct / (double)d->num_samples;
-  }
-  return AGN_OK;
+  return eval_result(c, ws, d->num_samples, out);
+}
+
+int agn_evaluate_noalloc(agn_ctx* c, const agn_data* d, float* row_loss, int32_t* row_pred,
+                         agn_eval_result* out) {
+  if (int r = check_ctx(c)) return r;
+  if (!d || !d->x || !d->y) return fail(c, AGN_EINVAL, "data, data->x and data->y must be non-NULL");
+  if (d->x_dtype != (c->dtype == AGN_BF16 ? 1 : 0))
+    return fail(c, AGN_EINVAL, "x_dtype must be 1 for AGN_BF16 contexts and 0 otherwise");
+  if (d->num_samples < 1) return fail(c, AGN_EINVAL, "num_samples must be >= 1");
+  // the most rows per forward pass (a multiple of 64, at most the
+  // allocating path's 8192) whose buffers fit in the scratch array
+  int64_t rows = EVAL_CHUNK;
+  while (rows >= NOALLOC_MIN_ROWS && eval_space_bytes(c, rows, nullptr, nullptr) > (int64_t)AGN_NOALLOC_SCRATCH_BYTES)
+    rows -= NOALLOC_MIN_ROWS;
+  if (rows < NOALLOC_MIN_ROWS)
+    return fail(c, AGN_EINVAL, "the evaluation buffers of 64 rows of this model exceed the " +
+                                   std::to_string(AGN_NOALLOC_SCRATCH_BYTES) +
+                                   "-byte scratch array of agn_evaluate_noalloc (use agn_evaluate)");
+  if (int r = set_device(c)) return r;
+  EvalSpace ws{};
+  eval_space_bytes(c, rows, c->scratch, &ws);
+  // bf16 operands of the central variable: the bf16 copy that the last
+  // commit wrote for the last committer's pull (before the first round,
+  // and after agn_set_central, every worker's copy is the central one)
+  if (c->dtype == AGN_BF16) ws.w16 = c->snap16 + (int64_t)c->last_committer * c->P_pad;
+  c->ls = c->stream;
+  c->untimed = 1;
+  const int r = enqueue_eval(c, d, row_loss, row_pred, ws);
+  c->untimed = 0;
+  if (r) return r;
+  c->eval_N = d->num_samples;
+  return eval_result(c, ws, d->num_samples, out);
 }
 
 int agn_temporal_efficiency(const double* t_a, const double* f_a, int64_t n_a, const double* t_b,
