@@ -10,6 +10,7 @@ namespace agn {
 namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 // Softmax cross-entropy of one mini-batch row per wave (the loss of Eq. 1).
 // loss_j = logsumexp(z_j) - z_{j,y_j};  dZ_j = (softmax(z_j) - onehot(y_j)) / m,
@@ -47,59 +48,78 @@ __global__ __launch_bounds__(256) void softmax_ce_kernel(SoftmaxArgs a) {
 }
 
 // Normalize + commit + pull (Eq. 2; Algorithm 1, Commit and Pull).
-// Each thread owns 4 consecutive parameters.  The deltas already carry the
-// 1/lambda normalization (stored by the last local step).  In commit order
-// j = 0..n-1, worker k = order[j]:  c <- c + delta_k;  pulled_k <- c.
-// Finally central <- c.  Elements are independent, so the sequential order
-// per element is exact and needs no atomics.  SCALED: c <- c + scale[j] *
-// delta_k, the staleness factor of the j-th commit (the DynSGD comparison
-// of Section 4).
-__device__ __forceinline__ void store_bf16x4(uint16_t* base, int64_t i4, f32x4 c) {
-  uint2 h;
+// The deltas already carry the 1/lambda normalization (stored by the last
+// local step).  In commit order j = 0..n-1, worker k = order[j]:
+// c <- c + delta_k;  pulled_k <- c.  Finally central <- c.  Elements are
+// independent, so the sequential order per element is exact and needs no
+// atomics.  SCALED: c <- c + scale[j] * delta_k, the staleness factor of
+// the j-th commit (the DynSGD comparison of Section 4).
+//
+// Each wave owns EPT runs of 64 float4 (a contiguous 1 KB run of every
+// stream per float4 a lane holds), and loads the deltas of CH workers before
+// adding and storing them.  The commit reads n+1 and writes n+1 streams at
+// once; longer runs per stream and fewer streams in flight keep the HBM
+// pages open longer.  NT: streaming stores of the pulled copies and the
+// central variable, for rounds whose buffers exceed the last-level cache.
+__device__ __forceinline__ u32x2 bf16x4(f32x4 c) {
+  u32x2 h;
   h.x = (uint32_t)f32_to_bf16_rne(c.x) | ((uint32_t)f32_to_bf16_rne(c.y) << 16);
   h.y = (uint32_t)f32_to_bf16_rne(c.z) | ((uint32_t)f32_to_bf16_rne(c.w) << 16);
-  reinterpret_cast<uint2*>(base)[i4] = h;
+  return h;
 }
 
-template <bool SCALED>
+template <bool NT, class T>
+__device__ __forceinline__ void put(T* p, T v) {
+  if (NT)
+    __builtin_nontemporal_store(v, p);
+  else
+    *p = v;
+}
+
+template <bool SCALED, int EPT, int CH, bool NT>
 __global__ __launch_bounds__(256) void commit_kernel(CommitArgs a) {
-  const int64_t e4 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int64_t wave = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int64_t n4 = a.count / 4, ps4 = a.pstride / 4;
-  if (e4 < n4) {
-    f32x4* central = reinterpret_cast<f32x4*>(a.central);
-    f32x4* snap = reinterpret_cast<f32x4*>(a.snap);
-    const f32x4* delta = reinterpret_cast<const f32x4*>(a.delta);
-    f32x4 c = central[e4];
-    int j = 0;
-    for (; j + 8 <= a.n; j += 8) {
-      int kk[8];
-      f32x4 d[8];
+  const int64_t e0 = wave * 64 * EPT + lane;  // float4 u of this lane: e0 + 64u
+  f32x4* __restrict__ central = reinterpret_cast<f32x4*>(a.central);
+  f32x4* __restrict__ snap = reinterpret_cast<f32x4*>(a.snap);
+  u32x2* __restrict__ snap16 = reinterpret_cast<u32x2*>(a.snap16);
+  const f32x4* __restrict__ delta = reinterpret_cast<const f32x4*>(a.delta);
+  f32x4 c[EPT];
+  bool ok[EPT];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        kk[u] = a.order[j + u];
-        d[u] = __builtin_nontemporal_load(&delta[(int64_t)kk[u] * ps4 + e4]);
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        if (SCALED)
-          c += a.scale[j + u] * d[u];
-        else
-          c += d[u];
-        snap[(int64_t)kk[u] * ps4 + e4] = c;
-        if (a.snap16) store_bf16x4(a.snap16, (int64_t)kk[u] * ps4 + e4, c);
-      }
-    }
-    for (; j < a.n; ++j) {
-      const int k = a.order[j];
-      if (SCALED)
-        c += a.scale[j] * __builtin_nontemporal_load(&delta[(int64_t)k * ps4 + e4]);
-      else
-        c += __builtin_nontemporal_load(&delta[(int64_t)k * ps4 + e4]);
-      snap[(int64_t)k * ps4 + e4] = c;
-      if (a.snap16) store_bf16x4(a.snap16, (int64_t)k * ps4 + e4, c);
-    }
-    central[e4] = c;
+  for (int u = 0; u < EPT; ++u) {
+    ok[u] = e0 + 64 * u < n4;
+    c[u] = ok[u] ? __builtin_nontemporal_load(&central[e0 + 64 * u]) : f32x4{0.f, 0.f, 0.f, 0.f};
   }
+  for (int j = 0; j < a.n; j += CH) {
+    f32x4 d[CH][EPT];
+    int64_t ko[CH];  // worker offset of the commit (-1 past the end)
+#pragma unroll
+    for (int v = 0; v < CH; ++v) {
+      ko[v] = j + v < a.n ? (int64_t)a.order[j + v] * ps4 : -1;
+#pragma unroll
+      for (int u = 0; u < EPT; ++u)
+        if (ko[v] >= 0 && ok[u]) d[v][u] = __builtin_nontemporal_load(&delta[ko[v] + e0 + 64 * u]);
+    }
+#pragma unroll
+    for (int v = 0; v < CH; ++v)
+#pragma unroll
+      for (int u = 0; u < EPT; ++u)
+        if (ko[v] >= 0 && ok[u]) {
+          if (SCALED)
+            c[u] += a.scale[j + v] * d[v][u];
+          else
+            c[u] += d[v][u];
+          const int64_t e = ko[v] + e0 + 64 * u;
+          put<NT>(&snap[e], c[u]);
+          if (snap16) put<NT>(&snap16[e], bf16x4(c[u]));
+        }
+  }
+#pragma unroll
+  for (int u = 0; u < EPT; ++u)
+    if (ok[u]) put<NT>(&central[e0 + 64 * u], c[u]);
   if (blockIdx.x == 0 && threadIdx.x == 0) *a.round += 1;
 }
 
@@ -267,13 +287,24 @@ hipError_t launch_softmax_ce(const SoftmaxArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_commit(const CommitArgs& a, hipStream_t s) {
+// Commits whose traffic exceeds this stream from HBM (the last-level
+// cache of MI355X is 256 MB): longer runs per wave and streaming stores
+constexpr double kCommitStreamBytes = 256.0 * 1024 * 1024;
+
+template <bool SCALED, int EPT, int CH, bool NT>
+hipError_t commit_go(const CommitArgs& a, hipStream_t s) {
   const int64_t n4 = a.count / 4;
-  if (a.scale)
-    AGN_LAUNCH(commit_kernel<true>, dim3(blocks_for(n4 > 0 ? n4 : 1, 256)), dim3(256), 0, s, a);
-  else
-    AGN_LAUNCH(commit_kernel<false>, dim3(blocks_for(n4 > 0 ? n4 : 1, 256)), dim3(256), 0, s, a);
+  const int64_t waves = (n4 + 64 * EPT - 1) / (64 * EPT);
+  AGN_LAUNCH((commit_kernel<SCALED, EPT, CH, NT>), dim3(blocks_for(waves > 0 ? waves : 1, 4)), dim3(256), 0, s, a);
   return hipGetLastError();
+}
+
+hipError_t launch_commit(const CommitArgs& a, hipStream_t s) {
+  const double bytes = (8.0 + (a.snap16 ? 2.0 : 0.0)) * (double)(a.n + 1) * (double)a.count;
+  const bool stream = bytes > kCommitStreamBytes;
+  if (a.scale)
+    return stream ? commit_go<true, 2, 2, true>(a, s) : commit_go<true, 1, 8, false>(a, s);
+  return stream ? commit_go<false, 2, 2, true>(a, s) : commit_go<false, 1, 8, false>(a, s);
 }
 
 hipError_t launch_pack(const PackArgs& pa, const float* padded, float* packed, hipStream_t s) {
