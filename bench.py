@@ -311,30 +311,31 @@ def summarize_mfma(d, workload, dtype):
     GRBM_GUI_ACTIVE, csv output under d/) -> per kernel class: the MFMA busy
     fraction (MfmaUtil: busy cycles of the matrix units over the dispatch's
     active cycles times the SIMD count, averaged over the class's launches
-    weighted by their active cycles) and the MFMA flops the counters saw per
-    launch; written to profiles/mfma_<workload>.json with the digest of the
+    weighted by their durations) and the MFMA flops the counters saw per
+    launch (with the achieved rate over the launches' durations); written to profiles/mfma_<workload>.json with the digest of the
     kernel sources, and printed as a text summary."""
     import collections
     import csv
     flops_name = "MfmaFlopsBF16" if dtype == "bf16" else "MfmaFlopsF32"
     per = collections.defaultdict(dict)
-    names = {}
+    names, dur = {}, {}
     with open(os.path.join(d, "run_counter_collection.csv")) as fh:
         for r in csv.DictReader(fh):
             k = r["Dispatch_Id"]
             per[k][r["Counter_Name"]] = per[k].get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
             names[k] = r["Kernel_Name"]
+            dur[k] = (float(r["End_Timestamp"]) - float(r["Start_Timestamp"])) * 1e-9
     cls = collections.defaultdict(lambda: {"busy_w": 0.0, "active": 0.0, "flops": 0.0, "launches": 0})
     kern = collections.defaultdict(lambda: {"busy_w": 0.0, "active": 0.0, "flops": 0.0, "launches": 0})
     for k, v in per.items():
-        if "MfmaUtil" not in v or "GRBM_GUI_ACTIVE" not in v:
+        if "MfmaUtil" not in v or dur[k] <= 0:
             continue
         for key, table in ((traffic_class(names[k]), cls), (names[k][:90], kern)):
             if key is None:
                 continue
             e = table[key]
-            e["busy_w"] += v["MfmaUtil"] / 100.0 * v["GRBM_GUI_ACTIVE"]
-            e["active"] += v["GRBM_GUI_ACTIVE"]
+            e["busy_w"] += v["MfmaUtil"] / 100.0 * dur[k]
+            e["active"] += dur[k]
             e["flops"] += v.get(flops_name, 0.0)
             e["launches"] += 1
     out = {"workload": workload, "kernel_source_sha256": kernel_source_digest(), "counter_flops": flops_name,
@@ -346,9 +347,11 @@ def summarize_mfma(d, workload, dtype):
             continue
         util = e["busy_w"] / e["active"]
         fl = e["flops"] / e["launches"]
-        out["classes"][c] = {"mfma_busy": util, "mfma_flops_per_launch": fl, "launches_sampled": e["launches"]}
+        rate = e["flops"] / e["active"] / 1e12
+        out["classes"][c] = {"mfma_busy": util, "mfma_flops_per_launch": fl, "counter_tflops": rate,
+                             "launches_sampled": e["launches"]}
         lines.append(f"class {c:9s}: MFMA busy {100 * util:6.2f} %   MFMA flops per launch {fl / 1e9:10.3f} G "
-                     f"({e['launches']} launches)")
+                     f"= {rate:7.2f} TFLOP/s over the launches' durations ({e['launches']} launches)")
     for k in sorted(kern, key=lambda k: -kern[k]["active"]):
         e = kern[k]
         if e["active"] <= 0:
