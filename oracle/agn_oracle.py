@@ -63,7 +63,7 @@ import numpy as np
 
 __all__ = [
     "splitmix64", "he_normal_init", "bf16_round", "batch_indices",
-    "loss_and_grads", "forward", "evaluate", "AGNOracle", "flat_params", "unflat_params",
+    "loss_and_grads", "forward", "evaluate", "AGNOracle", "flat_params", "unflat_params", "near_zero_units",
 ]
 
 _GAMMA = np.uint64(0x9E3779B97F4A7C15)
@@ -221,6 +221,28 @@ def loss_and_grads(params, xb: np.ndarray, yb: np.ndarray, prec: _Prec):
     return loss, grads
 
 
+def near_zero_units(params, xb: np.ndarray, prec: _Prec, rel: float = 1e-6):
+    """Diagnostic for the parity tests, not part of the method: per hidden
+    layer (H_1 .. H_{L-1}) the units whose pre-activation, for some row of
+    the batch, lies within rel times the sum of the magnitudes of its terms
+    of zero.  There a float32 sum taken in another order can land on the
+    other side of zero and flip the ReLU derivative (a step at zero), which
+    changes that unit's row of the layer's weight gradient and its bias
+    gradient by one sample's whole contribution.  The forward pass is the
+    one ``forward`` computes."""
+    L = len(params)
+    H = prec.op(np.asarray(xb, dtype=prec.dtype))
+    out = []
+    for l in range(L - 1):
+        W, b = params[l]
+        Wo = prec.op(W)
+        z = prec.mm(H, Wo.T) + b
+        scale = prec.mm(np.abs(H), np.abs(Wo).T) + np.abs(np.asarray(b, dtype=np.float64))
+        out.append(np.flatnonzero((np.abs(z) <= rel * scale).any(axis=0)))
+        H = prec.op(np.maximum(prec.st(z), 0))
+    return out
+
+
 # ---------------------------------------------------------------------------
 # Evaluation of a model over a labelled set (Section 4: the training and
 # validation accuracy of the central variable, the f(t) of Eq. 4)
@@ -325,6 +347,11 @@ class AGNOracle:
         self.staleness: List[List[int]] = []   # per round, in commit order
         self.last_loss = None
         self.last_deltas = None
+        # diagnostic for the parity tests (no effect on the arithmetic): when
+        # set, round() records per worker the hidden units near a ReLU flip
+        # (near_zero_units) over the worker's local steps in last_near
+        self.record_near = False
+        self.last_near = None
 
     # -- one worker's lambda local steps (Algorithm 1, inner loop + normalization)
     def _worker_round(self, k, X, y, S):
@@ -332,9 +359,13 @@ class AGNOracle:
         theta = [(W.copy(), b.copy()) for W, b in self.workers[k]]
         a = [(np.zeros_like(W), np.zeros_like(b)) for W, b in theta]
         losses = []
+        self._near = [set() for _ in range(len(theta) - 1)]
         for i in range(self.lam):
             t = self.r * self.lam + i
             idx = batch_indices(k, t, self.m, S)           # FetchNextMiniBatch
+            if self.record_near:
+                for acc, units in zip(self._near, near_zero_units(theta, X[idx], self.prec)):
+                    acc.update(int(u) for u in units)
             loss, grads = loss_and_grads(theta, X[idx], y[idx], self.prec)
             losses.append(loss)
             new_theta, new_a = [], []
@@ -382,12 +413,13 @@ class AGNOracle:
             X = (X.astype(np.uint32) << np.uint32(16)).view(np.float32)
         y = np.asarray(y)
         S = X.shape[0] // self.n
-        deltas, losses, finals = [], [], []
+        deltas, losses, finals, near = [], [], [], []
         for k in range(self.n):
             a, loss, theta_fin = self._worker_round(k, X, y, S)
             deltas.append(a)
             losses.append(loss)
             finals.append(theta_fin)
+            near.append([np.array(sorted(u), dtype=np.int64) for u in self._near])
         st = self.prec.st
         stale = []
         for k in order:
@@ -412,6 +444,7 @@ class AGNOracle:
         self.last_loss = np.array(losses, dtype=np.float32)
         self.last_deltas = deltas
         self.last_finals = finals
+        self.last_near = near if self.record_near else None
         self.r += 1
 
     # -- views

@@ -10,20 +10,31 @@ Gates (the stated bounds: float32 1e-4 after round 1 and 1e-3 after the
 last round, bf16 2e-2):
 * central variable and every pulled copy: vec and every weight tensor in
   max-norm at the bound; every bias tensor in max-norm at BIAS_FACTOR times
-  the bound.  Biases start at zero, so after a round a bias tensor holds
-  only the sum of the deltas; a ReLU derivative flipped by a rounding-level
-  difference (the derivative is a step at zero) shows there undiluted.  The
-  oracle against itself, its start perturbed by 1e-7, differs by 2.5e-4 and
-  4.0e-4 in the two hidden bias tensors after one round of the n = 8
-  workload, while its weights agree to 1.3e-6
+  the bound (round 1's pulled copies: PULLED_BIAS).  Biases start at zero,
+  so after a round a bias tensor holds only the sum of the deltas; a ReLU
+  derivative flipped by a rounding-level difference (the derivative is a
+  step at zero) shows there undiluted.  The oracle against itself, its
+  start perturbed by 1e-7, differs by 2.5e-4 and 4.0e-4 in the two hidden
+  bias tensors after one round of the n = 8 workload, while its weights
+  agree to 1.3e-6
   (test_oracle_sensitivity.py::test_fp32_round1_spread_at_784_1000_1000_10).
 * every worker's committed delta after round 1, against the oracle's
   displacement (theta_lambda - theta_0) / lambda: Frobenius DELTA_FRO and
-  max-norm DELTA_MAX.  Nothing dilutes a flipped derivative in one worker's
-  delta: the same pinned oracle run differs by up to 8e-3 (max-norm) and
-  1.0e-3 (Frobenius) there.  In bf16 every product operand is rounded to 8
-  bits and a rounding-level change cascades through the layers (percent
-  level after one step, pinned in the same file).
+  max-norm DELTA_MAX, leaving out the rows of units whose pre-activation
+  came within 1e-6 (relative to the sum of its terms' magnitudes) of zero
+  in the worker's local steps (the oracle records them).  A flip there
+  changes the unit's row of the weight delta by a whole sample's
+  contribution (measured on the GPU: 11 % of a delta's largest entry in one
+  worker of a 64-512-768-512-10 case, 1.1e-4 with its one flagged row left
+  out); what it does to the rest stays in the gates, and over many local
+  steps it does more: the changed weights change every later step.  Pinned
+  oracle runs (test_oracle_sensitivity.py): at 784-1000-1000-10 (lambda =
+  15) 8e-3 raw and 1.8e-3 with the flagged rows left out in the worker with
+  the flip, 6e-5 in the others; at 784-2000x3-10 (lambda = 30) up to 1.4e-2
+  with the rows left out in six of the forty workers.
+  In bf16 every product operand is rounded to 8 bits and a rounding-level
+  change cascades through the layers (percent level after one step, pinned
+  in the same file).
 * the commit itself, bit-exact: every pulled copy and the central variable
   equal the float32 prefix sums, in commit order, of the deltas the GPU
   stored, over the central variable the round started from (Eq. 2; each
@@ -55,6 +66,11 @@ TOL = {"fp32": (1e-4, 1e-3), "bf16": (2e-2, 2e-2)}
 BIAS_FACTOR = {"fp32": 10.0, "bf16": 1.0}
 DELTA_FRO = {"fp32": 1e-2, "bf16": 1e-1}
 DELTA_MAX = {"fp32": 5e-2, "bf16": 5e-1}
+# round 1: the biases of the j-th pulled copy are the sum of the first j
+# deltas' biases, so a flipped derivative in an early committer shows there
+# undiluted (the largest bias footprint of a flip measured on the GPU is
+# 3.8e-2 of the tensor's largest entry)
+PULLED_BIAS = {"fp32": 1e-1, "bf16": 5e-1}
 
 _DATA = {}
 
@@ -108,13 +124,36 @@ def check_params(got, ref, dims, tol, bias_bound, label):
     return errs, vec
 
 
-def check_delta(got, disp, dims, dtype, label):
-    errs, _ = tensor_errors(got, disp, dims)
-    worst_m = max(e[1] for e in errs)
-    worst_f = max(e[2] for e in errs)
-    print(f"{label}: delta max {worst_m:.2e} fro {worst_f:.2e} | {fmt(errs)}", flush=True)
-    assert worst_f <= DELTA_FRO[dtype], (label, errs)
-    assert worst_m <= DELTA_MAX[dtype], (label, errs)
+def check_delta(got, disp, dims, dtype, label, near=None):
+    """One worker's delta against the oracle's displacement, per tensor.
+    near: per hidden layer the units the oracle found within rounding
+    distance of a ReLU flip over the worker's local steps (near_zero_units);
+    their rows of the weight delta below them and their bias elements are
+    the direct footprint of a flip and are left out of the gated norms (the
+    raw max-norm is printed)."""
+    got = np.asarray(got, dtype=np.float64)
+    L = len(dims) - 1
+    worst_m = worst_f = raw = 0.0
+    parts = []
+    for name, a, b in tensor_slices(dims):
+        l = int(name[1:])
+        g, o = got[a:b], disp[a:b]
+        d = np.abs(g - o).reshape(dims[l + 1], -1)
+        ref = np.abs(o).reshape(dims[l + 1], -1)
+        keep = np.ones(dims[l + 1], dtype=bool)
+        if near is not None and l < L - 1:
+            keep[near[l]] = False
+        mx = max(np.max(ref), 1e-300)
+        m = np.max(d[keep]) / mx if keep.any() else 0.0
+        f = np.linalg.norm(d[keep]) / max(np.linalg.norm(ref[keep]), 1e-300) if keep.any() else 0.0
+        r = np.max(d) / mx
+        worst_m, worst_f, raw = max(worst_m, m), max(worst_f, f), max(raw, r)
+        parts.append(f"{name} {m:.1e}/{f:.1e}" + (f" ({int((~keep).sum())} rows near a flip, raw {r:.1e})"
+                                                   if not keep.all() else ""))
+    print(f"{label}: delta max {worst_m:.2e} fro {worst_f:.2e} (raw max {raw:.2e}) | " + "  ".join(parts),
+          flush=True)
+    assert worst_f <= DELTA_FRO[dtype], (label, parts)
+    assert worst_m <= DELTA_MAX[dtype], (label, parts)
     return worst_m, worst_f
 
 
@@ -146,18 +185,18 @@ def round1_against_live_oracle(g, o, wl, X, y, xd, yd, order):
     gpull = [g.worker_params(k).cpu().numpy() for k in range(wl.n)]
     gloss = g.loss().cpu().numpy()
     check_commit_prefix_sums(start, gdel, gpull, gc, order, f"{wl.name} round 1")
+    o.record_near = True
     o.round(X, y, order)
+    o.record_near = False
     np.testing.assert_allclose(gloss, o.last_loss, rtol=1e-4 if dtype == "fp32" else 2e-2)
     check_params(gc, o.central_flat(), wl.dims, tol, BIAS_FACTOR[dtype] * tol, f"{wl.name} round 1 central")
     worst = [0.0, 0.0]
     s64 = o_start.astype(np.float64)
     for k in range(wl.n):
         disp = (flat_params(o.last_finals[k]).astype(np.float64) - s64) / (wl.lam if o.normalize else 1.0)
-        m, f = check_delta(gdel[k], disp, wl.dims, dtype, f"{wl.name} round 1 worker {k}")
+        m, f = check_delta(gdel[k], disp, wl.dims, dtype, f"{wl.name} round 1 worker {k}", o.last_near[k])
         worst = [max(worst[0], m), max(worst[1], f)]
-        # (the biases of the j-th pulled copy are the sum of the first j
-        # deltas: the first holds one delta's, gated as deltas are)
-        check_params(gpull[k], o.worker_flat(k), wl.dims, tol, DELTA_MAX[dtype],
+        check_params(gpull[k], o.worker_flat(k), wl.dims, tol, PULLED_BIAS[dtype],
                      f"{wl.name} round 1 pulled copy {k}")
     print(f"{wl.name} round 1: worst delta max {worst[0]:.2e} fro {worst[1]:.2e} over {wl.n} workers",
           flush=True)

@@ -646,3 +646,24 @@ def test_staleness_scaling_uses_staleness_not_position():
     want = c1 + d1 + np.float32(1.0 / 3.0) * d0
     np.testing.assert_allclose(o.central_flat(), want, rtol=1e-14, atol=1e-15)
     assert np.max(np.abs(o.central_flat() - (c1 + d1 + 0.5 * d0))) > 1e-6
+
+
+def test_near_zero_units_flags_pre_activations_at_rounding_distance():
+    """The parity tests' flip diagnostic: a hidden pre-activation that is
+    zero up to rounding is flagged, with its layer and unit; one that is far
+    from zero is not, whatever the magnitude of its terms."""
+    prec = O._Prec(np.float64, False)
+    W0 = np.array([[1.0, -1.0], [3.0, 1.0], [1e-3, 0.0]])
+    b0 = np.zeros(3)
+    W1 = np.array([[1.0, 1.0, -1.0], [0.5, 0.0, 1.0]])
+    b1 = np.array([0.0, -2.0])
+    W2 = np.ones((2, 2))
+    b2 = np.zeros(2)
+    x = np.array([[0.75, 0.75], [1.0, 0.0]])
+    # layer 1: unit 0 is 0.75 - 0.75 = 0 for row 0; units 1 and 2 stay clear
+    # layer 2 (from relu(layer 1)): row 0 -> (3 - 0.00075, 1.5 + 0.00075 - 2),
+    # row 1 -> (1 + 3 - 0.001, 0.5 + 0.001 - 2): no zero
+    near = O.near_zero_units([(W0, b0), (W1, b1), (W2, b2)], x, prec)
+    assert [u.tolist() for u in near] == [[0], []]
+    near = O.near_zero_units([(W0, b0 + 1e-3), (W1, b1), (W2, b2)], x, prec)
+    assert [u.tolist() for u in near] == [[], []]
