@@ -63,6 +63,7 @@ struct agn_ctx {
   int32_t* order = nullptr;
   int64_t* round_dev = nullptr;
   float* zero = nullptr;  // 4 KB of zeros
+  float* sink = nullptr;  // 4 KB that absorbs stores past a matrix edge (never read)
   int64_t rounds = 0;
   int64_t N_fixed = -1;
   hipStream_t stream = nullptr;       // caller's stream (all work is ordered on it)
@@ -279,6 +280,7 @@ int enqueue_step(agn_ctx* c, const agn_data* d, int64_t S, int step) {
     w.lam = c->normalize ? (float)c->lam : 1.f;  // divisor of the committed delta
     w.last = last;
     w.zero = c->zero;
+    w.sink = c->sink;
     w.adam = adam_args(c, l);
     return w;
   };
@@ -713,7 +715,7 @@ int agn_create(const agn_shapes* shapes, int32_t n, int32_t lambda, float eta, u
             dalloc(c, &c->loss, (int64_t)n * lambda * c->m) == hipSuccess &&
             dalloc(c, &c->order, n) == hipSuccess && dalloc(c, &c->round_dev, 1) == hipSuccess &&
             dalloc(c, &c->commit_scale, n) == hipSuccess &&
-            dalloc(c, &c->zero, 1024) == hipSuccess;
+            dalloc(c, &c->zero, 1024) == hipSuccess && dalloc(c, &c->sink, 1024) == hipSuccess;
   if (ok && bf)
     ok = dalloc(c, &c->snap16, nps) == hipSuccess && dalloc(c, &c->buf16[0], nps) == hipSuccess &&
          dalloc(c, &c->buf16[1], nps) == hipSuccess;

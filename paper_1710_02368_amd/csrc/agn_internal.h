@@ -94,6 +94,7 @@ struct GemmArgs {
   int32_t last;
   const float* zero;  // a zeroed page (operand reads past an edge)
   AdamArgs adam;      // EPI_DW_UPDATE: Adam instead of SGD when adam.on
+  float* sink = nullptr;  // at least 256 writable bytes that absorb stores past an edge (never read)
 };
 
 // launchers (return hipError_t of the launch)
@@ -108,6 +109,11 @@ hipError_t launch_gemm_bf16_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStrea
 bool gemm_f32_dl_ok(int a_kc, int b_kc, const GemmArgs& g);
 hipError_t launch_gemm_f32_dl(int a_kc, int b_kc, const GemmArgs& g, hipStream_t s);
 hipError_t launch_gemm_f32_dl_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s);
+// the backward launch of a float32 hidden layer as column strips of its
+// weights (input gradient and weight gradient + update sharing each weight
+// block in LDS), used when gemm_f32_strip_ok
+bool gemm_f32_strip_ok(const GemmArgs& dx, const GemmArgs& dw);
+hipError_t launch_gemm_f32_strip_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s);
 struct HeadDwArgs;
 // the first layer's direct-load weight gradient with the output layer's
 // weight gradient + update (C <= 10) folded into the same launch

@@ -329,6 +329,7 @@ static hipError_t go(const GemmArgs& g, hipStream_t s) {
 
 hipError_t launch_gemm_f32_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s) {
   if (dx.epi != EPI_DX_MASK || dw.epi != EPI_DW_UPDATE) return hipErrorInvalidValue;
+  if (gemm_f32_strip_ok(dx, dw)) return launch_gemm_f32_strip_bwd(dx, dw, s);
   if (gemm_f32_dl_ok(1, 0, dx) && gemm_f32_dl_ok(0, 0, dw)) return launch_gemm_f32_dl_bwd(dx, dw, s);
   const int n1 = tiles_of(dx), n1pad = (n1 + kNumXcd - 1) / kNumXcd * kNumXcd;
   AGN_LAUNCH(gemm_f32_bwd_kernel, dim3(n1pad + tiles_of(dw)), dim3(NT), 0, s, dx, dw, n1, n1pad);

@@ -1,0 +1,384 @@
+// Backward launch of a hidden layer l >= 1 (float32) as column strips of the
+// layer's weights: the input-gradient product dZ_l = (dZ_{l+1} W_l) * [H_l > 0]
+// and the weight-gradient product dW_l = dZ_{l+1}^T H_l fused with the SGD
+// update of W_l and b_l (Algorithm 1, gradient line and local step).
+//
+// Both products read the same weights: the input gradient contracts W_l over
+// its rows (the layer's outputs i), the update rewrites it.  A workgroup owns
+// one worker and one strip of 64 columns j of W_l (64 inputs of the layer):
+// it holds H_l[:, strip] in LDS for the whole launch and walks the blocks of
+// 64 rows i.  Per block, dZ_{l+1}[:, block] and W_l[block, strip] travel into
+// LDS once (direct global->LDS loads, double-buffered) and feed both the
+// input gradient's 128 x 64 accumulator of the strip (K = the block's 64
+// rows i; masked by H_l from LDS at the end) and the block's 64 x 64 weight
+// gradient (K = the mini-batch) with its epilogue W_dst = W_src - eta * dW,
+// W_src from the same LDS tile (a round's last step stores (W_dst - W_snap)
+// / lambda instead).  So the weights are read from memory once and written
+// once per local step.  Eight waves, two per SIMD, each with a share of both
+// products (see below).
+//
+// MFMA v_mfma_f32_16x16x4f32: lane l supplies A[l%16][k] and B[k][l%16] for
+// k = its lane group's k, and holds D[4*(l/16) + r][l%16] in register r.
+//
+// LDS tiles hold 64 floats of each row followed by padding; the padded row
+// lengths make every LDS read of the inner loops a per-lane base address
+// plus a constant offset, free of bank conflicts:
+//   * dZ block, 128 x 64, rows of 68 floats: a column read over 16
+//     consecutive rows touches 16 distinct 16-byte bank groups, and a row
+//     read by four lane groups at rows 4 apart touches 64 distinct banks;
+//   * H strip, 128 x 64, rows of 72 floats: two lane groups at rows 4 apart
+//     reading 32 floats each touch opposite halves of the banks;
+//   * W block, 64 x 64, unpadded: it is read only along its rows.
+// A load instruction fills 1 KB of the tile; each lane loads the global chunk
+// that belongs at its 16 bytes, or a zeroed page for padding and past an edge.
+#include "direct_load.h"
+
+namespace agn {
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int STRIP = 64;        // columns j of W_l per workgroup
+constexpr int BLK = 64;          // rows i of W_l per block
+constexpr int ROWS = 128;        // mini-batch rows held (m <= ROWS)
+constexpr int NT_S = 512;        // 8 waves
+constexpr int ZS = 68;           // floats per LDS row: dZ block
+constexpr int HS = 72;           //                     H strip
+constexpr int WS = 64;           //                     W block
+constexpr int Z_F = ROWS * ZS;   // tile sizes in floats
+constexpr int H_F = ROWS * HS;
+constexpr int W_F = BLK * WS;
+constexpr int Z_Q = Z_F / 256;   // load instructions (1 KB each) per tile
+constexpr int H_Q = H_F / 256;
+constexpr int W_Q = W_F / 256;
+static_assert(Z_F % 256 == 0 && H_F % 256 == 0 && W_F % 256 == 0, "tiles fill whole load instructions");
+static_assert((H_F + 2 * (Z_F + W_F)) * 4 <= 160 * 1024, "LDS: H strip and two stages of dZ and W");
+// fewest workgroups (workers x strips) for which the strip schedule is used:
+// one workgroup per compute unit at a time (136 KB of LDS), so fewer would
+// leave compute units idle or the last wave of workgroups mostly empty
+constexpr int64_t kStripMinGroups = 1024;
+
+// Source of this lane's 16 bytes in load instruction q of a tile with S
+// floats per LDS row whose row r is row row0 + r of a row-major matrix (ld
+// floats per row), columns col0 .. col0 + 63; padding, rows >= nrow and
+// columns >= ncol (a multiple of 4) read zeros.
+template <int S>
+__device__ __forceinline__ const float* tile_src(const float* base, int64_t ld, int row0, int nrow, int col0,
+                                                 int ncol, int q, int lane, const float* zero) {
+  const int f = 256 * q + 4 * lane;
+  const int r = f / S, c = f - r * S;
+  const int gr = row0 + r, gc = col0 + c;
+  return (c < 64 && gr < nrow && gc < ncol) ? base + (int64_t)gr * ld + gc : zero;
+}
+
+struct StripCtx {
+  const float* dz;   // dZ_{l+1} of this worker [m][ld_z]
+  const float* w;    // W_l (source) of this worker [d_{l+1}][ldw]
+  int64_t ld_z, ldw;
+  int m, mo, j0, ncol;  // rows, layer outputs d_{l+1}, strip start, layer inputs d_l
+  const float* zero;
+};
+
+// The loads of block t (rows i0 = 64t): dZ[:, i0..] and W[i0.., strip] into
+// stage buffers zs, ws; instruction q of a tile is issued by wave q % 8.
+__device__ __forceinline__ void fire_block(const StripCtx& s, int t, float* zs, float* ws, int wave, int lane) {
+  const int i0 = BLK * t;
+#pragma unroll
+  for (int u = 0; u < (Z_Q + 7) / 8; ++u) {
+    const int q = wave + 8 * u;
+    if (q < Z_Q) fire(tile_src<ZS>(s.dz, s.ld_z, 0, s.m, i0, s.mo, q, lane, s.zero), lds_off(zs) + 1024 * q);
+  }
+#pragma unroll
+  for (int u = 0; u < W_Q / 8; ++u) {
+    const int q = wave + 8 * u;
+    fire(tile_src<WS>(s.w, s.ldw, i0, s.mo, s.j0, s.ncol, q, lane, s.zero), lds_off(ws) + 1024 * q);
+  }
+}
+
+// Every wave computes a part of both products for each block:
+//   * input gradient: rows 16w + 0..15 of the 128-row mini-batch (w = wave)
+//     x the strip's 64 columns, as 4 blocks of 16 x 16; block cb covers
+//     columns 4*(0..15) + cb, so one 16-byte LDS read of W gives a lane its
+//     operand of all four blocks.  K = the block's 64 rows i: lane group g
+//     supplies i = 16g + 4c + e in slice (c, e); four groups c of four
+//     slices, each reading A once (i = 16g + 4c .. +3 of row 16w + li) and
+//     B per slice.
+//   * weight gradient: rows i 16wi + 0..15 (wi = w / 2) x columns j
+//     32wj + 2*(0..15) + (0, 1) (wj = w % 2) of the block's 64 x 64, as 2
+//     blocks of 16 x 16 read with one 8-byte LDS read of H per slice.
+//     K = the mini-batch rows: lane group g supplies m = 16c + 4g + e in
+//     slice (c, e); eight groups c of four slices.
+// The two waves of a SIMD (w and w + 4) run the parts in opposite order, so
+// that one wave's weight-update epilogue (LDS reads of W_src, the update,
+// the stores) overlaps the other wave's MFMAs.  In each part the reads of
+// group c + 1 are issued before the MFMAs of group c; scheduling fences keep
+// the scheduler from sinking them next to their use.
+struct DxFrag {
+  f32x4 a, b[4];
+};
+
+// pa: row 16w + li, column 16g of the dZ block; pb: row 16g, column 4li of
+// the W block
+__device__ __forceinline__ void dx_read(const float* pa, const float* pb, int c, DxFrag& f) {
+  f.a = *reinterpret_cast<const f32x4*>(pa + 4 * c);
+#pragma unroll
+  for (int e = 0; e < 4; ++e) f.b[e] = *reinterpret_cast<const f32x4*>(pb + WS * (4 * c + e));
+}
+
+__device__ __forceinline__ void dx_part(const float* pa, const float* pb, f32x4 (&acc)[4]) {
+  DxFrag f[2];
+  dx_read(pa, pb, 0, f[0]);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    if (c + 1 < 4) {
+      dx_read(pa, pb, c + 1, f[(c + 1) & 1]);
+      __builtin_amdgcn_sched_group_barrier(0x100, 5, 0);  // the next group's LDS reads first
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e)
+#pragma unroll
+      for (int cb = 0; cb < 4; ++cb)
+        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(f[c & 1].a[e], f[c & 1].b[e][cb], acc[cb], 0, 0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);  // then this group's MFMAs
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+struct DwFrag {
+  float a[4];
+  f32x2 b[4];
+};
+
+// qa: row 4g, column 16wi + li of the dZ block; qb: row 4g, column
+// 32wj + 2li of the H strip
+__device__ __forceinline__ void dw_read(const float* qa, const float* qb, int c, DwFrag& f) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    f.a[e] = qa[ZS * (16 * c + e)];
+    f.b[e] = *reinterpret_cast<const f32x2*>(qb + HS * (16 * c + e));
+  }
+}
+
+// Slices of even and odd e accumulate into separate sets, added at the end:
+// four independent MFMA chains, as in the input-gradient part, instead of
+// two.  BIAS: also the lane's partial column sum of dZ (only the waves that
+// store the bias gradient pay for it)
+template <bool BIAS>
+__device__ __forceinline__ void dw_part(const float* qa, const float* qb, f32x4 (&out)[2], float& bsum) {
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) acc[h][0] = acc[h][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  DwFrag f[2];
+  dw_read(qa, qb, 0, f[0]);
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    if (c + 1 < 8) {
+      dw_read(qa, qb, c + 1, f[(c + 1) & 1]);
+      __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      acc[e & 1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(f[c & 1].a[e], f[c & 1].b[e].x, acc[e & 1][0], 0, 0, 0);
+      acc[e & 1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(f[c & 1].a[e], f[c & 1].b[e].y, acc[e & 1][1], 0, 0, 0);
+      if (BIAS) bsum += f[c & 1].a[e];
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  out[0] = acc[0][0] + acc[1][0];
+  out[1] = acc[0][1] + acc[1][1];
+}
+
+template <bool LAST>
+__global__ __launch_bounds__(NT_S) void gemm_f32_strip_bwd_kernel(GemmArgs dx, GemmArgs dw) {
+  __shared__ __attribute__((aligned(16))) float hs[H_F];
+  __shared__ __attribute__((aligned(16))) float zs0[Z_F];
+  __shared__ __attribute__((aligned(16))) float zs1[Z_F];
+  __shared__ __attribute__((aligned(16))) float ws0[W_F];
+  __shared__ __attribute__((aligned(16))) float ws1[W_F];
+  const int tid = threadIdx.x, lane = tid & 63, li = lane & 15, lg = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 7;  // uniform: the roles branch per wave
+  const int nstrip = (dx.N + STRIP - 1) / STRIP;
+  const int logical = xcd_remap(blockIdx.x, (int)gridDim.x);
+  const int worker = logical / nstrip, j0 = (logical % nstrip) * STRIP;
+  const int T = (dw.M + BLK - 1) / BLK;
+
+  StripCtx s;
+  s.dz = reinterpret_cast<const float*>(dx.a.ptr) + (int64_t)worker * dx.a.wstride;
+  s.w = dw.w_src + (int64_t)worker * dw.pstride;
+  s.ld_z = dx.a.ld;
+  s.ldw = dw.ldw;
+  s.m = dx.M;
+  s.mo = dw.M;
+  s.j0 = j0;
+  s.ncol = dx.N;
+  s.zero = dx.zero;
+  const float* h = reinterpret_cast<const float*>(dw.b.ptr) + (int64_t)worker * dw.b.wstride;
+
+  // prologue: the H strip, then block 0
+#pragma unroll
+  for (int u = 0; u < (H_Q + 7) / 8; ++u) {
+    const int q = wave + 8 * u;
+    if (q < H_Q) fire(tile_src<HS>(h, dw.b.ld, 0, s.m, j0, s.ncol, q, lane, s.zero), lds_off(hs) + 1024 * q);
+  }
+  fire_block(s, 0, zs0, ws0, wave, lane);
+
+  const int64_t wo = (int64_t)worker * dw.pstride;
+  const int wi = wave >> 1, wj = wave & 1;
+  // the bias is updated by the strip at j0 == 0 (waves with wj == 0)
+  const bool bias_wave = j0 == 0 && wj == 0;
+  // per-lane offsets of the reads (floats from the tile's start)
+  const int oxa = ZS * (16 * wave + li) + 16 * lg, oxb = WS * 16 * lg + 4 * li;
+  const int owa = ZS * 4 * lg + 16 * wi + li, owb = HS * 4 * lg + 32 * wj + 2 * li;
+  const int owe = WS * (16 * wi + 4 * lg) + 32 * wj + 2 * li;
+  f32x4 ax[4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b) ax[b] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // The weight update of a block: W_dst = W_src - eta * dW (a round's last
+  // step: (W_dst - W_snap) / lambda); lane: rows i = 16wi + 4lg + r, columns
+  // j = 32wj + 2li + (0, 1); the bias waves also update b at rows
+  // i = 16wi + li.
+  struct Update {
+    f32x4 aw[2];     // dW
+    f32x2 wsrc[4];   // W_src
+    f32x2 snap[4];   // W_snap (last step)
+    float bsum;      // partial column sum of dZ (bias waves)
+    float bsrc, bsnap;
+  };
+  // memory operands of block t's update, loaded a block ahead (rows and
+  // columns clamped into the matrix; the stores check the edges)
+  auto load_operands = [&](int t, Update& u) {
+    if (LAST) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int i = min(BLK * t + 16 * wi + 4 * lg + r, dw.M - 1);
+        const int j = min(j0 + 32 * wj + 2 * li, dw.N - 2);
+        u.snap[r] = *reinterpret_cast<const f32x2*>(dw.w_snap + wo + (int64_t)i * dw.ldw + j);
+      }
+    }
+    if (bias_wave) {
+      const int64_t e = wo + min(BLK * t + 16 * wi + li, dw.M - 1);
+      u.bsrc = dw.b_src[e];
+      if (LAST) u.bsnap = dw.b_snap[e];
+    }
+  };
+  auto weight_mma = [&](const float* zs, const float* ws, Update& u) {
+    u.bsum = 0.f;
+    if (bias_wave)
+      dw_part<true>(zs + owa, hs + owb, u.aw, u.bsum);
+    else
+      dw_part<false>(zs + owa, hs + owb, u.aw, u.bsum);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) u.wsrc[r] = *reinterpret_cast<const f32x2*>(ws + owe + WS * r);
+  };
+  // the stores of block t (past an edge into the sink)
+  auto weight_store = [&](int t, const Update& u) {
+    const int i0 = BLK * t;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      f32x2 v = {u.wsrc[r].x - dw.eta * u.aw[0][r], u.wsrc[r].y - dw.eta * u.aw[1][r]};
+      if (LAST) {
+        v.x = (v.x - u.snap[r].x) / dw.lam;
+        v.y = (v.y - u.snap[r].y) / dw.lam;
+      }
+      const int i = i0 + 16 * wi + 4 * lg + r, j = j0 + 32 * wj + 2 * li;
+      f32x2* dst = (i < dw.M && j < dw.N) ? reinterpret_cast<f32x2*>(dw.w_dst + wo + (int64_t)i * dw.ldw + j)
+                                          : reinterpret_cast<f32x2*>(dw.sink) + (lane & 31);
+      if (LAST)
+        *dst = v;
+      else
+        __builtin_nontemporal_store(v, dst);
+    }
+    if (bias_wave) {
+      // lane groups 1..3 hold partial sums of the same column of dZ as
+      // group 0: add them in a fixed order
+      const float p1 = __shfl(u.bsum, li + 16), p2 = __shfl(u.bsum, li + 32), p3 = __shfl(u.bsum, li + 48);
+      const float tot = ((u.bsum + p1) + p2) + p3;
+      const int i = i0 + 16 * wi + li;
+      if (lg == 0 && i < dw.M) {
+        const float nb = u.bsrc - dw.eta * tot;
+        dw.b_dst[wo + i] = LAST ? (nb - u.bsnap) / dw.lam : nb;
+      }
+    }
+  };
+
+  // Per block t: wait for its loads; store the update of block t-1 while
+  // the memory pipeline is empty (a store issued behind the next block's
+  // loads holds up the wave until they land); load the update operands of
+  // block t; issue the loads of block t+1; then the weight gradient and the
+  // input gradient of block t from LDS.
+  Update held;  // the update of block t-1, not yet stored
+  for (int t = 0; t < T; ++t) {
+    const float* zs = (t & 1) ? zs1 : zs0;
+    const float* ws = (t & 1) ? ws1 : ws0;
+    // every memory operation of this wave so far has completed (the loads
+    // of block t among them); after the barrier, those of every wave, and
+    // every wave is done with the other stage buffers
+    wait_lgkm0();
+    wait_vm<0>();
+    barrier();
+    if (t > 0) weight_store(t - 1, held);
+    load_operands(t, held);
+    if (t + 1 < T) fire_block(s, t + 1, (t & 1) ? zs0 : zs1, (t & 1) ? ws0 : ws1, wave, lane);
+    weight_mma(zs, ws, held);
+    dx_part(zs + oxa, ws + oxb, ax);
+  }
+  weight_store(T - 1, held);
+  // dZ_l = acc * [H_l > 0]; lane: rows 16w + 4lg + r, columns 4li + (0..3)
+  wait_lgkm0();
+  float* out = reinterpret_cast<float*>(dx.out) + (int64_t)worker * dx.ostride;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int m = 16 * wave + 4 * lg + r;
+    const f32x4 mk = *reinterpret_cast<const f32x4*>(hs + HS * m + 4 * li);
+    const f32x4 v = {mk.x > 0.f ? ax[0][r] : 0.f, mk.y > 0.f ? ax[1][r] : 0.f, mk.z > 0.f ? ax[2][r] : 0.f,
+                     mk.w > 0.f ? ax[3][r] : 0.f};
+    const int j = j0 + 4 * li;
+    if (m < dx.M && j < dx.N) *reinterpret_cast<f32x4*>(out + (int64_t)m * dx.ldo + j) = v;
+  }
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+}  // namespace
+
+// The strip schedule applies to one float32 hidden layer whose products share
+// their operands as enqueue_step builds them (input gradient: A = dZ_{l+1},
+// B = W_l, mask = H_l; weight gradient: A = dZ_{l+1}, B = H_l, W_src = W_l),
+// with a mini-batch of at most 128 rows, widths and row strides that allow
+// 16-byte chunks, SGD as the local rule, and enough strips (workers x
+// column strips) to give every compute unit several workgroups.
+bool gemm_f32_strip_ok(const GemmArgs& dx, const GemmArgs& dw) {
+  if (dx.epi != EPI_DX_MASK || dw.epi != EPI_DW_UPDATE || dw.adam.on || !dx.zero || !dw.sink) return false;
+  if (dx.M < 1 || dx.M > ROWS || dw.K != dx.M || dx.N != dw.N || dx.K != dw.M || dx.batch != dw.batch) return false;
+  if (dx.N % 4 || dw.M % 4 || dx.N < 2) return false;
+  if (dx.a.ptr != dw.a.ptr || dx.a.ld != dw.a.ld || dx.a.wstride != dw.a.wstride || dx.a.gather || dw.b.gather)
+    return false;
+  if (dx.b.ptr != dw.w_src || dx.b.ld != dw.ldw || dx.b.wstride != dw.pstride) return false;
+  if (dx.mask != dw.b.ptr || dx.ldm != dw.b.ld || dx.mstride != dw.b.wstride) return false;
+  const void* ptrs[] = {dx.a.ptr, dw.b.ptr, dw.w_src, dw.w_dst, dx.out, dx.zero, dw.sink};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return false;
+  if (dw.last && !aligned16(dw.w_snap)) return false;
+  if (dx.a.ld % 4 || dx.a.wstride % 4 || dw.b.ld % 4 || dw.b.wstride % 4 || dw.ldw % 4 || dw.pstride % 4 ||
+      dx.ldo % 4 || dx.ostride % 4)
+    return false;
+  const int64_t groups = (int64_t)dx.batch * ((dx.N + STRIP - 1) / STRIP);
+  return groups >= kStripMinGroups && groups < (1 << 30);
+}
+
+hipError_t launch_gemm_f32_strip_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s) {
+  if (!gemm_f32_strip_ok(dx, dw)) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)(dx.batch * ((dx.N + STRIP - 1) / STRIP))), block(NT_S);
+  if (dw.last)
+    AGN_LAUNCH(gemm_f32_strip_bwd_kernel<true>, grid, block, 0, s, dx, dw);
+  else
+    AGN_LAUNCH(gemm_f32_strip_bwd_kernel<false>, grid, block, 0, s, dx, dw);
+  return hipGetLastError();
+}
+
+}  // namespace agn
