@@ -68,15 +68,21 @@ __device__ __forceinline__ AdamCoef adam_coef(const Gather& g, const AdamArgs& a
   const double t = (double)(*g.round) * g.lam + g.step + 1;
   return {(float)(1.0 / (1.0 - pow((double)a.beta1, t))), (float)(1.0 / (1.0 - pow((double)a.beta2, t)))};
 }
-// One Adam moment update of element e (in place); returns the step
+// One Adam moment update of gradient g (m and v in place); returns the step
 // direction mhat / (sqrt(vhat) + eps), to be scaled by -eta.
+__device__ __forceinline__ float adam_moments(float g, float& m, float& v, const AdamArgs& a, const AdamCoef& c) {
+  m = a.beta1 * m + (1.f - a.beta1) * g;
+  v = a.beta2 * v + (1.f - a.beta2) * g * g;
+  return (m * c.c1) / (sqrtf(v * c.c2) + a.eps);
+}
+// the same for element e of the moment arrays m and v
 __device__ __forceinline__ float adam_dir(float g, float* m, float* v, int64_t e, const AdamArgs& a,
                                           const AdamCoef& c) {
-  const float m1 = a.beta1 * m[e] + (1.f - a.beta1) * g;
-  const float v1 = a.beta2 * v[e] + (1.f - a.beta2) * g * g;
+  float m1 = m[e], v1 = v[e];
+  const float d = adam_moments(g, m1, v1, a, c);
   m[e] = m1;
   v[e] = v1;
-  return (m1 * c.c1) / (sqrtf(v1 * c.c2) + a.eps);
+  return d;
 }
 
 // float32 -> bfloat16 bits, round to nearest even (finite inputs).

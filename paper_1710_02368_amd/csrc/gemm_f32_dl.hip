@@ -59,7 +59,9 @@ constexpr int NT = 256, TM = 64, BKD = 32, NS = 4;  // NS: LDS stages
 constexpr int TILE_F = TM * BKD;                     // floats per operand tile
 constexpr int STAGE_F = 2 * TILE_F;                  // A and B
 constexpr int EPI_F = TM * TM;                       // floats of one epilogue operand tile
+constexpr int EPI_ADAM_F = 3 * EPI_F + 2 * 256;      // W_src, the Adam moments, the bias moments
 constexpr int NWG_DW = 512;                          // persistent weight-gradient workgroups (2 per CU)
+constexpr int NWG_DW_ADAM = 256;                     // with Adam's moment tiles in LDS: 1 per CU
 
 __device__ __forceinline__ int kc_key(int r) { return (r & 7) ^ ((r >> 3) & 1); }
 __device__ __forceinline__ int kc_slot(int r, int q) { return r * 8 + (q ^ kc_key(r)); }
@@ -659,7 +661,7 @@ struct DwLoads {
 // snapshot's loads are ordinary loads, so the compiler waits for them where
 // the epilogue reads them; in LDS it would take a second tile buffer, and
 // with it the second workgroup of each CU.
-template <bool LAST>
+template <bool LAST, bool ADAM>
 __device__ __forceinline__ void fire_epi(const GemmArgs& g, const TileCoord& c, float* epi, float2 (&snap)[2][4],
                                          const Lanes& q) {
   const int64_t wo = (int64_t)c.worker * g.pstride;
@@ -670,6 +672,19 @@ __device__ __forceinline__ void fire_epi(const GemmArgs& g, const TileCoord& c, 
     const bool ok = row < g.M && col < g.N;
     const int64_t e = wo + (int64_t)row * g.ldw + col;
     fire(ok ? g.w_src + e : g.zero, lds_off(epi) + 4 * 256 * j);
+    if constexpr (ADAM) {
+      // the Adam moments of the same block, in the two tiles after it
+      fire(ok ? g.adam.mw + e : g.zero, lds_off(epi) + 4 * (EPI_F + 256 * j));
+      fire(ok ? g.adam.vw + e : g.zero, lds_off(epi) + 4 * (2 * EPI_F + 256 * j));
+    }
+  }
+  if constexpr (ADAM) {
+    // the bias moments of rows m0 .. m0 + 63 (lanes 0..15; every wave loads
+    // the same values, so that each issues the same number of loads)
+    const int row = c.m0 + 4 * q.lane;
+    const bool ok = q.lane < 16 && row < g.M;
+    fire(ok ? g.adam.mb + wo + row : g.zero, lds_off(epi) + 4 * 3 * EPI_F);
+    fire(ok ? g.adam.vb + wo + row : g.zero, lds_off(epi) + 4 * (3 * EPI_F + 256));
   }
   if constexpr (LAST) {
 #pragma unroll
@@ -683,10 +698,13 @@ __device__ __forceinline__ void fire_epi(const GemmArgs& g, const TileCoord& c, 
   }
 }
 
-template <bool LAST>
+// ADAM: Adam as the local rule; epi then holds W_src, the two moment tiles
+// and the bias moments (EPI_ADAM_F floats)
+template <bool LAST, bool ADAM>
 __device__ __forceinline__ void dw_tiles(const GemmArgs& g, const TileList tl, float* st0, float* st1, float* st2,
                                          float* st3, float* epi) {
-  constexpr int EPN = LAST ? 4 + 8 : 4;  // epilogue load instructions per wave and tile
+  // epilogue load instructions per wave and tile
+  constexpr int EPN = 4 + (LAST ? 8 : 0) + (ADAM ? 10 : 0);
   if (tl.count == 0) return;
   const int tid = threadIdx.x;
   const Lanes q{tid >> 6, tid & 63, (tid >> 6) >> 1, (tid >> 6) & 1, tid & 15, (tid & 63) >> 4};
@@ -727,7 +745,8 @@ __device__ __forceinline__ void dw_tiles(const GemmArgs& g, const TileList tl, f
     }
   }
   float2 snap[2][4];
-  fire_epi<LAST>(g, coord_of(g, tl.logical(0)), epi, snap, q);
+  fire_epi<LAST, ADAM>(g, coord_of(g, tl.logical(0)), epi, snap, q);
+  const AdamCoef ac = ADAM ? adam_coef(g.g, g.adam) : AdamCoef{1.f, 1.f};
   wait_vm<4 * (NS - 1) + EPN>();
   barrier();
   Frags f0, f1;
@@ -794,13 +813,23 @@ __device__ __forceinline__ void dw_tiles(const GemmArgs& g, const TileList tl, f
     // lane holds rows tr = wm*32 + 2*(4*lg + r) + bi, column pairs
     // tc = wn*32 + 2*li + (0, 1)
     float2 nw[2][4];
+    float2 mom[2][4][2];  // Adam: the updated moments (m, v)
 #pragma unroll
     for (int bi = 0; bi < 2; ++bi)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const int tr = q.wm * 32 + 2 * (4 * q.lg + r) + bi, tc = q.wn * 32 + 2 * q.li;
         const float2 ws = *reinterpret_cast<const float2*>(epi + tr * TM + tc);
-        float2 v{ws.x - g.eta * acc[bi][0][r], ws.y - g.eta * acc[bi][1][r]};
+        float dx = acc[bi][0][r], dy = acc[bi][1][r];
+        if constexpr (ADAM) {
+          float2 mm = *reinterpret_cast<const float2*>(epi + EPI_F + tr * TM + tc);
+          float2 vv = *reinterpret_cast<const float2*>(epi + 2 * EPI_F + tr * TM + tc);
+          dx = adam_moments(dx, mm.x, vv.x, g.adam, ac);
+          dy = adam_moments(dy, mm.y, vv.y, g.adam, ac);
+          mom[bi][r][0] = mm;
+          mom[bi][r][1] = vv;
+        }
+        float2 v{ws.x - g.eta * dx, ws.y - g.eta * dy};
         if (LAST) {
           v.x = (v.x - snap[bi][r].x) / g.lam;
           v.y = (v.y - snap[bi][r].y) / g.lam;
@@ -823,6 +852,11 @@ __device__ __forceinline__ void dw_tiles(const GemmArgs& g, const TileList tl, f
             *dst = v;
           else
             __builtin_nontemporal_store(v, dst);
+          if constexpr (ADAM) {
+            const int64_t e = wo + (int64_t)row * g.ldw + col;
+            __builtin_nontemporal_store(f32x2{mom[bi][r][0].x, mom[bi][r][0].y}, reinterpret_cast<f32x2*>(g.adam.mw + e));
+            __builtin_nontemporal_store(f32x2{mom[bi][r][1].x, mom[bi][r][1].y}, reinterpret_cast<f32x2*>(g.adam.vw + e));
+          }
         }
       }
     if (c.tile_n == 0 && q.wn == 0) {
@@ -841,7 +875,14 @@ __device__ __forceinline__ void dw_tiles(const GemmArgs& g, const TileList tl, f
           const int o = c.m0 + q.wm * 32 + 2 * q.li + b;
           if (o < g.M) {
             const int64_t e = wo + o;
-            const float nb = g.b_src[e] - g.eta * tot[b];
+            float stp = tot[b];
+            if constexpr (ADAM) {
+              float mb = epi[3 * EPI_F + (o - c.m0)], vb = epi[3 * EPI_F + 256 + (o - c.m0)];
+              stp = adam_moments(stp, mb, vb, g.adam, ac);
+              g.adam.mb[e] = mb;
+              g.adam.vb[e] = vb;
+            }
+            const float nb = g.b_src[e] - g.eta * stp;
             g.b_dst[e] = LAST ? (nb - g.b_snap[e]) / g.lam : nb;
           }
         }
@@ -856,7 +897,7 @@ __device__ __forceinline__ void dw_tiles(const GemmArgs& g, const TileList tl, f
       // every wave has read this tile's epilogue operands: load the next's
       wait_lgkm0();
       barrier();
-      fire_epi<LAST>(g, coord_of(g, tl.logical(i + 1)), epi, snap, q);
+      fire_epi<LAST, ADAM>(g, coord_of(g, tl.logical(i + 1)), epi, snap, q);
     }
   }
   // loads of the steps past the end (zero page) still write LDS
@@ -870,7 +911,7 @@ __device__ __forceinline__ void dw_tiles(const GemmArgs& g, const TileList tl, f
   __shared__ __attribute__((aligned(16))) float st1[STAGE_F];     \
   __shared__ __attribute__((aligned(16))) float st2[STAGE_F];     \
   __shared__ __attribute__((aligned(16))) float st3[STAGE_F];
-#define DL_EPI __shared__ __attribute__((aligned(16))) float epi[EPI_F];
+#define DL_EPI __shared__ __attribute__((aligned(16))) float epi[ADAM ? EPI_ADAM_F : EPI_F];
 
 // forward products, eight waves splitting each K step
 template <int EPI>
@@ -899,7 +940,7 @@ __device__ __forceinline__ int fewest_tiles_rank(int wg, int nwg) {
 // neither read nor write what the first layer's tiles do: unit u goes to
 // the workgroup of rank u mod nwg, before its tiles (the stage buffers are
 // free then, and these workgroups hold a tile fewer).
-template <bool LAST, int HCM>
+template <bool LAST, int HCM, bool ADAM>
 __global__ __launch_bounds__(NT) void gemm_f32_dl_dw_kernel(GemmArgs g, HeadDwArgs h) {
   DL_STAGES
   DL_EPI
@@ -914,7 +955,7 @@ __global__ __launch_bounds__(NT) void gemm_f32_dl_dw_kernel(GemmArgs g, HeadDwAr
     }
     if (ran) __syncthreads();    // before the tiles' loads land in the stages
   }
-  dw_tiles<LAST>(g, tiles_of_wg(tiles_dl(g), blockIdx.x, gridDim.x), st0, st1, st2, st3, epi);
+  dw_tiles<LAST, ADAM>(g, tiles_of_wg(tiles_dl(g), blockIdx.x, gridDim.x), st0, st1, st2, st3, epi);
 }
 
 // Weight-gradient tiles of workgroup `pid` in the combined backward launch
@@ -939,7 +980,7 @@ __device__ __forceinline__ TileList split_tiles(int T, int pid, int n1pad, int c
 
 // input-gradient tiles (one per workgroup, spread evenly over the XCDs),
 // and the weight-gradient tiles of the same layer on every workgroup
-template <bool LAST>
+template <bool LAST, bool ADAM>
 __global__ __launch_bounds__(NT) void gemm_f32_dl_bwd_kernel(GemmArgs dx, GemmArgs dw, int n1, int n1pad, int ca,
                                                              int cb) {
   DL_STAGES
@@ -951,7 +992,7 @@ __global__ __launch_bounds__(NT) void gemm_f32_dl_bwd_kernel(GemmArgs dx, GemmAr
     wait_lgkm0();
     barrier();
   }
-  dw_tiles<LAST>(dw, split_tiles(tiles_dl(dw), pid, n1pad, ca, cb), st0, st1, st2, st3, epi);
+  dw_tiles<LAST, ADAM>(dw, split_tiles(tiles_dl(dw), pid, n1pad, ca, cb), st0, st1, st2, st3, epi);
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
@@ -965,7 +1006,9 @@ bool operand_ok(const Operand& op, bool kc, int outer_n, int K) {
 // weight-gradient product: K-strided operands (B may be gathered when the
 // batch fits in a shard), a multiple of NS K steps, 16-byte epilogue rows
 bool dw_ok(const GemmArgs& g) {
-  if (g.epi != EPI_DW_UPDATE || !g.zero || g.adam.on) return false;  // (Adam: register-staged kernel)
+  if (g.epi != EPI_DW_UPDATE || !g.zero) return false;
+  if (g.adam.on && (!aligned16(g.adam.mw) || !aligned16(g.adam.vw) || !aligned16(g.adam.mb) || !aligned16(g.adam.vb)))
+    return false;
   const Operand& a = g.a;
   const Operand& b = g.b;
   if (!a.vec || !b.vec || a.gather || !aligned16(a.ptr) || !aligned16(b.ptr)) return false;
@@ -977,8 +1020,8 @@ bool dw_ok(const GemmArgs& g) {
 }
 
 int dw_grid(const GemmArgs& g) {
-  const int t = (tiles_dl(g) + kNumXcd - 1) / kNumXcd * kNumXcd;
-  return t < NWG_DW ? t : NWG_DW;
+  const int t = (tiles_dl(g) + kNumXcd - 1) / kNumXcd * kNumXcd, cap = g.adam.on ? NWG_DW_ADAM : NWG_DW;
+  return t < cap ? t : cap;
 }
 
 }  // namespace
@@ -999,10 +1042,16 @@ hipError_t launch_gemm_f32_dl(int a_kc, int b_kc, const GemmArgs& g, hipStream_t
     AGN_LAUNCH((gemm_f32_dl_kernel<true, false, EPI_DX_MASK>), grid, block, 0, s, g);
   else if (!a_kc && !b_kc && g.epi == EPI_DW_UPDATE) {
     const HeadDwArgs none{};
-    if (g.last)
-      AGN_LAUNCH((gemm_f32_dl_dw_kernel<true, 0>), dim3(dw_grid(g)), block, 0, s, g, none);
-    else
-      AGN_LAUNCH((gemm_f32_dl_dw_kernel<false, 0>), dim3(dw_grid(g)), block, 0, s, g, none);
+    if (g.adam.on) {
+      if (g.last)
+        AGN_LAUNCH((gemm_f32_dl_dw_kernel<true, 0, true>), dim3(dw_grid(g)), block, 0, s, g, none);
+      else
+        AGN_LAUNCH((gemm_f32_dl_dw_kernel<false, 0, true>), dim3(dw_grid(g)), block, 0, s, g, none);
+    } else if (g.last) {
+      AGN_LAUNCH((gemm_f32_dl_dw_kernel<true, 0, false>), dim3(dw_grid(g)), block, 0, s, g, none);
+    } else {
+      AGN_LAUNCH((gemm_f32_dl_dw_kernel<false, 0, false>), dim3(dw_grid(g)), block, 0, s, g, none);
+    }
   } else {
     return hipErrorInvalidValue;
   }
@@ -1015,10 +1064,16 @@ bool gemm_f32_dl_dw_head_ok(const GemmArgs& g, const HeadDwArgs& h) {
 
 hipError_t launch_gemm_f32_dl_dw_head(const GemmArgs& g, const HeadDwArgs& h, hipStream_t s) {
   if (!gemm_f32_dl_dw_head_ok(g, h)) return hipErrorInvalidValue;
-  if (g.last)
-    AGN_LAUNCH((gemm_f32_dl_dw_kernel<true, 10>), dim3(dw_grid(g)), dim3(NT), 0, s, g, h);
-  else
-    AGN_LAUNCH((gemm_f32_dl_dw_kernel<false, 10>), dim3(dw_grid(g)), dim3(NT), 0, s, g, h);
+  if (g.adam.on) {
+    if (g.last)
+      AGN_LAUNCH((gemm_f32_dl_dw_kernel<true, 10, true>), dim3(dw_grid(g)), dim3(NT), 0, s, g, h);
+    else
+      AGN_LAUNCH((gemm_f32_dl_dw_kernel<false, 10, true>), dim3(dw_grid(g)), dim3(NT), 0, s, g, h);
+  } else if (g.last) {
+    AGN_LAUNCH((gemm_f32_dl_dw_kernel<true, 10, false>), dim3(dw_grid(g)), dim3(NT), 0, s, g, h);
+  } else {
+    AGN_LAUNCH((gemm_f32_dl_dw_kernel<false, 10, false>), dim3(dw_grid(g)), dim3(NT), 0, s, g, h);
+  }
   return hipGetLastError();
 }
 
@@ -1028,7 +1083,8 @@ hipError_t launch_gemm_f32_dl_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStr
   // (an input-gradient tile of a 1000-wide layer carries the MFMA work of
   // eight weight-gradient tiles), at least 8 and at most one per
   // weight-gradient tile
-  int n2 = n1pad < NWG_DW ? n1pad : NWG_DW;
+  const int cap = dw.adam.on ? NWG_DW_ADAM : NWG_DW;
+  int n2 = n1pad < cap ? n1pad : cap;
   const int t2 = dw_grid(dw);
   if (n2 > t2) n2 = t2;
   if (n2 < kNumXcd) n2 = kNumXcd;
@@ -1045,10 +1101,16 @@ hipError_t launch_gemm_f32_dl_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStr
   if (ca * a > q) ca = q / a;
   const int cb = (q - ca * a + b - 1) / b;
   const dim3 grid(n1pad + n2), block(NT);
-  if (dw.last)
-    AGN_LAUNCH(gemm_f32_dl_bwd_kernel<true>, grid, block, 0, s, dx, dw, n1, n1pad, ca, cb);
-  else
-    AGN_LAUNCH(gemm_f32_dl_bwd_kernel<false>, grid, block, 0, s, dx, dw, n1, n1pad, ca, cb);
+  if (dw.adam.on) {
+    if (dw.last)
+      AGN_LAUNCH((gemm_f32_dl_bwd_kernel<true, true>), grid, block, 0, s, dx, dw, n1, n1pad, ca, cb);
+    else
+      AGN_LAUNCH((gemm_f32_dl_bwd_kernel<false, true>), grid, block, 0, s, dx, dw, n1, n1pad, ca, cb);
+  } else if (dw.last) {
+    AGN_LAUNCH((gemm_f32_dl_bwd_kernel<true, false>), grid, block, 0, s, dx, dw, n1, n1pad, ca, cb);
+  } else {
+    AGN_LAUNCH((gemm_f32_dl_bwd_kernel<false, false>), grid, block, 0, s, dx, dw, n1, n1pad, ca, cb);
+  }
   return hipGetLastError();
 }
 

@@ -192,7 +192,9 @@ __device__ __forceinline__ void dw_part(const float* qa, const float* qb, f32x4 
   out[1] = acc[0][1] + acc[1][1];
 }
 
-template <bool LAST>
+// ADAM: Adam as the local rule, its moments read with the update's other
+// memory operands and written with the weights
+template <bool LAST, bool ADAM>
 __global__ __launch_bounds__(NT_S) void gemm_f32_strip_bwd_kernel(GemmArgs dx, GemmArgs dw) {
   __shared__ __attribute__((aligned(16))) float hs[H_F];
   __shared__ __attribute__((aligned(16))) float zs0[Z_F];
@@ -227,6 +229,7 @@ __global__ __launch_bounds__(NT_S) void gemm_f32_strip_bwd_kernel(GemmArgs dx, G
   fire_block(s, 0, zs0, ws0, wave, lane);
 
   const int64_t wo = (int64_t)worker * dw.pstride;
+  const AdamCoef ac = ADAM ? adam_coef(dw.g, dw.adam) : AdamCoef{1.f, 1.f};
   const int wi = wave >> 1, wj = wave & 1;
   // the bias is updated by the strip at j0 == 0 (waves with wj == 0)
   const bool bias_wave = j0 == 0 && wj == 0;
@@ -238,32 +241,41 @@ __global__ __launch_bounds__(NT_S) void gemm_f32_strip_bwd_kernel(GemmArgs dx, G
 #pragma unroll
   for (int b = 0; b < 4; ++b) ax[b] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // The weight update of a block: W_dst = W_src - eta * dW (a round's last
-  // step: (W_dst - W_snap) / lambda); lane: rows i = 16wi + 4lg + r, columns
+  // The weight update of a block: W_dst = W_src - eta * dW, or with Adam
+  // W_src - eta * mhat / (sqrt(vhat) + eps) (a round's last step: (W_dst -
+  // W_snap) / lambda); lane: rows i = 16wi + 4lg + r, columns
   // j = 32wj + 2li + (0, 1); the bias waves also update b at rows
   // i = 16wi + li.
   struct Update {
     f32x4 aw[2];     // dW
     f32x2 wsrc[4];   // W_src
     f32x2 snap[4];   // W_snap (last step)
+    f32x2 mw[4], vw[4];  // Adam moments of the weights
     float bsum;      // partial column sum of dZ (bias waves)
-    float bsrc, bsnap;
+    float bsrc, bsnap, mb, vb;
   };
   // memory operands of block t's update, loaded a block ahead (rows and
   // columns clamped into the matrix; the stores check the edges)
   auto load_operands = [&](int t, Update& u) {
-    if (LAST) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int i = min(BLK * t + 16 * wi + 4 * lg + r, dw.M - 1);
-        const int j = min(j0 + 32 * wj + 2 * li, dw.N - 2);
-        u.snap[r] = *reinterpret_cast<const f32x2*>(dw.w_snap + wo + (int64_t)i * dw.ldw + j);
+    for (int r = 0; r < 4; ++r) {
+      const int i = min(BLK * t + 16 * wi + 4 * lg + r, dw.M - 1);
+      const int j = min(j0 + 32 * wj + 2 * li, dw.N - 2);
+      const int64_t e = wo + (int64_t)i * dw.ldw + j;
+      if (LAST) u.snap[r] = *reinterpret_cast<const f32x2*>(dw.w_snap + e);
+      if (ADAM) {
+        u.mw[r] = *reinterpret_cast<const f32x2*>(dw.adam.mw + e);
+        u.vw[r] = *reinterpret_cast<const f32x2*>(dw.adam.vw + e);
       }
     }
     if (bias_wave) {
       const int64_t e = wo + min(BLK * t + 16 * wi + li, dw.M - 1);
       u.bsrc = dw.b_src[e];
       if (LAST) u.bsnap = dw.b_snap[e];
+      if (ADAM) {
+        u.mb = dw.adam.mb[e];
+        u.vb = dw.adam.vb[e];
+      }
     }
   };
   auto weight_mma = [&](const float* zs, const float* ws, Update& u) {
@@ -280,28 +292,49 @@ __global__ __launch_bounds__(NT_S) void gemm_f32_strip_bwd_kernel(GemmArgs dx, G
     const int i0 = BLK * t;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      f32x2 v = {u.wsrc[r].x - dw.eta * u.aw[0][r], u.wsrc[r].y - dw.eta * u.aw[1][r]};
+      f32x2 d = {u.aw[0][r], u.aw[1][r]}, m = {0.f, 0.f}, v2 = {0.f, 0.f};
+      if (ADAM) {
+        float mx = u.mw[r].x, my = u.mw[r].y, vx = u.vw[r].x, vy = u.vw[r].y;
+        d.x = adam_moments(d.x, mx, vx, dw.adam, ac);
+        d.y = adam_moments(d.y, my, vy, dw.adam, ac);
+        m = f32x2{mx, my};
+        v2 = f32x2{vx, vy};
+      }
+      f32x2 v = {u.wsrc[r].x - dw.eta * d.x, u.wsrc[r].y - dw.eta * d.y};
       if (LAST) {
         v.x = (v.x - u.snap[r].x) / dw.lam;
         v.y = (v.y - u.snap[r].y) / dw.lam;
       }
       const int i = i0 + 16 * wi + 4 * lg + r, j = j0 + 32 * wj + 2 * li;
-      f32x2* dst = (i < dw.M && j < dw.N) ? reinterpret_cast<f32x2*>(dw.w_dst + wo + (int64_t)i * dw.ldw + j)
-                                          : reinterpret_cast<f32x2*>(dw.sink) + (lane & 31);
+      const bool in = i < dw.M && j < dw.N;
+      const int64_t e = wo + (int64_t)i * dw.ldw + j;
+      f32x2* sink = reinterpret_cast<f32x2*>(dw.sink) + (lane & 31);
+      f32x2* dst = in ? reinterpret_cast<f32x2*>(dw.w_dst + e) : sink;
       if (LAST)
         *dst = v;
       else
         __builtin_nontemporal_store(v, dst);
+      if (ADAM) {
+        __builtin_nontemporal_store(m, in ? reinterpret_cast<f32x2*>(dw.adam.mw + e) : sink);
+        __builtin_nontemporal_store(v2, in ? reinterpret_cast<f32x2*>(dw.adam.vw + e) : sink);
+      }
     }
     if (bias_wave) {
       // lane groups 1..3 hold partial sums of the same column of dZ as
       // group 0: add them in a fixed order
       const float p1 = __shfl(u.bsum, li + 16), p2 = __shfl(u.bsum, li + 32), p3 = __shfl(u.bsum, li + 48);
-      const float tot = ((u.bsum + p1) + p2) + p3;
+      float tot = ((u.bsum + p1) + p2) + p3;
       const int i = i0 + 16 * wi + li;
       if (lg == 0 && i < dw.M) {
+        const int64_t e = wo + i;
+        if (ADAM) {
+          float m = u.mb, v2 = u.vb;
+          tot = adam_moments(tot, m, v2, dw.adam, ac);
+          dw.adam.mb[e] = m;
+          dw.adam.vb[e] = v2;
+        }
         const float nb = u.bsrc - dw.eta * tot;
-        dw.b_dst[wo + i] = LAST ? (nb - u.bsnap) / dw.lam : nb;
+        dw.b_dst[e] = LAST ? (nb - u.bsnap) / dw.lam : nb;
       }
     }
   };
@@ -350,10 +383,10 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 // their operands as enqueue_step builds them (input gradient: A = dZ_{l+1},
 // B = W_l, mask = H_l; weight gradient: A = dZ_{l+1}, B = H_l, W_src = W_l),
 // with a mini-batch of at most 128 rows, widths and row strides that allow
-// 16-byte chunks, SGD as the local rule, and enough strips (workers x
+// 16-byte chunks (the Adam moments too), and enough strips (workers x
 // column strips) to give every compute unit several workgroups.
 bool gemm_f32_strip_ok(const GemmArgs& dx, const GemmArgs& dw) {
-  if (dx.epi != EPI_DX_MASK || dw.epi != EPI_DW_UPDATE || dw.adam.on || !dx.zero || !dw.sink) return false;
+  if (dx.epi != EPI_DX_MASK || dw.epi != EPI_DW_UPDATE || !dx.zero || !dw.sink) return false;
   if (dx.M < 1 || dx.M > ROWS || dw.K != dx.M || dx.N != dw.N || dx.K != dw.M || dx.batch != dw.batch) return false;
   if (dx.N % 4 || dw.M % 4 || dx.N < 2) return false;
   if (dx.a.ptr != dw.a.ptr || dx.a.ld != dw.a.ld || dx.a.wstride != dw.a.wstride || dx.a.gather || dw.b.gather)
@@ -364,6 +397,7 @@ bool gemm_f32_strip_ok(const GemmArgs& dx, const GemmArgs& dw) {
   for (const void* p : ptrs)
     if (!aligned16(p)) return false;
   if (dw.last && !aligned16(dw.w_snap)) return false;
+  if (dw.adam.on && (!aligned16(dw.adam.mw) || !aligned16(dw.adam.vw) || !dw.adam.mb || !dw.adam.vb)) return false;
   if (dx.a.ld % 4 || dx.a.wstride % 4 || dw.b.ld % 4 || dw.b.wstride % 4 || dw.ldw % 4 || dw.pstride % 4 ||
       dx.ldo % 4 || dx.ostride % 4)
     return false;
@@ -374,10 +408,16 @@ bool gemm_f32_strip_ok(const GemmArgs& dx, const GemmArgs& dw) {
 hipError_t launch_gemm_f32_strip_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s) {
   if (!gemm_f32_strip_ok(dx, dw)) return hipErrorInvalidValue;
   const dim3 grid((unsigned)(dx.batch * ((dx.N + STRIP - 1) / STRIP))), block(NT_S);
-  if (dw.last)
-    AGN_LAUNCH(gemm_f32_strip_bwd_kernel<true>, grid, block, 0, s, dx, dw);
-  else
-    AGN_LAUNCH(gemm_f32_strip_bwd_kernel<false>, grid, block, 0, s, dx, dw);
+  if (dw.adam.on) {
+    if (dw.last)
+      AGN_LAUNCH((gemm_f32_strip_bwd_kernel<true, true>), grid, block, 0, s, dx, dw);
+    else
+      AGN_LAUNCH((gemm_f32_strip_bwd_kernel<false, true>), grid, block, 0, s, dx, dw);
+  } else if (dw.last) {
+    AGN_LAUNCH((gemm_f32_strip_bwd_kernel<true, false>), grid, block, 0, s, dx, dw);
+  } else {
+    AGN_LAUNCH((gemm_f32_strip_bwd_kernel<false, false>), grid, block, 0, s, dx, dw);
+  }
   return hipGetLastError();
 }
 

@@ -202,6 +202,62 @@ def round1_against_live_oracle(g, o, wl, X, y, xd, yd, order):
           flush=True)
 
 
+def adam_step_bound(beta1, beta2, steps):
+    """Largest |mhat_t / sqrt(vhat_t)| over t <= steps for any gradients
+    (eps = 0; Adam, Kingma & Ba 2015): by Cauchy-Schwarz,
+    sum_i b1^(t-i) |g_i| <= sqrt(sum_i b1^(2(t-i)) / b2^(t-i)) *
+    sqrt(sum_i b2^(t-i) g_i^2), so the ratio is at most
+    (1-b1)/(1-b1^t) * sqrt((1-b2^t)/(1-b2)) * sqrt(sum_j (b1^2/b2)^j)."""
+    best = 0.0
+    for t in range(1, steps + 1):
+        s = sum((beta1 * beta1 / beta2) ** j for j in range(t))
+        best = max(best, (1 - beta1) / (1 - beta1 ** t) * np.sqrt((1 - beta2 ** t) / (1 - beta2)) * np.sqrt(s))
+    return best
+
+
+def check_adam_round1(g, o, wl, X, y, xd, yd, order, adam):
+    """Round 1 with Adam as the local rule against the live oracle.
+
+    Adam divides each component's step by the root of its own squared
+    gradient history, so the step carries the relative error of that
+    component's gradient: a gradient that is a cancellation of larger terms,
+    or one whose sign a flipped ReLU derivative changes (a pre-activation
+    within rounding distance of zero: one sample's contribution switched on
+    or off), moves its component by up to 2 eta apart, and the changed
+    parameters feed every later product of the worker.  Measured at
+    64-516-512-10, 128 workers, lambda = 3: most workers agree to about 1e-5 (Frobenius, worst tensor of the
+    delta), a few (4 of 128) by 1e-3 to 5e-2.  The gates: the commit bit for
+    bit; every delta component within the bound two Adam trajectories of
+    lambda steps can differ by (adam_step_bound); the median worker within
+    1e-4 and nine in ten within 1e-3.  A mistake in the update itself (a
+    moment or a bias correction of the wrong element, worker or step) moves
+    every worker, not a few."""
+    start = g.central().cpu().numpy()
+    ulps = start.view(np.int32).astype(np.int64) - o.central_flat().view(np.int32).astype(np.int64)
+    assert np.max(np.abs(ulps)) <= 1, "initial central variables differ"
+    g.round(xd, yd, order)
+    gdel = [g.delta(k).cpu().numpy() for k in range(wl.n)]
+    check_commit_prefix_sums(start, gdel, [g.worker_params(k).cpu().numpy() for k in range(wl.n)],
+                             g.central().cpu().numpy(), order, f"{wl.name} round 1")
+    o.round(X, y, order)
+    np.testing.assert_allclose(g.loss().cpu().numpy(), o.last_loss, rtol=1e-4)
+    s64 = start.astype(np.float64)
+    bound = 2 * adam_step_bound(adam[0], adam[1], wl.lam) * wl.eta * 1.0001
+    fro = []
+    for k in range(wl.n):
+        disp = (flat_params(o.last_finals[k]).astype(np.float64) - s64) / wl.lam
+        d = gdel[k].astype(np.float64)
+        err = np.abs(d - disp)
+        assert err.max() <= bound, (k, err.max(), bound)
+        fro.append(max(np.linalg.norm(d[a:b] - disp[a:b]) / np.linalg.norm(disp[a:b])
+                       for _, a, b in tensor_slices(wl.dims)))
+    fro = np.array(fro)
+    print(f"{wl.name} round 1 deltas (Frobenius, worst tensor): median {np.median(fro):.2e}, "
+          f"above 1e-3: {int(np.sum(fro > 1e-3))} of {wl.n}, worst {fro.max():.2e}", flush=True)
+    assert np.median(fro) <= 1e-4, np.median(fro)
+    assert np.mean(fro > 1e-3) <= 0.1, np.sort(fro)[-16:]
+
+
 @pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", ["mlp1000_n8", "mlp1000_n20"])
 def test_all_rounds_live_oracle(name):

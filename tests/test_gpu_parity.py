@@ -190,6 +190,34 @@ def test_small_shapes(case):
     run_parity(wl, tol1, tolN, normalize=normalize, adam=adam, staleness_scaled=scaled)
 
 
+@pytest.mark.timeout(300)
+def test_adam_persistent_weight_gradient():
+    """Adam as the local rule on the persistent direct-load weight-gradient
+    kernels: the first layer's (with the output layer's folded in) and the
+    combined backward launch of the hidden layer, 40 workers of
+    128-256-256-10, so that each workgroup walks several tiles (the Adam
+    variant runs one workgroup per compute unit).  Round 1 under the gates of
+    check_adam_round1 (the commit bit for bit, every delta component within
+    Adam's step bound, the median worker within 1e-4); round 2's commit bit
+    for bit."""
+    agn = _agn()
+    from tests.test_gpu_fullsize import check_adam_round1, check_commit_prefix_sums
+    wl = W.small_workload("adam_persistent", (128, 256, 256, 10), 40, 3, 128, 0.002, 2, 40 * 256,
+                          data="sparse_teacher2", order="permutation")
+    X, y = W.make_data(wl)
+    xd, yd = to_device(X, y)
+    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, adam=ADAM)
+    o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, adam=ADAM)
+    orders = W.commit_orders(wl)
+    check_adam_round1(g, o, wl, X, y, xd, yd, orders[0], ADAM)
+    start = g.central().cpu().numpy()
+    g.round(xd, yd, orders[1])
+    check_commit_prefix_sums(start, [g.delta(k).cpu().numpy() for k in range(wl.n)],
+                             [g.worker_params(k).cpu().numpy() for k in range(wl.n)], g.central().cpu().numpy(),
+                             orders[1], "adam_persistent round 2")
+    g.close()
+
+
 def test_downpour_lambda1_rules_coincide():
     """With lambda = 1 the normalized and the accumulated commit are the same
     rule (DOWNPOUR, Section 3 footnote to Eq. 1): bitwise equal results."""

@@ -8,10 +8,11 @@ Shapes: strips and row blocks with ragged ends (996 and 1004 are not
 multiples of 64), a row stride padded past the width (996 -> 1000), a
 mini-batch below the 128 rows the schedule holds (m = 100), several local
 steps (the round's last step stores the normalized displacement), two
-rounds.  Gates as in the full-size tests (test_gpu_fullsize.py): round 1
-against the live oracle on the whole central variable, every delta and every
-pulled copy, and the commit bit for bit; round 2 on the central variable and
-the pulled copies.
+rounds, Adam as the local rule.  Gates as in the full-size tests
+(test_gpu_fullsize.py): round 1 against the live oracle on the whole central
+variable, every delta and every pulled copy, and the commit bit for bit;
+round 2 on the central variable and the pulled copies.  Adam: see
+check_adam_round1 (test_gpu_fullsize.py).
 """
 import numpy as np
 import pytest
@@ -19,14 +20,18 @@ import pytest
 import workloads as W
 from oracle import AGNOracle
 from tests.helpers import to_device, require_gpu
-from tests.test_gpu_fullsize import BIAS_FACTOR, TOL, check_params, round1_against_live_oracle
+from tests.test_gpu_fullsize import (BIAS_FACTOR, TOL, check_adam_round1, check_commit_prefix_sums, check_params,
+                                     round1_against_live_oracle)
 
 pytestmark = pytest.mark.gpu
 
+ADAM = (0.9, 0.999, 1e-8)
+
 STRIP_CASES = [
-    # name, dims, n, lam, m, eta, rounds, N, data
+    # name, dims, n, lam, m, eta, rounds, N, data[, adam]
     ("strip_ragged", (96, 996, 1004, 12), 64, 2, 100, 0.02, 2, 64 * 300, "sparse_teacher2"),
     ("strip_two_hidden", (64, 512, 768, 512, 10), 128, 3, 128, 0.02, 2, 128 * 256, "sparse_teacher2"),
+    ("strip_adam", (64, 516, 512, 10), 128, 3, 120, 0.002, 2, 128 * 256, "sparse_teacher2", ADAM),
 ]
 
 
@@ -39,15 +44,26 @@ def strip_groups(dims, n, layer):
 def test_strip_schedule(case):
     require_gpu()
     import paper_1710_02368_amd as agn
-    name, dims, n, lam, m, eta, R, N, data = case
+    name, dims, n, lam, m, eta, R, N, data = case[:9]
+    adam = case[9] if len(case) > 9 else None
     # every hidden layer l >= 1 below the output layer runs the strip schedule
     assert all(strip_groups(dims, n, l) >= 1024 for l in range(1, len(dims) - 2))
     wl = W.small_workload(name, dims, n, lam, m, eta, R, N, data=data, order="permutation")
     X, y = W.make_data(wl)
     xd, yd = to_device(X, y)
-    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed)
-    o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed)
+    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, adam=adam)
+    o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, adam=adam)
     orders = W.commit_orders(wl)
+    if adam is not None:
+        check_adam_round1(g, o, wl, X, y, xd, yd, orders[0], adam)
+        for r, order in enumerate(orders[1:], start=2):
+            start = g.central().cpu().numpy()
+            g.round(xd, yd, order)
+            gdel = [g.delta(k).cpu().numpy() for k in range(wl.n)]
+            check_commit_prefix_sums(start, gdel, [g.worker_params(k).cpu().numpy() for k in range(wl.n)],
+                                     g.central().cpu().numpy(), order, f"{name} round {r}")
+        g.close()
+        return
     round1_against_live_oracle(g, o, wl, X, y, xd, yd, orders[0])
     tol = TOL["fp32"][1]
     for r, order in enumerate(orders[1:], start=2):
