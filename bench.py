@@ -235,6 +235,29 @@ def copy_calibration(nbytes=1 << 30, reps=5):
     print(json.dumps({"copy_bytes": nbytes, "reps": reps}))
 
 
+def copy_ceiling(total_bytes, reps=5):
+    """GB/s of a plain device-to-device copy that reads and writes
+    total_bytes in all (half each), timed with events on the copy's stream:
+    the rate a streaming kernel of that size reaches on this device, beside
+    the published 8 TB/s."""
+    import torch
+    n = max(1 << 20, int(total_bytes) // 8)
+    x = torch.empty(n, dtype=torch.float32, device="cuda").fill_(1.0)
+    y = torch.empty_like(x)
+    for _ in range(2):
+        y.copy_(x)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(reps):
+        y.copy_(x)
+    stop.record()
+    torch.cuda.synchronize()
+    gbs = 8.0 * n * reps / (start.elapsed_time(stop) * 1e-3) / 1e9
+    del x, y
+    torch.cuda.empty_cache()
+    return gbs
+
+
 # rocprofv3 kernel names -> the kernel classes the library times
 def traffic_class(name):
     if "commit_kernel" in name:
@@ -533,6 +556,7 @@ def main():
                  "launches": dom_cnt})
     c_avg = c_ms * 1e-3 / max(c_cnt, 1)
     commit_gbs = work["commit"]["bytes"] / c_avg / 1e9
+    copy_gbs = copy_ceiling(work["commit"]["bytes"])
     out = {
         "metric": METRIC, "value": round(value, 1), "unit": "worker-samples/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(dt * 1e3 / args.steps, 4),
@@ -547,7 +571,10 @@ def main():
                             "unit": "GB/s", "frac": round(commit_gbs / PEAK_HBM_GBS, 4),
                             "avg_launch_us": round(c_avg * 1e6, 2),
                             "algorithmic_per_launch": work["commit"]["bytes"],
-                            "traffic": stored_traffic(wl.name, "commit")},
+                            "traffic": stored_traffic(wl.name, "commit"),
+                            "copy_ceiling": {"achieved": round(copy_gbs, 1), "unit": "GB/s",
+                                             "kind": "device-to-device copy of the same bytes, same run"},
+                            "frac_of_copy": round(commit_gbs / copy_gbs, 4)},
         "round_mfma_util": round(wl.flops_per_round / (dt / args.steps) / 1e12 / PEAK_TFLOPS[wl.dtype], 4),
         "kernels": breakdown,
     }

@@ -58,6 +58,9 @@ static_assert((H_F + 2 * (Z_F + W_F)) * 4 <= 160 * 1024, "LDS: H strip and two s
 // one workgroup per compute unit at a time (136 KB of LDS), so fewer would
 // leave compute units idle or the last wave of workgroups mostly empty
 constexpr int64_t kStripMinGroups = 1024;
+// waves that issue a block's loads inside the loop (the others go straight
+// to their MFMAs while these wait for room in the memory pipeline)
+constexpr int FIRE_WAVES = 4;
 
 // Source of this lane's 16 bytes in load instruction q of a tile with S
 // floats per LDS row whose row r is row row0 + r of a row-major matrix (ld
@@ -81,18 +84,21 @@ struct StripCtx {
 };
 
 // The loads of block t (rows i0 = 64t): dZ[:, i0..] and W[i0.., strip] into
-// stage buffers zs, ws; instruction q of a tile is issued by wave q % 8.
+// stage buffers zs, ws; instruction q of a tile is issued by wave q % NW
+// (waves NW.. issue none).
+template <int NW>
 __device__ __forceinline__ void fire_block(const StripCtx& s, int t, float* zs, float* ws, int wave, int lane) {
+  if (wave >= NW) return;
   const int i0 = BLK * t;
 #pragma unroll
-  for (int u = 0; u < (Z_Q + 7) / 8; ++u) {
-    const int q = wave + 8 * u;
+  for (int u = 0; u < (Z_Q + NW - 1) / NW; ++u) {
+    const int q = wave + NW * u;
     if (q < Z_Q) fire(tile_src<ZS>(s.dz, s.ld_z, 0, s.m, i0, s.mo, q, lane, s.zero), lds_off(zs) + 1024 * q);
   }
 #pragma unroll
-  for (int u = 0; u < W_Q / 8; ++u) {
-    const int q = wave + 8 * u;
-    fire(tile_src<WS>(s.w, s.ldw, i0, s.mo, s.j0, s.ncol, q, lane, s.zero), lds_off(ws) + 1024 * q);
+  for (int u = 0; u < (W_Q + NW - 1) / NW; ++u) {
+    const int q = wave + NW * u;
+    if (q < W_Q) fire(tile_src<WS>(s.w, s.ldw, i0, s.mo, s.j0, s.ncol, q, lane, s.zero), lds_off(ws) + 1024 * q);
   }
 }
 
@@ -109,11 +115,12 @@ __device__ __forceinline__ void fire_block(const StripCtx& s, int t, float* zs, 
 //     blocks of 16 x 16 read with one 8-byte LDS read of H per slice.
 //     K = the mini-batch rows: lane group g supplies m = 16c + 4g + e in
 //     slice (c, e); eight groups c of four slices.
-// The two waves of a SIMD (w and w + 4) run the parts in opposite order, so
-// that one wave's weight-update epilogue (LDS reads of W_src, the update,
-// the stores) overlaps the other wave's MFMAs.  In each part the reads of
-// group c + 1 are issued before the MFMAs of group c; scheduling fences keep
-// the scheduler from sinking them next to their use.
+// Every wave runs its weight-gradient part first, then its input-gradient
+// part: the older wave of a SIMD wins the MFMA arbitration, so in the other
+// order one wave's update epilogue ran while its partner had no MFMAs left.
+// In each part the reads of group c + 1 are issued before the MFMAs of group
+// c; scheduling fences keep the scheduler from sinking them next to their
+// use.
 struct DxFrag {
   f32x4 a, b[4];
 };
@@ -192,8 +199,128 @@ __device__ __forceinline__ void dw_part(const float* qa, const float* qb, f32x4 
   out[1] = acc[0][1] + acc[1][1];
 }
 
+// The weight update of a 64 x 64 block: W_dst = W_src - eta * dW, or with
+// Adam W_src - eta * mhat / (sqrt(vhat) + eps) (a round's last step: (W_dst -
+// W_snap) / lambda); lane: rows i = i0 + 16wi + 4lg + r, columns
+// j = j0 + 32wj + 2li + (0, 1) (wi = wave / 2, wj = wave % 2); in the strip
+// that holds column 0 the waves with wj == 0 also update b at rows
+// i = i0 + 16wi + li.
+struct Update {
+  f32x4 aw[2];         // dW
+  f32x2 wsrc[4];       // W_src
+  f32x2 snap[4];       // W_snap (last step)
+  f32x2 mw[4], vw[4];  // Adam moments of the weights
+  float bsum;          // partial column sum of dZ (bias waves)
+  float bsrc, bsnap, mb, vb;
+};
+
 // ADAM: Adam as the local rule, its moments read with the update's other
 // memory operands and written with the weights
+template <bool LAST, bool ADAM>
+struct StripUpdate {
+  const GemmArgs& dw;
+  AdamCoef ac;
+  int wi, wj, li, lg, lane;
+  int owa, owb, owe;  // per-lane read offsets in the dZ, H and W tiles
+
+  __device__ __forceinline__ StripUpdate(const GemmArgs& g, int wave, int li_, int lg_, int lane_)
+      : dw(g), ac(ADAM ? adam_coef(g.g, g.adam) : AdamCoef{1.f, 1.f}), wi(wave >> 1), wj(wave & 1), li(li_),
+        lg(lg_), lane(lane_) {
+    owa = ZS * 4 * lg + 16 * wi + li;
+    owb = HS * 4 * lg + 32 * wj + 2 * li;
+    owe = WS * (16 * wi + 4 * lg) + 32 * wj + 2 * li;
+  }
+
+  // the update's memory operands (rows and columns clamped into the
+  // matrix; the stores check the edges)
+  __device__ __forceinline__ void load(Update& u, int64_t wo, int i0, int j0, bool bias) const {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int i = min(i0 + 16 * wi + 4 * lg + r, dw.M - 1);
+      const int j = min(j0 + 32 * wj + 2 * li, dw.N - 2);
+      const int64_t e = wo + (int64_t)i * dw.ldw + j;
+      if (LAST) u.snap[r] = *reinterpret_cast<const f32x2*>(dw.w_snap + e);
+      if (ADAM) {
+        u.mw[r] = *reinterpret_cast<const f32x2*>(dw.adam.mw + e);
+        u.vw[r] = *reinterpret_cast<const f32x2*>(dw.adam.vw + e);
+      }
+    }
+    if (bias && wj == 0) {
+      const int64_t e = wo + min(i0 + 16 * wi + li, dw.M - 1);
+      u.bsrc = dw.b_src[e];
+      if (LAST) u.bsnap = dw.b_snap[e];
+      if (ADAM) {
+        u.mb = dw.adam.mb[e];
+        u.vb = dw.adam.vb[e];
+      }
+    }
+  }
+
+  // the block's weight gradient from the dZ block zs and the strip hs, and
+  // W_src from the W block ws
+  __device__ __forceinline__ void mma(const float* zs, const float* ws, const float* hs, Update& u,
+                                      bool bias) const {
+    u.bsum = 0.f;
+    if (bias && wj == 0)
+      dw_part<true>(zs + owa, hs + owb, u.aw, u.bsum);
+    else
+      dw_part<false>(zs + owa, hs + owb, u.aw, u.bsum);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) u.wsrc[r] = *reinterpret_cast<const f32x2*>(ws + owe + WS * r);
+  }
+
+  // the block's stores (past an edge into the sink)
+  __device__ __forceinline__ void store(const Update& u, int64_t wo, int i0, int j0, bool bias) const {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      f32x2 d = {u.aw[0][r], u.aw[1][r]}, m = {0.f, 0.f}, v2 = {0.f, 0.f};
+      if (ADAM) {
+        float mx = u.mw[r].x, my = u.mw[r].y, vx = u.vw[r].x, vy = u.vw[r].y;
+        d.x = adam_moments(d.x, mx, vx, dw.adam, ac);
+        d.y = adam_moments(d.y, my, vy, dw.adam, ac);
+        m = f32x2{mx, my};
+        v2 = f32x2{vx, vy};
+      }
+      f32x2 v = {u.wsrc[r].x - dw.eta * d.x, u.wsrc[r].y - dw.eta * d.y};
+      if (LAST) {
+        v.x = (v.x - u.snap[r].x) / dw.lam;
+        v.y = (v.y - u.snap[r].y) / dw.lam;
+      }
+      const int i = i0 + 16 * wi + 4 * lg + r, j = j0 + 32 * wj + 2 * li;
+      const bool in = i < dw.M && j < dw.N;
+      const int64_t e = wo + (int64_t)i * dw.ldw + j;
+      f32x2* sink = reinterpret_cast<f32x2*>(dw.sink) + (lane & 31);
+      f32x2* dst = in ? reinterpret_cast<f32x2*>(dw.w_dst + e) : sink;
+      if (LAST)
+        *dst = v;
+      else
+        __builtin_nontemporal_store(v, dst);
+      if (ADAM) {
+        __builtin_nontemporal_store(m, in ? reinterpret_cast<f32x2*>(dw.adam.mw + e) : sink);
+        __builtin_nontemporal_store(v2, in ? reinterpret_cast<f32x2*>(dw.adam.vw + e) : sink);
+      }
+    }
+    if (bias && wj == 0) {
+      // lane groups 1..3 hold partial sums of the same column of dZ as
+      // group 0: add them in a fixed order
+      const float p1 = __shfl(u.bsum, li + 16), p2 = __shfl(u.bsum, li + 32), p3 = __shfl(u.bsum, li + 48);
+      float tot = ((u.bsum + p1) + p2) + p3;
+      const int i = i0 + 16 * wi + li;
+      if (lg == 0 && i < dw.M) {
+        const int64_t e = wo + i;
+        if (ADAM) {
+          float m = u.mb, v2 = u.vb;
+          tot = adam_moments(tot, m, v2, dw.adam, ac);
+          dw.adam.mb[e] = m;
+          dw.adam.vb[e] = v2;
+        }
+        const float nb = u.bsrc - dw.eta * tot;
+        dw.b_dst[e] = LAST ? (nb - u.bsnap) / dw.lam : nb;
+      }
+    }
+  }
+};
+
 template <bool LAST, bool ADAM>
 __global__ __launch_bounds__(NT_S) void gemm_f32_strip_bwd_kernel(GemmArgs dx, GemmArgs dw) {
   __shared__ __attribute__((aligned(16))) float hs[H_F];
@@ -226,118 +353,17 @@ __global__ __launch_bounds__(NT_S) void gemm_f32_strip_bwd_kernel(GemmArgs dx, G
     const int q = wave + 8 * u;
     if (q < H_Q) fire(tile_src<HS>(h, dw.b.ld, 0, s.m, j0, s.ncol, q, lane, s.zero), lds_off(hs) + 1024 * q);
   }
-  fire_block(s, 0, zs0, ws0, wave, lane);
+  fire_block<8>(s, 0, zs0, ws0, wave, lane);
 
   const int64_t wo = (int64_t)worker * dw.pstride;
-  const AdamCoef ac = ADAM ? adam_coef(dw.g, dw.adam) : AdamCoef{1.f, 1.f};
-  const int wi = wave >> 1, wj = wave & 1;
-  // the bias is updated by the strip at j0 == 0 (waves with wj == 0)
-  const bool bias_wave = j0 == 0 && wj == 0;
-  // per-lane offsets of the reads (floats from the tile's start)
+  const StripUpdate<LAST, ADAM> up(dw, wave, li, lg, lane);
+  // the bias is updated by the strip at j0 == 0
+  const bool bias = j0 == 0;
+  // per-lane offsets of the input-gradient reads (floats from the tile's start)
   const int oxa = ZS * (16 * wave + li) + 16 * lg, oxb = WS * 16 * lg + 4 * li;
-  const int owa = ZS * 4 * lg + 16 * wi + li, owb = HS * 4 * lg + 32 * wj + 2 * li;
-  const int owe = WS * (16 * wi + 4 * lg) + 32 * wj + 2 * li;
   f32x4 ax[4];
 #pragma unroll
   for (int b = 0; b < 4; ++b) ax[b] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  // The weight update of a block: W_dst = W_src - eta * dW, or with Adam
-  // W_src - eta * mhat / (sqrt(vhat) + eps) (a round's last step: (W_dst -
-  // W_snap) / lambda); lane: rows i = 16wi + 4lg + r, columns
-  // j = 32wj + 2li + (0, 1); the bias waves also update b at rows
-  // i = 16wi + li.
-  struct Update {
-    f32x4 aw[2];     // dW
-    f32x2 wsrc[4];   // W_src
-    f32x2 snap[4];   // W_snap (last step)
-    f32x2 mw[4], vw[4];  // Adam moments of the weights
-    float bsum;      // partial column sum of dZ (bias waves)
-    float bsrc, bsnap, mb, vb;
-  };
-  // memory operands of block t's update, loaded a block ahead (rows and
-  // columns clamped into the matrix; the stores check the edges)
-  auto load_operands = [&](int t, Update& u) {
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int i = min(BLK * t + 16 * wi + 4 * lg + r, dw.M - 1);
-      const int j = min(j0 + 32 * wj + 2 * li, dw.N - 2);
-      const int64_t e = wo + (int64_t)i * dw.ldw + j;
-      if (LAST) u.snap[r] = *reinterpret_cast<const f32x2*>(dw.w_snap + e);
-      if (ADAM) {
-        u.mw[r] = *reinterpret_cast<const f32x2*>(dw.adam.mw + e);
-        u.vw[r] = *reinterpret_cast<const f32x2*>(dw.adam.vw + e);
-      }
-    }
-    if (bias_wave) {
-      const int64_t e = wo + min(BLK * t + 16 * wi + li, dw.M - 1);
-      u.bsrc = dw.b_src[e];
-      if (LAST) u.bsnap = dw.b_snap[e];
-      if (ADAM) {
-        u.mb = dw.adam.mb[e];
-        u.vb = dw.adam.vb[e];
-      }
-    }
-  };
-  auto weight_mma = [&](const float* zs, const float* ws, Update& u) {
-    u.bsum = 0.f;
-    if (bias_wave)
-      dw_part<true>(zs + owa, hs + owb, u.aw, u.bsum);
-    else
-      dw_part<false>(zs + owa, hs + owb, u.aw, u.bsum);
-#pragma unroll
-    for (int r = 0; r < 4; ++r) u.wsrc[r] = *reinterpret_cast<const f32x2*>(ws + owe + WS * r);
-  };
-  // the stores of block t (past an edge into the sink)
-  auto weight_store = [&](int t, const Update& u) {
-    const int i0 = BLK * t;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      f32x2 d = {u.aw[0][r], u.aw[1][r]}, m = {0.f, 0.f}, v2 = {0.f, 0.f};
-      if (ADAM) {
-        float mx = u.mw[r].x, my = u.mw[r].y, vx = u.vw[r].x, vy = u.vw[r].y;
-        d.x = adam_moments(d.x, mx, vx, dw.adam, ac);
-        d.y = adam_moments(d.y, my, vy, dw.adam, ac);
-        m = f32x2{mx, my};
-        v2 = f32x2{vx, vy};
-      }
-      f32x2 v = {u.wsrc[r].x - dw.eta * d.x, u.wsrc[r].y - dw.eta * d.y};
-      if (LAST) {
-        v.x = (v.x - u.snap[r].x) / dw.lam;
-        v.y = (v.y - u.snap[r].y) / dw.lam;
-      }
-      const int i = i0 + 16 * wi + 4 * lg + r, j = j0 + 32 * wj + 2 * li;
-      const bool in = i < dw.M && j < dw.N;
-      const int64_t e = wo + (int64_t)i * dw.ldw + j;
-      f32x2* sink = reinterpret_cast<f32x2*>(dw.sink) + (lane & 31);
-      f32x2* dst = in ? reinterpret_cast<f32x2*>(dw.w_dst + e) : sink;
-      if (LAST)
-        *dst = v;
-      else
-        __builtin_nontemporal_store(v, dst);
-      if (ADAM) {
-        __builtin_nontemporal_store(m, in ? reinterpret_cast<f32x2*>(dw.adam.mw + e) : sink);
-        __builtin_nontemporal_store(v2, in ? reinterpret_cast<f32x2*>(dw.adam.vw + e) : sink);
-      }
-    }
-    if (bias_wave) {
-      // lane groups 1..3 hold partial sums of the same column of dZ as
-      // group 0: add them in a fixed order
-      const float p1 = __shfl(u.bsum, li + 16), p2 = __shfl(u.bsum, li + 32), p3 = __shfl(u.bsum, li + 48);
-      float tot = ((u.bsum + p1) + p2) + p3;
-      const int i = i0 + 16 * wi + li;
-      if (lg == 0 && i < dw.M) {
-        const int64_t e = wo + i;
-        if (ADAM) {
-          float m = u.mb, v2 = u.vb;
-          tot = adam_moments(tot, m, v2, dw.adam, ac);
-          dw.adam.mb[e] = m;
-          dw.adam.vb[e] = v2;
-        }
-        const float nb = u.bsrc - dw.eta * tot;
-        dw.b_dst[e] = LAST ? (nb - u.bsnap) / dw.lam : nb;
-      }
-    }
-  };
 
   // Per block t: wait for its loads; store the update of block t-1 while
   // the memory pipeline is empty (a store issued behind the next block's
@@ -354,13 +380,13 @@ __global__ __launch_bounds__(NT_S) void gemm_f32_strip_bwd_kernel(GemmArgs dx, G
     wait_lgkm0();
     wait_vm<0>();
     barrier();
-    if (t > 0) weight_store(t - 1, held);
-    load_operands(t, held);
-    if (t + 1 < T) fire_block(s, t + 1, (t & 1) ? zs0 : zs1, (t & 1) ? ws0 : ws1, wave, lane);
-    weight_mma(zs, ws, held);
+    if (t > 0) up.store(held, wo, BLK * (t - 1), j0, bias);
+    up.load(held, wo, BLK * t, j0, bias);
+    if (t + 1 < T) fire_block<FIRE_WAVES>(s, t + 1, (t & 1) ? zs0 : zs1, (t & 1) ? ws0 : ws1, wave, lane);
+    up.mma(zs, ws, hs, held, bias);
     dx_part(zs + oxa, ws + oxb, ax);
   }
-  weight_store(T - 1, held);
+  up.store(held, wo, BLK * (T - 1), j0, bias);
   // dZ_l = acc * [H_l > 0]; lane: rows 16w + 4lg + r, columns 4li + (0..3)
   wait_lgkm0();
   float* out = reinterpret_cast<float*>(dx.out) + (int64_t)worker * dx.ostride;
