@@ -107,14 +107,17 @@ __device__ __forceinline__ void fire_block(const StripCtx& s, int t, float* zs, 
 //     x the strip's 64 columns, as 4 blocks of 16 x 16; block cb covers
 //     columns 4*(0..15) + cb, so one 16-byte LDS read of W gives a lane its
 //     operand of all four blocks.  K = the block's 64 rows i: lane group g
-//     supplies i = 16g + 4c + e in slice (c, e); four groups c of four
-//     slices, each reading A once (i = 16g + 4c .. +3 of row 16w + li) and
-//     B per slice.
+//     supplies i = 16c + 4g + e in slice (c, e); four groups c of four
+//     slices, each reading A once (i = 16c + 4g .. +3 of row 16w + li) and
+//     B per slice.  Group c covers rows 16c .. 16c + 15 of the block, so the
+//     groups past the layer's last row (zeros in both tiles) are skipped.
 //   * weight gradient: rows i 16wi + 0..15 (wi = w / 2) x columns j
 //     32wj + 2*(0..15) + (0, 1) (wj = w % 2) of the block's 64 x 64, as 2
 //     blocks of 16 x 16 read with one 8-byte LDS read of H per slice.
 //     K = the mini-batch rows: lane group g supplies m = 16c + 4g + e in
 //     slice (c, e); eight groups c of four slices.
+//     A wave whose 16 rows i all lie past the layer's last row skips its
+//     MFMAs (only the last block of a ragged layer has such rows).
 // Every wave runs its weight-gradient part first, then its input-gradient
 // part: the older wave of a SIMD wins the MFMA arbitration, so in the other
 // order one wave's update epilogue ran while its partner had no MFMAs left.
@@ -125,12 +128,20 @@ struct DxFrag {
   f32x4 a, b[4];
 };
 
-// pa: row 16w + li, column 16g of the dZ block; pb: row 16g, column 4li of
+// pa: row 16w + li, column 4g of the dZ block; pb: row 4g, column 4li of
 // the W block
 __device__ __forceinline__ void dx_read(const float* pa, const float* pb, int c, DxFrag& f) {
-  f.a = *reinterpret_cast<const f32x4*>(pa + 4 * c);
+  f.a = *reinterpret_cast<const f32x4*>(pa + 16 * c);
 #pragma unroll
-  for (int e = 0; e < 4; ++e) f.b[e] = *reinterpret_cast<const f32x4*>(pb + WS * (4 * c + e));
+  for (int e = 0; e < 4; ++e) f.b[e] = *reinterpret_cast<const f32x4*>(pb + WS * (16 * c + e));
+}
+
+__device__ __forceinline__ void dx_mma(const DxFrag& f, f32x4 (&acc)[4]) {
+#pragma unroll
+  for (int e = 0; e < 4; ++e)
+#pragma unroll
+    for (int cb = 0; cb < 4; ++cb)
+      acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(f.a[e], f.b[e][cb], acc[cb], 0, 0, 0);
 }
 
 __device__ __forceinline__ void dx_part(const float* pa, const float* pb, f32x4 (&acc)[4]) {
@@ -143,13 +154,19 @@ __device__ __forceinline__ void dx_part(const float* pa, const float* pb, f32x4 
       dx_read(pa, pb, c + 1, f[(c + 1) & 1]);
       __builtin_amdgcn_sched_group_barrier(0x100, 5, 0);  // the next group's LDS reads first
     }
-#pragma unroll
-    for (int e = 0; e < 4; ++e)
-#pragma unroll
-      for (int cb = 0; cb < 4; ++cb)
-        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(f[c & 1].a[e], f[c & 1].b[e][cb], acc[cb], 0, 0, 0);
+    dx_mma(f[c & 1], acc);
     __builtin_amdgcn_sched_group_barrier(0x008, 16, 0);  // then this group's MFMAs
     __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// The last block of a layer whose rows end inside it: only its first nc
+// groups (1 <= nc < 4) hold rows of the layer
+__device__ __forceinline__ void dx_part_tail(const float* pa, const float* pb, int nc, f32x4 (&acc)[4]) {
+  for (int c = 0; c < nc; ++c) {
+    DxFrag f;
+    dx_read(pa, pb, c, f);
+    dx_mma(f, acc);
   }
 }
 
@@ -258,7 +275,7 @@ struct StripUpdate {
 
   // the block's weight gradient from the dZ block zs and the strip hs, and
   // W_src from the W block ws
-  __device__ __forceinline__ void mma(const float* zs, const float* ws, const float* hs, Update& u,
+  __device__ __forceinline__ void mma(const float* zs, const float* ws, const float* hs, Update& u, int i0,
                                       bool bias) const {
     u.bsum = 0.f;
     if (bias && wj == 0)
@@ -360,7 +377,9 @@ __global__ __launch_bounds__(NT_S) void gemm_f32_strip_bwd_kernel(GemmArgs dx, G
   // the bias is updated by the strip at j0 == 0
   const bool bias = j0 == 0;
   // per-lane offsets of the input-gradient reads (floats from the tile's start)
-  const int oxa = ZS * (16 * wave + li) + 16 * lg, oxb = WS * 16 * lg + 4 * li;
+  const int oxa = ZS * (16 * wave + li) + 4 * lg, oxb = WS * 4 * lg + 4 * li;
+  // groups of 16 rows of the last block that hold rows of the layer
+  const int nc_last = (dw.M - BLK * (T - 1) + 15) / 16;
   f32x4 ax[4];
 #pragma unroll
   for (int b = 0; b < 4; ++b) ax[b] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -383,7 +402,7 @@ __global__ __launch_bounds__(NT_S) void gemm_f32_strip_bwd_kernel(GemmArgs dx, G
     if (t > 0) up.store(held, wo, BLK * (t - 1), j0, bias);
     up.load(held, wo, BLK * t, j0, bias);
     if (t + 1 < T) fire_block<FIRE_WAVES>(s, t + 1, (t & 1) ? zs0 : zs1, (t & 1) ? ws0 : ws1, wave, lane);
-    up.mma(zs, ws, hs, held, bias);
+    up.mma(zs, ws, hs, held, BLK * t, bias);
     dx_part(zs + oxa, ws + oxb, ax);
   }
   up.store(held, wo, BLK * (T - 1), j0, bias);

@@ -5,7 +5,8 @@ strips of 64 reach 1024 (one workgroup per compute unit at a time), so these
 shapes use many workers: 64 x 16 and 128 x 8 strips.
 
 Shapes: strips and row blocks with ragged ends (996 and 1004 are not
-multiples of 64), a row stride padded past the width (996 -> 1000), a
+multiples of 64; 968 leaves 8 rows in the last block, so most of its MFMA
+groups are skipped), a row stride padded past the width (996 -> 1000), a
 mini-batch below the 128 rows the schedule holds (m = 100), several local
 steps (the round's last step stores the normalized displacement), two
 rounds, Adam as the local rule.  Gates as in the full-size tests
@@ -30,6 +31,7 @@ ADAM = (0.9, 0.999, 1e-8)
 STRIP_CASES = [
     # name, dims, n, lam, m, eta, rounds, N, data[, adam]
     ("strip_ragged", (96, 996, 1004, 12), 64, 2, 100, 0.02, 2, 64 * 300, "sparse_teacher2"),
+    ("strip_short_tail", (96, 1000, 968, 12), 64, 2, 128, 0.02, 2, 64 * 300, "sparse_teacher2"),
     ("strip_two_hidden", (64, 512, 768, 512, 10), 128, 3, 128, 0.02, 2, 128 * 256, "sparse_teacher2"),
     ("strip_adam", (64, 516, 512, 10), 128, 3, 120, 0.002, 2, 128 * 256, "sparse_teacher2", ADAM),
 ]
