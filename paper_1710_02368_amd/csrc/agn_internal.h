@@ -114,6 +114,11 @@ hipError_t launch_gemm_f32_dl_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStr
 // block in LDS), used when gemm_f32_strip_ok
 bool gemm_f32_strip_ok(const GemmArgs& dx, const GemmArgs& dw);
 hipError_t launch_gemm_f32_strip_bwd(const GemmArgs& dx, const GemmArgs& dw, hipStream_t s);
+// the first layer's weight gradient + update as 64-row strips of W_0 (the
+// dZ_1 strip in LDS, the gathered data rows streamed), used when
+// gemm_f32_strip_dw_ok
+bool gemm_f32_strip_dw_ok(const GemmArgs& dw);
+hipError_t launch_gemm_f32_strip_dw(const GemmArgs& dw, hipStream_t s);
 struct HeadDwArgs;
 // the first layer's direct-load weight gradient with the output layer's
 // weight gradient + update (C <= 10) folded into the same launch

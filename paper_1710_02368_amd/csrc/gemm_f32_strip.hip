@@ -31,6 +31,8 @@
 //   * W block, 64 x 64, unpadded: it is read only along its rows.
 // A load instruction fills 1 KB of the tile; each lane loads the global chunk
 // that belongs at its 16 bytes, or a zeroed page for padding and past an edge.
+#include <type_traits>
+
 #include "direct_load.h"
 
 namespace agn {
@@ -420,6 +422,155 @@ __global__ __launch_bounds__(NT_S) void gemm_f32_strip_bwd_kernel(GemmArgs dx, G
   }
 }
 
+// ---------------------------------------------------------------------------
+// The first layer's weight gradient as strips of its rows: dW_0 = dZ_1^T X_b
+// (X_b: the worker's mini-batch rows of the data set, K = m) fused with the
+// update of W_0 and b_0 (Algorithm 1, gradient line and local step).  A
+// workgroup owns one worker and one strip of 64 rows i of W_0 (64 units of
+// the first hidden layer): dZ_1[:, strip] (128 x 64) stays in LDS for the
+// whole launch, and the workgroup walks the blocks of 64 columns j (inputs).
+// Per block only the gathered X_b[:, block] (128 x 64) travels into LDS
+// (direct loads, double-buffered, issued by four waves); W_src, and on a
+// round's last step W_snap, come into registers for the update.  The product
+// and the update's lane layout are those of the backward strip kernel's
+// weight-gradient part (dZ strip as A, X block as B), so the bias gradient
+// comes from the A fragments of the first block.
+
+// Source of this lane's 16 bytes in load instruction q of the X block whose
+// row r is batch row r of worker k (data-set row k*S + (tb + r) mod S),
+// columns col0 .. col0 + 63; padding, rows >= m and columns >= ncol read
+// zeros.
+__device__ __forceinline__ const float* xblock_src(const float* x, int64_t ldx, int64_t rowk, int64_t S, int64_t tb,
+                                                   int m, int col0, int ncol, int q, int lane, const float* zero) {
+  const int f = 256 * q + 4 * lane;
+  const int r = f / HS, c = f - r * HS;
+  const int gc = col0 + c;
+  if (c >= 64 || r >= m || gc >= ncol) return zero;
+  int64_t j = tb + r;
+  if (j >= S) j -= S;
+  return x + (rowk + j) * ldx + gc;
+}
+
+template <bool LAST>
+__global__ __launch_bounds__(512) void gemm_f32_strip_dw_kernel(GemmArgs dw) {
+  __shared__ __attribute__((aligned(16))) float zs[Z_F];
+  __shared__ __attribute__((aligned(16))) float xs0[H_F];
+  __shared__ __attribute__((aligned(16))) float xs1[H_F];
+  const int tid = threadIdx.x, lane = tid & 63, li = lane & 15, lg = lane >> 4;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 7;  // uniform: the roles branch per wave
+  const int wi = wave >> 1, wj = wave & 1;
+  const int nstrip = (dw.M + STRIP - 1) / STRIP;
+  const int logical = xcd_remap(blockIdx.x, (int)gridDim.x);
+  const int worker = logical / nstrip, i0 = (logical % nstrip) * STRIP;
+  const int T = (dw.N + BLK - 1) / BLK;
+  const int m = dw.K;
+  const float* dz = reinterpret_cast<const float*>(dw.a.ptr) + (int64_t)worker * dw.a.wstride;
+  const float* x = reinterpret_cast<const float*>(dw.b.ptr);
+  const int64_t S = dw.g.S, rowk = (int64_t)worker * S;
+  const int64_t tb = (gather_step(dw.g) * dw.g.mb) % S;
+  // the loads of X block t into dst; instruction q is issued by wave q % NW
+  auto fire_x = [&](auto nw, int t, float* dst) {
+    constexpr int NW = decltype(nw)::value;
+#pragma unroll
+    for (int u = 0; u < (H_Q + NW - 1) / NW; ++u) {
+      const int q = wave + NW * u;
+      if (q < H_Q)
+        fire(xblock_src(x, dw.b.ld, rowk, S, tb, m, BLK * t, dw.N, q, lane, dw.zero), lds_off(dst) + 1024 * q);
+    }
+  };
+
+  // prologue: the dZ strip and X block 0, issued by every wave
+#pragma unroll
+  for (int u = 0; u < (Z_Q + 7) / 8; ++u) {
+    const int q = wave + 8 * u;
+    if (q < Z_Q) fire(tile_src<ZS>(dz, dw.a.ld, 0, m, i0, dw.M, q, lane, dw.zero), lds_off(zs) + 1024 * q);
+  }
+  fire_x(std::integral_constant<int, 8>{}, 0, xs0);
+
+  const int64_t wo = (int64_t)worker * dw.pstride;
+  const int owa = ZS * 4 * lg + 16 * wi + li, owb = HS * 4 * lg + 32 * wj + 2 * li;
+  // this lane's rows of the update: i0 + 16wi + 4lg + r (clamped for the loads)
+  int64_t rowo[4];
+  bool rin[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int i = i0 + 16 * wi + 4 * lg + r;
+    rin[r] = i < dw.M;
+    rowo[r] = wo + (int64_t)min(i, dw.M - 1) * dw.ldw;
+  }
+  f32x4 aw[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  f32x2 wsrc[4], snap[4];
+  float bsum = 0.f;
+
+  // the update of block t (columns j0 = 64t + 32wj + 2li, +1): its operands
+  // (UPL loads) and its stores (exactly 4, past an edge into the sink)
+  constexpr int UPL = LAST ? 8 : 4;
+  auto load_update = [&](int t) {
+    const int j = min(BLK * t + 32 * wj + 2 * li, dw.N - 2);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      wsrc[r] = *reinterpret_cast<const f32x2*>(dw.w_src + rowo[r] + j);
+      if (LAST) snap[r] = *reinterpret_cast<const f32x2*>(dw.w_snap + rowo[r] + j);
+    }
+  };
+  auto store_update = [&](int t) {
+    const int j = BLK * t + 32 * wj + 2 * li;
+    f32x2* sink = reinterpret_cast<f32x2*>(dw.sink) + (lane & 31);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      f32x2 v = {wsrc[r].x - dw.eta * aw[0][r], wsrc[r].y - dw.eta * aw[1][r]};
+      if (LAST) {
+        v.x = (v.x - snap[r].x) / dw.lam;
+        v.y = (v.y - snap[r].y) / dw.lam;
+      }
+      f32x2* dst = rin[r] && j < dw.N ? reinterpret_cast<f32x2*>(dw.w_dst + rowo[r] + j) : sink;
+      if (LAST)
+        *dst = v;
+      else
+        __builtin_nontemporal_store(v, dst);
+    }
+  };
+
+  // Per block t: wait for its loads; issue the loads of block t+1 (waves
+  // 0-3); the product of block t from LDS; then its update's stores and the
+  // update operands of block t+1.  Those two sets of memory operations
+  // (4 + UPL per wave) are younger than every direct load a wave waits for
+  // at the next block, so they stay in flight across the barrier; a store
+  // or load issued at the start of a block waited behind that block's
+  // direct loads.
+  load_update(0);
+  for (int t = 0; t < T; ++t) {
+    const float* xs = (t & 1) ? xs1 : xs0;
+    wait_lgkm0();
+    if (t == 0)
+      wait_vm<UPL>();
+    else
+      wait_vm<4 + UPL>();
+    barrier();
+    if (t + 1 < T && wave < 4) fire_x(std::integral_constant<int, 4>{}, t + 1, (t & 1) ? xs0 : xs1);
+    if (t == 0 && wj == 0) {
+      dw_part<true>(zs + owa, xs + owb, aw, bsum);
+    } else {
+      float unused = 0.f;
+      dw_part<false>(zs + owa, xs + owb, aw, unused);
+    }
+    store_update(t);
+    if (t + 1 < T) load_update(t + 1);
+  }
+  if (wj == 0) {
+    // the bias of rows i0 + 16wi + li: lane groups 1..3 hold partial sums
+    // of the same column of dZ_1 as group 0, added in a fixed order
+    const float p1 = __shfl(bsum, li + 16), p2 = __shfl(bsum, li + 32), p3 = __shfl(bsum, li + 48);
+    const float tot = ((bsum + p1) + p2) + p3;
+    const int i = i0 + 16 * wi + li;
+    if (lg == 0 && i < dw.M) {
+      const int64_t e = wo + i;
+      const float nb = dw.b_src[e] - dw.eta * tot;
+      dw.b_dst[e] = LAST ? (nb - dw.b_snap[e]) / dw.lam : nb;
+    }
+  }
+}
+
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
 }  // namespace
@@ -463,6 +614,33 @@ hipError_t launch_gemm_f32_strip_bwd(const GemmArgs& dx, const GemmArgs& dw, hip
   } else {
     AGN_LAUNCH((gemm_f32_strip_bwd_kernel<false, false>), grid, block, 0, s, dx, dw);
   }
+  return hipGetLastError();
+}
+
+// The strip schedule of the first layer's weight gradient: gathered data
+// rows as B (a batch within a shard), dZ_1 as A, SGD as the local rule, a
+// mini-batch of at most 128 rows, 16-byte rows, and enough strips (workers x
+// 64-row strips of W_0) to give every compute unit several workgroups.
+bool gemm_f32_strip_dw_ok(const GemmArgs& dw) {
+  if (dw.epi != EPI_DW_UPDATE || !dw.zero || !dw.sink || dw.adam.on || dw.w_dst16) return false;
+  if (!dw.b.gather || dw.a.gather || dw.K < 1 || dw.K > ROWS || dw.K > dw.g.S) return false;
+  if (dw.M % 4 || dw.N % 4 || dw.N < 2) return false;
+  const void* ptrs[] = {dw.a.ptr, dw.b.ptr, dw.w_src, dw.w_dst, dw.zero, dw.sink};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return false;
+  if (dw.last && !aligned16(dw.w_snap)) return false;
+  if (dw.a.ld % 4 || dw.a.wstride % 4 || dw.b.ld % 4 || dw.ldw % 4 || dw.pstride % 4) return false;
+  const int64_t groups = (int64_t)dw.batch * ((dw.M + STRIP - 1) / STRIP);
+  return groups >= kStripMinGroups && groups < (1 << 30);
+}
+
+hipError_t launch_gemm_f32_strip_dw(const GemmArgs& dw, hipStream_t s) {
+  if (!gemm_f32_strip_dw_ok(dw)) return hipErrorInvalidValue;
+  const dim3 grid((unsigned)(dw.batch * ((dw.M + STRIP - 1) / STRIP))), block(512);
+  if (dw.last)
+    AGN_LAUNCH((gemm_f32_strip_dw_kernel<true>), grid, block, 0, s, dw);
+  else
+    AGN_LAUNCH((gemm_f32_strip_dw_kernel<false>), grid, block, 0, s, dw);
   return hipGetLastError();
 }
 
