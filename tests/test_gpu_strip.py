@@ -1,8 +1,10 @@
-"""The strip schedule of a float32 hidden layer's backward launch (input
-gradient and weight gradient + update sharing each weight block in LDS)
-against the oracle.  The library takes that schedule when workers x column
-strips of 64 reach 1024 (one workgroup per compute unit at a time), so these
-shapes use many workers: 64 x 16 and 128 x 8 strips.
+"""The strip schedules against the oracle: the backward launch of a float32
+hidden layer (input gradient and weight gradient + update sharing each
+weight block in LDS) and, with SGD, the first layer's weight gradient +
+update as 64-row strips of W_0 (gathered data rows streamed past a dZ_1
+strip held in LDS).  The library takes them when workers x strips of 64
+reach 1024 (one workgroup per compute unit at a time), so these shapes use
+many workers: 64 x 16 and 128 x 8 strips.
 
 Shapes: strips and row blocks with ragged ends (996 and 1004 are not
 multiples of 64; 968 leaves 8 rows in the last block, so most of its MFMA
