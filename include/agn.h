@@ -241,6 +241,52 @@ const char* agn_last_error(const agn_ctx* ctx);
 /* Free everything (waits for the stream first).  NULL is a no-op. */
 void agn_destroy(agn_ctx* ctx);
 
+/* ---- checkpoint / resume ---------------------------------------------- */
+
+/* The complete state of a context between rounds, so that a context with
+ * the same configuration continues the run exactly where it was saved
+ * (Algorithm 1 keeps no other state across rounds): the central variable;
+ * each worker's last pulled copy of it, from which its next round starts;
+ * the round counter (the workers' local step counter t = round * lambda +
+ * i, which picks the mini-batches); the commit bookkeeping behind the
+ * staleness of each commit (commits applied so far, and per worker the
+ * count at its last pull); the per-row losses of the last round (what
+ * agn_loss reports); and, with Adam as the local rule, each worker's two
+ * moment estimates.  The deltas of the last round are not part of it:
+ * agn_debug_delta returns AGN_ESTATE until a round has run after
+ * agn_set_state.
+ *
+ * Layout of the state (HOST memory, native byte order): a header (magic
+ * "AGNSTATE", format version 1, the configuration: L, m, n, lambda, dtype,
+ * optimizer, normalization, staleness scaling, dims, eta, Adam's beta1,
+ * beta2, eps, P; the round counter, the commit counter, num_samples of the
+ * rounds so far (-1: none), the worker that committed last); then n int64
+ * pull counters, n int64 staleness values of the last round's commits, the
+ * n * lambda * m float32 per-row losses; then float32 vectors of P
+ * parameters in the packed layout of agn_central: the central variable,
+ * the n pulled copies in worker order, and with Adam the n first-moment and
+ * the n second-moment vectors. */
+
+/* Size in bytes of the state of ctx (-1 for a NULL context). */
+int64_t agn_state_bytes(const agn_ctx* ctx);
+
+/* Write the state of ctx into out (HOST, exactly agn_state_bytes(ctx)
+ * bytes, caller-owned).  Waits for the work enqueued on the context's
+ * stream first.  AGN_EINVAL for a NULL out or another size. */
+int agn_get_state(agn_ctx* ctx, void* out, int64_t bytes);
+
+/* Replace the state of ctx by a state written by agn_get_state (HOST,
+ * `bytes` bytes, read during the call only).  ctx must have the same
+ * configuration as the context the state was taken from: layer widths, m,
+ * n, lambda, eta, dtype, commit rule and staleness scaling, and the local
+ * rule (select Adam with agn_set_optimizer before restoring an Adam state).
+ * Everything is checked on the host before any device work: AGN_EINVAL
+ * (state unchanged) for another size, magic, format version or
+ * configuration, or inconsistent counters.  The bf16 copies of the pulled
+ * copies (bf16 contexts) are rebuilt from the float32 ones, as the commit
+ * writes them.  Returns after the copies have completed. */
+int agn_set_state(agn_ctx* ctx, const void* in, int64_t bytes);
+
 /* ---- test hooks (not on the timed path) ------------------------------- */
 
 /* Before the first round only (AGN_ESTATE otherwise): set the central

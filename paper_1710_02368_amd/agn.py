@@ -29,7 +29,7 @@ EXPORTED = [
     "agn_worker_params", "agn_debug_batch_indices", "agn_set_kernel_timing",
     "agn_kernel_timing", "agn_kernel_class_work", "agn_debug_delta", "agn_set_normalization",
     "agn_set_optimizer", "agn_evaluate", "agn_temporal_efficiency", "agn_set_staleness_scaling",
-    "agn_staleness", "agn_evaluate_noalloc",
+    "agn_staleness", "agn_evaluate_noalloc", "agn_state_bytes", "agn_get_state", "agn_set_state",
 ]
 
 
@@ -84,6 +84,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         "agn_central": (i32, [vp, vp]),
         "agn_loss": (i32, [vp, vp]),
         "agn_num_params": (i64, [vp]),
+        "agn_state_bytes": (i64, [vp]),
+        "agn_get_state": (i32, [vp, vp, i64]),
+        "agn_set_state": (i32, [vp, vp, i64]),
         "agn_last_error": (ctypes.c_char_p, [vp]),
         "agn_destroy": (None, [vp]),
         "agn_set_central": (i32, [vp, vp]),
@@ -231,6 +234,20 @@ def agn_set_central(ctx, inp):
     _check(load_library().agn_set_central(ctx, ctypes.c_void_p(inp.data_ptr())), ctx)
 
 
+def agn_state_bytes(ctx) -> int:
+    return int(load_library().agn_state_bytes(ctx))
+
+
+def agn_get_state(ctx, out):
+    """out: a writable, C-contiguous host buffer (numpy uint8) of agn_state_bytes bytes."""
+    _check(load_library().agn_get_state(ctx, ctypes.c_void_p(out.ctypes.data), int(out.nbytes)), ctx)
+
+
+def agn_set_state(ctx, inp):
+    """inp: a C-contiguous host buffer (numpy uint8) holding a state from agn_get_state."""
+    _check(load_library().agn_set_state(ctx, ctypes.c_void_p(inp.ctypes.data), int(inp.nbytes)), ctx)
+
+
 def agn_worker_params(ctx, worker: int, out):
     _check(load_library().agn_worker_params(ctx, int(worker), ctypes.c_void_p(out.data_ptr())), ctx)
 
@@ -319,6 +336,18 @@ class AGN:
         out = torch.empty(self.P, dtype=torch.float32, device="cuda")
         agn_worker_params(self.ctx, k, out)
         return out
+
+    def get_state(self):
+        """The context's state (checkpoint) as a numpy uint8 array on the host."""
+        import numpy as np
+        out = np.empty(agn_state_bytes(self.ctx), dtype=np.uint8)
+        agn_get_state(self.ctx, out)
+        return out
+
+    def set_state(self, state):
+        """Restore a state taken by get_state (a context of the same configuration)."""
+        import numpy as np
+        agn_set_state(self.ctx, np.ascontiguousarray(state, dtype=np.uint8))
 
     def delta(self, k):
         torch = _torch()

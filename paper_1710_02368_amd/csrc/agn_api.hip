@@ -95,6 +95,7 @@ struct agn_ctx {
   int64_t eval_N = 0;                  // rows of the last agn_evaluate call
   unsigned char* scratch = nullptr;    // this device's scratch array (agn_evaluate_noalloc)
   int last_committer = 0;              // worker that committed last (its pulled copy is the central variable)
+  int have_deltas = 0;                 // the delta buffers hold the last round's deltas (not after agn_set_state)
   int capturing = 0;
   int untimed = 0;                     // launch without timing events (agn_evaluate_noalloc)
   hipStream_t ls = nullptr;           // stream the launch sequence is enqueued on
@@ -889,6 +890,7 @@ int agn_round(agn_ctx* c, const agn_data* d, const int32_t* order) {
   }
   c->N_fixed = d->num_samples;
   c->last_committer = order[c->n - 1];
+  c->have_deltas = 1;
   ++c->rounds;
   for (int j = 0; j < c->n; ++j) c->pulled_version[order[j]] = c->version + j + 1;
   c->version += c->n;
@@ -989,6 +991,192 @@ void agn_destroy(agn_ctx* c) {
   delete c;
 }
 
+// ---- checkpoint / resume ---------------------------------------------------
+
+namespace {
+
+constexpr char kStateMagic[8] = {'A', 'G', 'N', 'S', 'T', 'A', 'T', 'E'};
+constexpr int32_t kStateVersion = 1;
+
+struct StateHeader {
+  char magic[8];
+  int32_t version, L, m, n, lam, dtype, optimizer, normalize, staleness_scaling;
+  int32_t dims[AGN_MAX_LAYERS + 1];
+  float eta, beta1, beta2, adam_eps;
+  int64_t P, rounds, commits, num_samples, last_committer;
+};
+
+StateHeader state_header(const agn_ctx* c) {
+  StateHeader h;
+  std::memset(&h, 0, sizeof(h));
+  std::memcpy(h.magic, kStateMagic, sizeof(h.magic));
+  h.version = kStateVersion;
+  h.L = c->L;
+  h.m = c->m;
+  h.n = c->n;
+  h.lam = c->lam;
+  h.dtype = c->dtype;
+  h.optimizer = c->optimizer;
+  h.normalize = c->normalize;
+  h.staleness_scaling = c->staleness_scaling;
+  for (int l = 0; l <= c->L; ++l) h.dims[l] = c->dims[l];
+  h.eta = c->eta;
+  h.beta1 = c->optimizer == AGN_OPT_ADAM ? c->beta1 : 0.f;
+  h.beta2 = c->optimizer == AGN_OPT_ADAM ? c->beta2 : 0.f;
+  h.adam_eps = c->optimizer == AGN_OPT_ADAM ? c->adam_eps : 0.f;
+  h.P = c->P;
+  h.rounds = c->rounds;
+  h.commits = c->version;
+  h.num_samples = c->N_fixed;
+  h.last_committer = c->last_committer;
+  return h;
+}
+
+// float32 vectors of P parameters in the state: central, n pulled copies,
+// and with Adam 2n moment vectors
+int64_t state_vectors(const agn_ctx* c) { return 1 + (int64_t)c->n * (c->optimizer == AGN_OPT_ADAM ? 3 : 1); }
+int64_t state_loss_floats(const agn_ctx* c) { return (int64_t)c->n * c->lam * c->m; }
+int64_t state_size(const agn_ctx* c) {
+  return (int64_t)sizeof(StateHeader) + 2 * (int64_t)c->n * (int64_t)sizeof(int64_t) +
+         (state_loss_floats(c) + state_vectors(c) * c->P) * (int64_t)sizeof(float);
+}
+
+// device vector v of the state (padded layout, P_pad floats)
+float* state_vector(agn_ctx* c, int64_t v) {
+  if (v == 0) return c->central;
+  --v;
+  if (v < c->n) return c->snap + v * c->P_pad;
+  v -= c->n;
+  if (v < c->n) return c->mom_m + v * c->P_pad;
+  return c->mom_v + (v - c->n) * c->P_pad;
+}
+
+// padded <-> packed on the host (the layout of agn_central)
+void pack_host(const PackArgs& pa, const float* padded, float* packed) {
+  for (int t = 0; t < pa.ntensors; ++t) {
+    const TensorDesc& d = pa.t[t];
+    for (int r = 0; r < d.rows; ++r)
+      std::memcpy(packed + d.packed_off + (int64_t)r * d.cols, padded + d.padded_off + (int64_t)r * d.ld,
+                  (size_t)d.cols * sizeof(float));
+  }
+}
+void unpack_host(const PackArgs& pa, const float* packed, float* padded) {
+  for (int t = 0; t < pa.ntensors; ++t) {
+    const TensorDesc& d = pa.t[t];
+    for (int r = 0; r < d.rows; ++r)
+      std::memcpy(padded + d.padded_off + (int64_t)r * d.ld, packed + d.packed_off + (int64_t)r * d.cols,
+                  (size_t)d.cols * sizeof(float));
+  }
+}
+
+// the first field of h that differs from the configuration of c, or nullptr
+const char* state_mismatch(const agn_ctx* c, const StateHeader& h) {
+  const StateHeader o = state_header(c);
+  if (std::memcmp(h.magic, kStateMagic, sizeof(h.magic)) != 0) return "magic (not an AGN state)";
+  if (h.version != kStateVersion) return "format version";
+  if (h.L != o.L) return "number of layers";
+  for (int l = 0; l <= AGN_MAX_LAYERS; ++l)
+    if (h.dims[l] != o.dims[l]) return "layer widths";
+  if (h.m != o.m) return "mini-batch size m";
+  if (h.n != o.n) return "number of workers n";
+  if (h.lam != o.lam) return "lambda";
+  if (h.dtype != o.dtype) return "dtype";
+  if (h.optimizer != o.optimizer) return "local rule (select Adam with agn_set_optimizer before restoring an Adam state)";
+  if (h.normalize != o.normalize) return "commit rule (agn_set_normalization)";
+  if (h.staleness_scaling != o.staleness_scaling) return "staleness scaling (agn_set_staleness_scaling)";
+  if (std::memcmp(&h.eta, &o.eta, sizeof(float)) != 0) return "eta";
+  if (std::memcmp(&h.beta1, &o.beta1, 3 * sizeof(float)) != 0) return "Adam's beta1, beta2 or eps";
+  if (h.P != o.P) return "number of parameters";
+  return nullptr;
+}
+
+}  // namespace
+
+int64_t agn_state_bytes(const agn_ctx* c) { return c ? state_size(c) : -1; }
+
+int agn_get_state(agn_ctx* c, void* out, int64_t bytes) {
+  if (int r = check_ctx(c)) return r;
+  if (!out) return fail(c, AGN_EINVAL, "out is NULL");
+  if (bytes != state_size(c))
+    return fail(c, AGN_EINVAL, "the state needs exactly " + std::to_string(state_size(c)) + " bytes");
+  if (int r = set_device(c)) return r;
+  HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  char* p = static_cast<char*>(out);
+  const StateHeader h = state_header(c);
+  std::memcpy(p, &h, sizeof(h));
+  p += sizeof(h);
+  for (int k = 0; k < c->n; ++k) {
+    const int64_t pv = c->pulled_version[k];
+    std::memcpy(p + k * sizeof(int64_t), &pv, sizeof(pv));
+    const int64_t st = k < (int)c->last_staleness.size() ? c->last_staleness[k] : 0;
+    std::memcpy(p + (c->n + k) * sizeof(int64_t), &st, sizeof(st));
+  }
+  p += 2 * c->n * sizeof(int64_t);
+  const int64_t nl = state_loss_floats(c);
+  HIP_CHECK(c, hipMemcpyAsync(p, c->loss, nl * sizeof(float), hipMemcpyDeviceToHost, c->stream));
+  p += nl * sizeof(float);
+  std::vector<float> tmp((size_t)c->P_pad);
+  for (int64_t v = 0; v < state_vectors(c); ++v) {
+    HIP_CHECK(c, hipMemcpyAsync(tmp.data(), state_vector(c, v), c->P_pad * sizeof(float), hipMemcpyDeviceToHost,
+                                c->stream));
+    HIP_CHECK(c, hipStreamSynchronize(c->stream));
+    pack_host(c->pack, tmp.data(), reinterpret_cast<float*>(p));
+    p += c->P * sizeof(float);
+  }
+  HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  return AGN_OK;
+}
+
+int agn_set_state(agn_ctx* c, const void* in, int64_t bytes) {
+  if (int r = check_ctx(c)) return r;
+  if (!in) return fail(c, AGN_EINVAL, "in is NULL");
+  if (bytes != state_size(c))
+    return fail(c, AGN_EINVAL, "a state of this context has exactly " + std::to_string(state_size(c)) + " bytes");
+  const char* p = static_cast<const char*>(in);
+  StateHeader h;
+  std::memcpy(&h, p, sizeof(h));
+  if (const char* what = state_mismatch(c, h))
+    return fail(c, AGN_EINVAL, std::string("the state was taken from another configuration: ") + what);
+  // the counters must be consistent: rounds * n commits, pull counters in
+  // [0, commits], a worker that committed last
+  if (h.rounds < 0 || h.commits != h.rounds * h.n || h.last_committer < 0 || h.last_committer >= h.n ||
+      (h.rounds > 0 && h.num_samples < h.n) || (h.rounds == 0 && h.num_samples != -1))
+    return fail(c, AGN_EINVAL, "inconsistent round counters in the state");
+  std::vector<int64_t> pv(c->n), st(c->n);
+  std::memcpy(pv.data(), p + sizeof(h), c->n * sizeof(int64_t));
+  std::memcpy(st.data(), p + sizeof(h) + c->n * sizeof(int64_t), c->n * sizeof(int64_t));
+  for (int k = 0; k < c->n; ++k)
+    if (pv[k] < 0 || pv[k] > h.commits) return fail(c, AGN_EINVAL, "inconsistent pull counters in the state");
+  if (int r = set_device(c)) return r;
+  HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  p += sizeof(h) + 2 * c->n * sizeof(int64_t);
+  const int64_t nl = state_loss_floats(c);
+  HIP_CHECK(c, hipMemcpyAsync(c->loss, p, nl * sizeof(float), hipMemcpyHostToDevice, c->stream));
+  HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  p += nl * sizeof(float);
+  std::vector<float> tmp((size_t)c->P_pad, 0.f);  // padding stays zero
+  for (int64_t v = 0; v < state_vectors(c); ++v) {
+    unpack_host(c->pack, reinterpret_cast<const float*>(p), tmp.data());
+    HIP_CHECK(c, hipMemcpyAsync(state_vector(c, v), tmp.data(), c->P_pad * sizeof(float), hipMemcpyHostToDevice,
+                                c->stream));
+    HIP_CHECK(c, hipStreamSynchronize(c->stream));
+    p += c->P * sizeof(float);
+  }
+  if (c->dtype == AGN_BF16)  // the bf16 copies of the pulls, as the commit writes them
+    HIP_CHECK(c, launch_copy_bf16(c->snap, c->snap16, (int64_t)c->n * c->P_pad, c->stream));
+  const int64_t rounds = h.rounds;
+  HIP_CHECK(c, hipMemcpyAsync(c->round_dev, &rounds, sizeof(rounds), hipMemcpyHostToDevice, c->stream));
+  HIP_CHECK(c, hipStreamSynchronize(c->stream));
+  c->rounds = h.rounds;
+  c->version = h.commits;
+  c->N_fixed = h.num_samples;
+  c->last_committer = (int)h.last_committer;
+  c->pulled_version = pv;
+  c->last_staleness = h.rounds > 0 ? st : std::vector<int64_t>();
+  c->have_deltas = 0;
+  return AGN_OK;
+}
+
 int agn_set_central(agn_ctx* c, const float* in) {
   if (int r = check_ctx(c)) return r;
   if (!in) return fail(c, AGN_EINVAL, "in is NULL");
@@ -1014,7 +1202,7 @@ int agn_debug_delta(agn_ctx* c, int32_t worker, float* out) {
   if (int r = check_ctx(c)) return r;
   if (!out) return fail(c, AGN_EINVAL, "out is NULL");
   if (worker < 0 || worker >= c->n) return fail(c, AGN_EINVAL, "worker out of range");
-  if (c->rounds == 0) return fail(c, AGN_ESTATE, "no round has run yet");
+  if (!c->have_deltas) return fail(c, AGN_ESTATE, "no round has run since the context was created or restored");
   if (int r = set_device(c)) return r;
   const float* delta = c->buf[(c->lam - 1) & 1] + (int64_t)worker * c->P_pad;
   HIP_CHECK(c, launch_pack(c->pack, delta, out, c->stream));

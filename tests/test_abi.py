@@ -68,6 +68,14 @@ def test_null_arguments_are_rejected():
     assert isinstance(agn.agn_last_error(None), str)
 
 
+def test_null_state_arguments_are_rejected():
+    lib = agn.load_library()
+    assert lib.agn_state_bytes(None) == -1
+    assert lib.agn_get_state(None, None, 0) == -1
+    assert lib.agn_set_state(None, None, 0) == -1
+    assert "null context" in agn.agn_last_error(None)
+
+
 def test_null_evaluate_arguments_are_rejected():
     lib = agn.load_library()
     assert lib.agn_evaluate(None, None, None, None, None) == -1
