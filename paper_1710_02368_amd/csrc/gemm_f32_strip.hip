@@ -162,16 +162,6 @@ __device__ __forceinline__ void dx_part(const float* pa, const float* pb, f32x4 
   }
 }
 
-// The last block of a layer whose rows end inside it: only its first nc
-// groups (1 <= nc < 4) hold rows of the layer
-__device__ __forceinline__ void dx_part_tail(const float* pa, const float* pb, int nc, f32x4 (&acc)[4]) {
-  for (int c = 0; c < nc; ++c) {
-    DxFrag f;
-    dx_read(pa, pb, c, f);
-    dx_mma(f, acc);
-  }
-}
-
 struct DwFrag {
   float a[4];
   f32x2 b[4];
@@ -277,7 +267,7 @@ struct StripUpdate {
 
   // the block's weight gradient from the dZ block zs and the strip hs, and
   // W_src from the W block ws
-  __device__ __forceinline__ void mma(const float* zs, const float* ws, const float* hs, Update& u, int i0,
+  __device__ __forceinline__ void mma(const float* zs, const float* ws, const float* hs, Update& u,
                                       bool bias) const {
     u.bsum = 0.f;
     if (bias && wj == 0)
@@ -380,8 +370,6 @@ __global__ __launch_bounds__(NT_S) void gemm_f32_strip_bwd_kernel(GemmArgs dx, G
   const bool bias = j0 == 0;
   // per-lane offsets of the input-gradient reads (floats from the tile's start)
   const int oxa = ZS * (16 * wave + li) + 4 * lg, oxb = WS * 4 * lg + 4 * li;
-  // groups of 16 rows of the last block that hold rows of the layer
-  const int nc_last = (dw.M - BLK * (T - 1) + 15) / 16;
   f32x4 ax[4];
 #pragma unroll
   for (int b = 0; b < 4; ++b) ax[b] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -404,7 +392,7 @@ __global__ __launch_bounds__(NT_S) void gemm_f32_strip_bwd_kernel(GemmArgs dx, G
     if (t > 0) up.store(held, wo, BLK * (t - 1), j0, bias);
     up.load(held, wo, BLK * t, j0, bias);
     if (t + 1 < T) fire_block<FIRE_WAVES>(s, t + 1, (t & 1) ? zs0 : zs1, (t & 1) ? ws0 : ws1, wave, lane);
-    up.mma(zs, ws, hs, held, BLK * t, bias);
+    up.mma(zs, ws, hs, held, bias);
     dx_part(zs + oxa, ws + oxb, ax);
   }
   up.store(held, wo, BLK * (T - 1), j0, bias);
