@@ -270,7 +270,7 @@ def traffic_class(name):
         return "bwd"
     if "gemm_f32_dl_dw_kernel" in name or "gemm_f32_strip_dw_kernel" in name or "<false, false, 3>" in name:
         return "dw_first"
-    if "<true, true" in name or "_fwd8_kernel" in name:
+    if "<true, true" in name or "_fwd8_kernel" in name or "gemm_bf16_dl_big_kernel" in name:
         return "fwd"
     return None
 

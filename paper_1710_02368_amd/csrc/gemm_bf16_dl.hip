@@ -4,11 +4,12 @@
 // three K steps ahead of their use, and the fragments of the next K step
 // are read from LDS while the MFMAs of the current one run.
 //
-// Tile: TR x TR outputs per workgroup of 4 waves, TR = 128 (two workgroups
-// per CU) or 256 (forward products with a whole 256-row mini-batch per
-// tile, one workgroup per CU); wave (wm, wn) owns a TR/2 x TR/2 quarter as
-// blocks of v_mfma_f32_32x32x16_bf16; K in steps of 32 (two MFMA slices of
-// 16).  In one MFMA, lane (li = l%32, lh = l/32) supplies
+// Tile: TR x TR outputs per workgroup, TR = 128 (4 waves, two workgroups
+// per CU; wave (wm, wn) owns a 64 x 64 quarter) or 256 (forward products
+// with a whole 256-row mini-batch per tile, one workgroup of 8 waves per
+// CU; wave (wm, wn) owns 128 x 64), as blocks of v_mfma_f32_32x32x16_bf16;
+// K in steps of 32 (two MFMA slices of 16).  In one MFMA, lane (li = l%32,
+// lh = l/32) supplies
 // A[i = li][k = 8*lh .. 8*lh+7] and B[k = 8*lh .. 8*lh+7][j = li], 16 bytes
 // each; the 128-tile accumulators are laid out as the shared epilogues
 // expect.
@@ -79,9 +80,9 @@ __device__ __forceinline__ int ks_byte(int k, int c) { return (Geo<TR>::CPK * k 
 //   K-strided: k row RPI*j + l/CPK, column chunk (l%CPK) ^ key(k) (k rows
 //     may be gathered data-set rows: batch index kk of worker w is row
 //     w*S + (tb + kk) mod S, tb = t*m mod S, with K <= S).
-template <bool KC, int TR>
+template <bool KC, int TR, int IPW_ = Geo<TR>::IPW>
 struct Loader {
-  static constexpr int IPW = Geo<TR>::IPW, CPK = Geo<TR>::CPK, RPI = Geo<TR>::RPI;
+  static constexpr int IPW = IPW_, CPK = Geo<TR>::CPK, RPI = Geo<TR>::RPI;
   const uint16_t* zero;
   // the lane's source at k0 = 0 in instruction u: its row (KC) or column
   // chunk (KS), clamped into the matrix -- rows and columns past the edge
@@ -154,11 +155,10 @@ struct Frags {
   bf16x8 a[Geo<TR>::NB][2], b[Geo<TR>::NB][2];
 };
 
-template <bool KC, int TR>
-__device__ __forceinline__ void frag(const char* tile, int outer_off, int li, int lh,
-                                     bf16x8 (&f)[Geo<TR>::NB][2]) {
+template <bool KC, int TR, int NBLK = Geo<TR>::NB>
+__device__ __forceinline__ void frag(const char* tile, int outer_off, int li, int lh, bf16x8 (&f)[NBLK][2]) {
 #pragma unroll
-  for (int b = 0; b < Geo<TR>::NB; ++b)
+  for (int b = 0; b < NBLK; ++b)
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       if (KC) {
@@ -256,124 +256,14 @@ __host__ __device__ inline int tiles16(const GemmArgs& g) {
   return ((g.M + TR - 1) / TR) * ((g.N + TR - 1) / TR) * g.batch;
 }
 
-// Epilogue of a 256 x 256 tile of the forward or input-gradient product:
-// two passes of 128 rows.  In pass h the two waves with wm == h stage
-// their accumulators in LDS, then every thread stores 16-byte row chunks
-// (8 bf16 or 4 float32 columns) with their operands (bias, ReLU mask)
-// loaded up front from indices clamped into the matrix (element by element
-// only where a chunk crosses the matrix edge).
-template <int EPI>
-__device__ __forceinline__ void out_epilogue_big(const GemmArgs& g, int worker, int m0, int n0,
-                                                 const f32x16 (&acc)[4][4], float* et) {
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1, li = lane & 31, lh = lane >> 5;
-  constexpr bool F32 = EPI == EPI_FWD_LINEAR;
-  constexpr int CW = F32 ? 4 : 8;     // columns per chunk
-  constexpr int CPR = 256 / CW;       // chunks per row
-  constexpr int NC = 128 * CPR / NT;  // chunks per thread and pass
-  const int colc = (tid % CPR) * CW;  // this thread's chunk column (the same for all its chunks)
-  const int cbase = n0 + colc;
-  float bv[CW];
-  if (EPI == EPI_FWD_RELU || EPI == EPI_FWD_LINEAR) {
-#pragma unroll
-    for (int j = 0; j < CW; ++j) bv[j] = g.bias[(int64_t)worker * g.bstride + min(cbase + j, g.N - 1)];
-  }
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    uint4 mv[NC];
-    if (EPI == EPI_DX_MASK) {
-      const int cm = min(cbase, (g.N - 1) / 8 * 8);  // (rows of the mask are padded to 8)
-#pragma unroll
-      for (int u = 0; u < NC; ++u) {
-        const int row = min(m0 + 128 * h + (tid + NT * u) / CPR, g.M - 1);
-        mv[u] = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(g.mask) +
-                                                (int64_t)worker * g.mstride + (int64_t)row * g.ldm + cm);
-      }
-    }
-    if (h == 1) __syncthreads();  // every thread is done reading pass 0's rows
-    if (wm == h) {
-#pragma unroll
-      for (int bi = 0; bi < 4; ++bi)
-#pragma unroll
-        for (int bj = 0; bj < 4; ++bj)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            et[(32 * bi + 8 * (r >> 2) + 4 * lh + (r & 3)) * EPI_BIG_LD + wn * 128 + 32 * bj + li] = acc[bi][bj][r];
-    }
-    __syncthreads();
-    if (EPI == EPI_FWD_RELU || EPI == EPI_FWD_LINEAR) {
-#pragma unroll
-      for (int j = 0; j < CW; j += 2) asm volatile("" ::"v"(bv[j]), "v"(bv[j + 1]));
-    }
-    if (EPI == EPI_DX_MASK) {
-#pragma unroll
-      for (int u = 0; u < NC; ++u) asm volatile("" ::"v"(mv[u].x), "v"(mv[u].w));
-    }
-    if (cbase >= g.N) continue;
-    const bool whole = cbase + CW <= g.N;
-#pragma unroll
-    for (int u = 0; u < NC; ++u) {
-      const int rl = (tid + NT * u) / CPR, row = m0 + 128 * h + rl;
-      if (row >= g.M) continue;
-      float v[CW];
-#pragma unroll
-      for (int j = 0; j < CW; j += 4) {
-        const float4 a = *reinterpret_cast<const float4*>(et + rl * EPI_BIG_LD + colc + j);
-        v[j] = a.x;
-        v[j + 1] = a.y;
-        v[j + 2] = a.z;
-        v[j + 3] = a.w;
-      }
-      const int64_t o = (int64_t)worker * g.ostride + (int64_t)row * g.ldo + cbase;
-      if (F32) {
-        float* out = reinterpret_cast<float*>(g.out) + o;
-#pragma unroll
-        for (int j = 0; j < CW; ++j) v[j] += bv[j];
-        if (whole) {
-          *reinterpret_cast<float4*>(out) = make_float4(v[0], v[1], v[2], v[3]);
-        } else {
-          for (int j = 0; j < CW && cbase + j < g.N; ++j) out[j] = v[j];
-        }
-      } else {
-        uint16_t hv[CW];
-        if (EPI == EPI_FWD_RELU) {
-#pragma unroll
-          for (int j = 0; j < CW; ++j) {
-            const float z = v[j] + bv[j];
-            hv[j] = f32_to_bf16_rne(z > 0.f ? z : 0.f);
-          }
-        } else {  // EPI_DX_MASK
-          const uint32_t mw[4] = {mv[u].x, mv[u].y, mv[u].z, mv[u].w};
-#pragma unroll
-          for (int j = 0; j < CW; ++j) {
-            const uint16_t m = (uint16_t)(mw[j / 2] >> (16 * (j % 2)));
-            hv[j] = f32_to_bf16_rne(bf16_to_f32(m) > 0.f ? v[j] : 0.f);
-          }
-        }
-        uint16_t* out = reinterpret_cast<uint16_t*>(g.out) + o;
-        if (whole) {
-          uint4 pk;
-          pk.x = (uint32_t)hv[0] | ((uint32_t)hv[1] << 16);
-          pk.y = (uint32_t)hv[2] | ((uint32_t)hv[3] << 16);
-          pk.z = (uint32_t)hv[4] | ((uint32_t)hv[5] << 16);
-          pk.w = (uint32_t)hv[6] | ((uint32_t)hv[7] << 16);
-          *reinterpret_cast<uint4*>(out) = pk;
-        } else {
-          for (int j = 0; j < CW && cbase + j < g.N; ++j) out[j] = hv[j];
-        }
-      }
-    }
-  }
-}
-
-// One TR x TR output tile (logical tile id `logical`) of one product; lds:
-// LDS_DL (TR = 128) or LDS_BIG (TR = 256) bytes.  256 x 256 tiles serve the
-// forward and input-gradient products only.
+// One TR x TR output tile (logical tile id `logical`) of one product (TR =
+// 128; the 256 x 256 forward tiles have a kernel of their own below); lds:
+// LDS_DL bytes.
 template <bool A_KC, bool B_KC, int EPI, int TR>
 __device__ __forceinline__ void tile_dl16(const GemmArgs& g, const int logical, char* lds) {
   constexpr bool DW = EPI == EPI_DW_UPDATE;
   constexpr int NB = Geo<TR>::NB, IPW = Geo<TR>::IPW, STAGE = Geo<TR>::STAGE;
-  static_assert(TR == 128 || !DW, "weight-gradient tiles are 128 x 128");
+  static_assert(TR == 128, "four-wave tiles are 128 x 128");
   const int tid = threadIdx.x;
   const Lanes q{tid >> 6, tid & 63, (tid >> 6) >> 1, (tid >> 6) & 1, tid & 31, (tid & 63) >> 5};
   const int tm = (g.M + TR - 1) / TR, tn = (g.N + TR - 1) / TR;
@@ -464,9 +354,7 @@ __device__ __forceinline__ void tile_dl16(const GemmArgs& g, const int logical, 
   wait_lgkm0();
   barrier();
 
-  if constexpr (TR == 256) {
-    out_epilogue_big<EPI>(g, worker, m0, n0, acc, reinterpret_cast<float*>(lds));
-  } else if constexpr (!DW) {
+  if constexpr (!DW) {
     out_epilogue_lds<EPI>(g, worker, m0, n0, acc, reinterpret_cast<float*>(lds));
   } else {
     const AdamCoef ac = g.adam.on ? adam_coef(g.g, g.adam) : AdamCoef{1.f, 1.f};
@@ -499,11 +387,235 @@ __global__ __launch_bounds__(NT) void gemm_bf16_dl_kernel(GemmArgs g) {
   tile_dl16<A_KC, B_KC, EPI, 128>(g, xcd_remap(blockIdx.x, tiles16<128>(g)), lds);
 }
 
+// ---------------------------------------------------------------------------
+// Forward product in 256 x 256 tiles with eight waves (two per SIMD): wave
+// (wm, wn) = (w / 4, w % 4) owns rows 128wm .. +127 and columns 64wn .. +63
+// of the tile as 4 x 2 blocks of 32 x 32, and issues two load instructions
+// per operand and K step (instruction j = 2w + u).  With one wave per SIMD
+// a wave held up in instruction issue (waiting for room in the memory
+// pipeline), on its LDS reads or at the barrier left the matrix core idle;
+// with two, the other wave of the SIMD runs its MFMAs meanwhile.
+constexpr int NT_BIG = 512;
+constexpr int IPW_BIG = 2;
+
+struct FragsBig {
+  bf16x8 a[4][2], b[2][2];
+};
+
+// the wave's fragments of one K step, slice 0's reads first
+__device__ __forceinline__ void read_frags_big(const char* stage, int wm, int wn, int li, int lh, FragsBig& f) {
+  const char* tb = stage + Geo<256>::TILE;
+#pragma unroll
+  for (int sl = 0; sl < 2; ++sl) {
+#pragma unroll
+    for (int b = 0; b < 4; ++b)
+      f.a[b][sl] = *reinterpret_cast<const bf16x8*>(stage + kc_byte(wm * 128 + 32 * b + li, 2 * sl + lh));
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+      f.b[b][sl] = *reinterpret_cast<const bf16x8*>(tb + kc_byte(wn * 64 + 32 * b + li, 2 * sl + lh));
+  }
+}
+
+// K step kt: wait until step kt's loads have landed (at most the loads of
+// steps kt+1 and kt+2 still in flight) and every wave is done reading the
+// stage of step kt-1; start the loads of step kt+3 into that stage; read
+// this step's fragments and run its MFMAs.  The fragments are read in the
+// step that uses them (one set of registers: the other wave of the SIMD
+// runs its MFMAs meanwhile); slice 0's MFMAs start while slice 1's reads
+// are in flight.
+__device__ __forceinline__ void k_step_big(int wave, int wm, int wn, int li, int lh, const char* rd, char* wr,
+                                           const uint16_t* const (&src)[2 * IPW_BIG], f32x16 (&acc)[4][2]) {
+  __builtin_amdgcn_sched_barrier(0);
+  wait_lgkm0();
+  wait_vm<2 * IPW_BIG * (NS - 2)>();
+  barrier();
+  const uint32_t wa = lds_off(wr) + 1024 * IPW_BIG * wave;
+#pragma unroll
+  for (int u = 0; u < IPW_BIG; ++u) fire(src[u], wa + 1024 * u);
+#pragma unroll
+  for (int u = 0; u < IPW_BIG; ++u) fire(src[IPW_BIG + u], wa + Geo<256>::TILE + 1024 * u);
+  FragsBig f;
+  read_frags_big(rd, wm, wn, li, lh, f);
+#pragma unroll
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+      for (int bj = 0; bj < 2; ++bj)
+        acc[bi][bj] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[bi][s], f.b[bj][s], acc[bi][bj], 0, 0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// Epilogue of the eight-wave tile: two passes of 128 rows; in pass h the
+// four waves with wm == h stage their accumulators in LDS, then every
+// thread stores 16-byte row chunks (8 bf16 or 4 float32 columns) with the
+// bias loaded up front from indices clamped into the matrix (element by
+// element only where a chunk crosses the matrix edge).
+template <int EPI>
+__device__ __forceinline__ void out_epilogue_big8(const GemmArgs& g, int worker, int m0, int n0,
+                                                  const f32x16 (&acc)[4][2], float* et) {
+  static_assert(EPI == EPI_FWD_RELU || EPI == EPI_FWD_LINEAR, "forward products only");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 2, wn = wave & 3, li = lane & 31, lh = lane >> 5;
+  constexpr bool F32 = EPI == EPI_FWD_LINEAR;
+  constexpr int CW = F32 ? 4 : 8;         // columns per chunk
+  constexpr int CPR = 256 / CW;           // chunks per row
+  constexpr int NC = 128 * CPR / NT_BIG;  // chunks per thread and pass
+  const int colc = (tid % CPR) * CW;      // this thread's chunk column (the same for all its chunks)
+  const int cbase = n0 + colc;
+  float bv[CW];
+#pragma unroll
+  for (int j = 0; j < CW; ++j) bv[j] = g.bias[(int64_t)worker * g.bstride + min(cbase + j, g.N - 1)];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    if (h == 1) __syncthreads();  // every thread is done reading pass 0's rows
+    if (wm == h) {
+#pragma unroll
+      for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+        for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            et[(32 * bi + 8 * (r >> 2) + 4 * lh + (r & 3)) * EPI_BIG_LD + wn * 64 + 32 * bj + li] = acc[bi][bj][r];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < CW; j += 2) asm volatile("" ::"v"(bv[j]), "v"(bv[j + 1]));
+    if (cbase >= g.N) continue;
+    const bool whole = cbase + CW <= g.N;
+#pragma unroll
+    for (int u = 0; u < NC; ++u) {
+      const int rl = (tid + NT_BIG * u) / CPR, row = m0 + 128 * h + rl;
+      if (row >= g.M) continue;
+      float v[CW];
+#pragma unroll
+      for (int j = 0; j < CW; j += 4) {
+        const float4 a = *reinterpret_cast<const float4*>(et + rl * EPI_BIG_LD + colc + j);
+        v[j] = a.x;
+        v[j + 1] = a.y;
+        v[j + 2] = a.z;
+        v[j + 3] = a.w;
+      }
+      const int64_t o = (int64_t)worker * g.ostride + (int64_t)row * g.ldo + cbase;
+      if (F32) {
+        float* out = reinterpret_cast<float*>(g.out) + o;
+#pragma unroll
+        for (int j = 0; j < CW; ++j) v[j] += bv[j];
+        if (whole) {
+          *reinterpret_cast<float4*>(out) = make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+          for (int j = 0; j < CW && cbase + j < g.N; ++j) out[j] = v[j];
+        }
+      } else {
+        uint16_t hv[CW];
+#pragma unroll
+        for (int j = 0; j < CW; ++j) {
+          const float z = v[j] + bv[j];
+          hv[j] = f32_to_bf16_rne(z > 0.f ? z : 0.f);
+        }
+        uint16_t* out = reinterpret_cast<uint16_t*>(g.out) + o;
+        if (whole) {
+          uint4 pk;
+          pk.x = (uint32_t)hv[0] | ((uint32_t)hv[1] << 16);
+          pk.y = (uint32_t)hv[2] | ((uint32_t)hv[3] << 16);
+          pk.z = (uint32_t)hv[4] | ((uint32_t)hv[5] << 16);
+          pk.w = (uint32_t)hv[6] | ((uint32_t)hv[7] << 16);
+          *reinterpret_cast<uint4*>(out) = pk;
+        } else {
+          for (int j = 0; j < CW && cbase + j < g.N; ++j) out[j] = hv[j];
+        }
+      }
+    }
+  }
+}
+
 // 256 x 256 tiles, one workgroup per CU (LDS)
-template <bool A_KC, bool B_KC, int EPI>
-__global__ __launch_bounds__(NT) void gemm_bf16_dl_big_kernel(GemmArgs g) {
+template <int EPI>
+__global__ __launch_bounds__(NT_BIG) void gemm_bf16_dl_big_kernel(GemmArgs g) {
   __shared__ __attribute__((aligned(16))) char lds[LDS_BIG];
-  tile_dl16<A_KC, B_KC, EPI, 256>(g, xcd_remap(blockIdx.x, tiles16<256>(g)), lds);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6) & 7;
+  const int wm = wave >> 2, wn = wave & 3, li = lane & 31, lh = lane >> 5;
+  const int logical = xcd_remap(blockIdx.x, tiles16<256>(g));
+  const int tm = (g.M + 255) / 256, tn = (g.N + 255) / 256;
+  const int worker = logical / (tm * tn), rem = logical % (tm * tn);
+  const int m0 = (rem % tm) * 256, n0 = (rem / tm) * 256;
+  constexpr int STAGE = Geo<256>::STAGE;
+  char* const st0 = lds;
+  char* const st1 = lds + STAGE;
+  char* const st2 = lds + 2 * STAGE;
+  char* const st3 = lds + 3 * STAGE;
+
+  Loader<true, 256, IPW_BIG> la, lb;
+  la.init(g.a, g.g, g.zero, worker, m0, g.M, g.K, wave, lane);
+  lb.init(g.b, g.g, g.zero, worker, n0, g.N, g.K, wave, lane);
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int bi = 0; bi < 4; ++bi)
+#pragma unroll
+    for (int bj = 0; bj < 2; ++bj)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[bi][bj][r] = 0.f;
+
+  const int nk = (g.K + BK - 1) / BK;
+  {
+    // steps 0 .. NS-2 in flight (2*IPW_BIG load instructions per wave and step)
+    char* const stg[NS - 1] = {st0, st1, st2};
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s) {
+      const uint32_t wa = lds_off(stg[s]) + 1024 * IPW_BIG * wave;
+#pragma unroll
+      for (int u = 0; u < IPW_BIG; ++u) fire(la.src(s * BK, u), wa + 1024 * u);
+#pragma unroll
+      for (int u = 0; u < IPW_BIG; ++u) fire(lb.src(s * BK, u), wa + Geo<256>::TILE + 1024 * u);
+    }
+  }
+
+  // step kt reads stage kt % 4 and loads step kt + 3 into stage (kt + 3) % 4:
+  // from the precomputed full-step sources while that step lies inside K,
+  // else through the bounds checks (the zero page past K)
+  auto step = [&](auto full, const char* rd, char* wr, int kt) {
+    const int k0 = (kt + NS - 1) * BK;
+    const uint16_t* src[2 * IPW_BIG];
+#pragma unroll
+    for (int u = 0; u < IPW_BIG; ++u) {
+      if constexpr (decltype(full)::value) {
+        src[u] = la.src_full(k0, u);
+        src[IPW_BIG + u] = lb.src_full(k0, u);
+      } else {
+        src[u] = la.src(k0, u);
+        src[IPW_BIG + u] = lb.src(k0, u);
+      }
+    }
+    k_step_big(wave, wm, wn, li, lh, rd, wr, src, acc);
+  };
+  using Full = std::true_type;
+  using Checked = std::false_type;
+  const int nk4 = nk & ~3;
+  int nfast = (la.full_ok && lb.full_ok) ? g.K / BK - (NS - 1) : 0;  // steps kt whose step kt+3 is full
+  nfast = nfast > 0 ? nfast & ~3 : 0;
+  int kt = 0;
+  for (; kt < nfast && kt < nk4; kt += 4) {
+    step(Full{}, st0, st3, kt);
+    step(Full{}, st1, st0, kt + 1);
+    step(Full{}, st2, st1, kt + 2);
+    step(Full{}, st3, st2, kt + 3);
+  }
+  for (; kt < nk4; kt += 4) {
+    step(Checked{}, st0, st3, kt);
+    step(Checked{}, st1, st0, kt + 1);
+    step(Checked{}, st2, st1, kt + 2);
+    step(Checked{}, st3, st2, kt + 3);
+  }
+  if (nk4 < nk) step(Checked{}, st0, st3, nk4);
+  if (nk4 + 1 < nk) step(Checked{}, st1, st0, nk4 + 1);
+  if (nk4 + 2 < nk) step(Checked{}, st2, st1, nk4 + 2);
+  // every load (also those of the steps past the end) has landed and every
+  // wave is done reading the stages: the LDS is free for the epilogue
+  wait_vm<0>();
+  wait_lgkm0();
+  barrier();
+  out_epilogue_big8<EPI>(g, worker, m0, n0, acc, reinterpret_cast<float*>(lds));
 }
 
 // The backward products of one layer in one launch: input-gradient tiles
@@ -562,9 +674,9 @@ hipError_t launch_gemm_bf16_dl(int a_kc, int b_kc, const GemmArgs& g, hipStream_
   if (use_big(a_kc, b_kc, g)) {
     const dim3 grid(tiles16<256>(g));
     if (g.epi == EPI_FWD_RELU)
-      AGN_LAUNCH((gemm_bf16_dl_big_kernel<true, true, EPI_FWD_RELU>), grid, block, 0, s, g);
+      AGN_LAUNCH((gemm_bf16_dl_big_kernel<EPI_FWD_RELU>), grid, dim3(NT_BIG), 0, s, g);
     else
-      AGN_LAUNCH((gemm_bf16_dl_big_kernel<true, true, EPI_FWD_LINEAR>), grid, block, 0, s, g);
+      AGN_LAUNCH((gemm_bf16_dl_big_kernel<EPI_FWD_LINEAR>), grid, dim3(NT_BIG), 0, s, g);
     return hipGetLastError();
   }
   const dim3 grid(tiles16<128>(g));

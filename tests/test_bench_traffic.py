@@ -52,7 +52,7 @@ def test_traffic_classes():
     assert bench.traffic_class("void agn::(anonymous namespace)::gemm_f32_dl_dw_kernel<true>(x)") == "dw_first"
     assert bench.traffic_class("void agn::(anonymous namespace)::gemm_f32_strip_dw_kernel<false>(agn::GemmArgs)") == "dw_first"
     assert bench.traffic_class("void agn::(anonymous namespace)::gemm_f32_strip_bwd_kernel<false, false>(x)") == "bwd"
-    assert bench.traffic_class("void agn::(anonymous namespace)::gemm_bf16_dl_big_kernel<true, true, 0>(x)") == "fwd"
+    assert bench.traffic_class("void agn::(anonymous namespace)::gemm_bf16_dl_big_kernel<0>(agn::GemmArgs)") == "fwd"
     assert bench.traffic_class("void agn::(anonymous namespace)::gemm_f32_dl_fwd8_kernel<0>(agn::GemmArgs)") == "fwd"
     assert bench.traffic_class("void agn::(anonymous namespace)::head_dw_kernel<10>(x)") == "output_dw"
     assert bench.traffic_class("void agn::(anonymous namespace)::head_kernel<10, 16, false>(x)") == "output"
