@@ -302,3 +302,40 @@ def test_evaluate_full_size(name, rows, rounds):
     print(f"{name}: rows {rows}, row loss err {err:.2e}, near-tie rows {close}, "
           f"loss {res[0]:.5f}, acc {res[1]:.4f}", flush=True)
     g.close()
+
+
+def test_accumulated_commits_fail_to_converge_where_agn_does():
+    """The paper's motivating contrast (Section 2, the accumulated-gradient
+    DOWNPOUR divergence figure) on the library itself: the same workers,
+    learning rate, local steps and commit orders, once with the normalized
+    commit (Eq. 2 with Eq. 1's delta / lambda) and once committing the
+    accumulated update.  The central variable's loss, measured by
+    agn_evaluate after every round, falls in every round under AGN, and under
+    accumulated commits it does not, ending well above AGN's.  The same
+    workload pins the oracle's trajectories in test_oracle_pins.py; here each
+    measured loss is also held to the oracle's evaluation of the oracle's
+    central variable after the same round."""
+    agn = _agn()
+    dims, n, lam, eta, m, R = (20, 16, 4), 8, 10, 0.1, 16, 6
+    wl = W.small_workload("dv", dims, n, lam, m, eta, R, 4096, data="gauss_linear", order="permutation")
+    X, y = W.make_data(wl)
+    xd, yd = to_device(X, y)
+    xe, ye = to_device(X[:1024], y[:1024])
+    traj = {}
+    for normalize in (True, False):
+        g = agn.AGN(dims, n, lam, eta, m, seed=wl.seed, normalize=normalize)
+        o = AGNOracle(dims, n, lam, eta, m, seed=wl.seed, normalize=normalize)
+        losses = []
+        for order in W.commit_orders(wl):
+            g.round(xd, yd, order)
+            o.round(X, y, order)
+            loss, _, _ = g.evaluate(xe, ye)
+            ref = evaluate(unflat_params(o.central_flat(), dims), X[:1024], y[:1024])[0].mean()
+            assert abs(loss - ref) <= 1e-3 * max(1.0, abs(ref)), (normalize, len(losses), loss, ref)
+            losses.append(loss)
+        g.close()
+        traj[normalize] = np.array(losses)
+    agn_l, acc_l = traj[True], traj[False]
+    assert np.all(np.diff(agn_l) < 0), agn_l
+    assert not np.all(np.diff(acc_l) < 0), acc_l
+    assert acc_l[-1] > 1.5 * agn_l[-1] and acc_l.mean() > 1.5 * agn_l.mean(), (agn_l, acc_l)

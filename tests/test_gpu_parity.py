@@ -42,6 +42,12 @@ SMALL = [
     ("sgd_n1_lam1", (50, 70, 4), 1, 1, 130, 0.05, 3, 300, "gauss_linear", "sequential", "fp32"),
     ("wide_tiles", (96, 300, 300, 12), 5, 2, 70, 0.05, 2, 1000, "sparse_teacher2", "permutation", "fp32"),
     ("batch_of_one", (16, 8, 2), 2, 3, 1, 0.1, 3, 10, "gauss_linear", "permutation", "fp32"),
+    # the largest sizes the library accepts: AGN_MAX_LAYERS weight layers, and
+    # AGN_MAX_WORKERS workers (commit orders over 256 workers, staleness up
+    # to 255)
+    ("max_layers", (24, 20, 18, 22, 16, 20, 24, 18, 16, 20, 22, 18, 16, 20, 24, 18, 6), 2, 2, 12, 0.05, 2, 200,
+     "gauss_linear", "permutation", "fp32"),
+    ("max_workers", (20, 16, 5), 256, 2, 8, 0.05, 2, 256 * 40, "gauss_linear", "permutation", "fp32"),
     # output-layer paths: many classes (separate logits product + softmax kernel),
     # a hidden width beyond the fused kernel's reach, and a fused kernel whose
     # LDS-resident output weights exceed 64 KB
