@@ -402,6 +402,44 @@ def test_errors_leave_state_unchanged():
     g.close()
 
 
+def test_divergent_learning_rate_is_reported_not_fatal():
+    """A learning rate far too large for the model (eta = 1e5): the weights
+    grow by orders of magnitude per round and overflow float32 within a few
+    rounds, in the oracle as on the GPU.  The library keeps running (every
+    round returns success), round 1 still matches the oracle, and the
+    divergence shows where a caller looks for it: non-finite entries in the
+    per-worker losses of agn_loss and in the central variable; agn_evaluate
+    of the diverged central variable returns a non-finite mean loss and
+    predictions inside the class range."""
+    agn = _agn()
+    wl = W.small_workload("diverge", (20, 12, 4), 3, 2, 5, 1e5, 4, 60)
+    X, y = W.make_data(wl)
+    xd, yd = to_device(X, y)
+    g = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed)
+    o = AGNOracle(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed)
+    orders = W.commit_orders(wl)
+    with np.errstate(all="ignore"):
+        g.round(xd, yd, orders[0])
+        o.round(X, y, orders[0])
+        err, where = rel_err(g.central().cpu().numpy(), o.central_flat(), wl.dims)
+        assert err <= FP32_TOL_1, (where, err)
+        oracle_finite = [bool(np.isfinite(o.central_flat()).all())]
+        for order in orders[1:]:
+            g.round(xd, yd, order)
+            o.round(X, y, order)
+            oracle_finite.append(bool(np.isfinite(o.central_flat()).all()))
+    assert not oracle_finite[-1], oracle_finite                 # the oracle diverged too
+    c = g.central().cpu().numpy()
+    assert not np.isfinite(c).all()
+    assert not np.isfinite(g.loss().cpu().numpy()).all()
+    loss, acc, correct = g.evaluate(xd, yd)
+    assert not np.isfinite(loss) and 0 <= correct <= X.shape[0] and acc == correct / X.shape[0]
+    _, rl, rp = g.evaluate(xd, yd, row_outputs=True)
+    rp = rp.cpu().numpy()
+    assert rp.min() >= 0 and rp.max() < wl.dims[-1]
+    g.close()
+
+
 @pytest.mark.parametrize("dims,folded", [((100, 200, 136, 10), True), ((100, 200, 136, 12), False),
                                          ((100, 200, 10), True)])
 def test_output_layer_update_rides_in_first_layer_launch(dims, folded):
