@@ -122,3 +122,19 @@ def test_temporal_efficiency_rejects_bad_curves(ta, fa, tb, fb):
     with pytest.raises(agn.AGNError) as ei:
         agn.agn_temporal_efficiency(ta, fa, tb, fb)
     assert ei.value.code == -1
+
+
+def test_plain_c_program_uses_the_abi(tmp_path):
+    """agn.h compiles as ISO C99 with every warning an error, a C program links
+    against libagn.so, and the argument checks answer it as documented
+    (AGN_EINVAL with no context and a message; NULL contexts refused; Eq. 4
+    of two identical curves is 1).  No device is needed."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("no C compiler")
+    agn.load_library()
+    from tests.c_abi import build as c_build
+    exe = c_build.build(str(tmp_path))
+    r = subprocess.run([exe, "validate"], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0 and "0 failure(s)" in r.stdout, r.stdout + r.stderr
