@@ -402,6 +402,35 @@ def test_errors_leave_state_unchanged():
     g.close()
 
 
+def test_rounds_on_a_caller_stream_match_the_null_stream():
+    """A context bound to a stream the caller created (agn_set_stream, here a
+    torch stream of default priority) records and replays its round graph on
+    that stream: three rounds equal, bit for bit, the same rounds of a context
+    on the null stream, and the per-worker losses too."""
+    agn = _agn()
+    import torch
+    wl = W.small_workload("stream", (100, 70, 60, 10), 4, 3, 20, 0.05, 3, 400, order="permutation")
+    X, y = W.make_data(wl)
+    xd, yd = to_device(X, y)
+    orders = W.commit_orders(wl)
+    g0 = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed)
+    for order in orders:
+        g0.round(xd, yd, order)
+    ref_c, ref_l = g0.central().cpu().numpy(), g0.loss().cpu().numpy()
+    g0.close()
+    torch.cuda.synchronize()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        g1 = agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed)
+        for order in orders:
+            g1.round(xd, yd, order)
+        c1, l1 = g1.central(), g1.loss()
+    s.synchronize()
+    assert np.array_equal(c1.cpu().numpy(), ref_c)
+    assert np.array_equal(l1.cpu().numpy(), ref_l)
+    g1.close()
+
+
 def test_divergent_learning_rate_is_reported_not_fatal():
     """A learning rate far too large for the model (eta = 1e5): the weights
     grow by orders of magnitude per round and overflow float32 within a few
