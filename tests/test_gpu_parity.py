@@ -431,6 +431,37 @@ def test_rounds_on_a_caller_stream_match_the_null_stream():
     g1.close()
 
 
+def test_interleaved_contexts_keep_their_own_state():
+    """Two contexts in one process, a float32 and a bf16 one of different
+    shapes, their rounds interleaved: each ends bit for bit where it ends
+    when it runs alone (no state shared between contexts)."""
+    agn = _agn()
+    cases = [W.small_workload("ctx_a", (100, 70, 60, 10), 4, 3, 20, 0.05, 3, 400, order="permutation"),
+             W.small_workload("ctx_b", (136, 264, 200, 10), 3, 2, 40, 0.05, 3, 650, data="sparse_teacher2",
+                              order="permutation", dtype="bf16")]
+    data = [W.make_data(wl) for wl in cases]
+    dev = [to_device(X, y) for X, y in data]
+    orders = [W.commit_orders(wl) for wl in cases]
+
+    def make(wl):
+        return agn.AGN(wl.dims, wl.n, wl.lam, wl.eta, wl.m, seed=wl.seed, dtype=wl.dtype)
+
+    alone = []
+    for k, wl in enumerate(cases):
+        g = make(wl)
+        for order in orders[k]:
+            g.round(*dev[k], order)
+        alone.append(g.central().cpu().numpy())
+        g.close()
+    gs = [make(wl) for wl in cases]
+    for r in range(3):
+        for k in (1, 0):
+            gs[k].round(*dev[k], orders[k][r])
+    for k in range(2):
+        assert np.array_equal(gs[k].central().cpu().numpy(), alone[k]), cases[k].name
+        gs[k].close()
+
+
 def test_divergent_learning_rate_is_reported_not_fatal():
     """A learning rate far too large for the model (eta = 1e5): the weights
     grow by orders of magnitude per round and overflow float32 within a few
