@@ -13,6 +13,8 @@ namespace {
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float epi_f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t epi_u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int TB = 128;          // tile edge (M and N)
 constexpr int NT = 256;          // threads per workgroup
@@ -22,7 +24,12 @@ constexpr int EPI_BYTES = TB * EPI_LD * 4;
 // Weight-gradient epilogue through LDS: the float32 accumulator tile is
 // written to LDS, then every thread streams 16-byte chunks of rows (W_src
 // read, W_dst and its bf16 shadow written), so the master-weight traffic is
-// coalesced.  Needs 16-byte rows.
+// coalesced.  Needs 16-byte rows.  The master weights (and snapshot) come
+// in and the updated weights and their bf16 shadow go out as streaming
+// (non-temporal) accesses: each is touched once per local step, at the
+// wide workload 14 B per parameter of 200M-parameter layers, far beyond the
+// caches, where cached accesses only evicted the operands the products
+// share.
 __host__ __device__ inline bool dw_vec_ok(const GemmArgs& g) {
   const uintptr_t p = (uintptr_t)g.w_src | (uintptr_t)g.w_dst | (g.last ? (uintptr_t)g.w_snap : 0);
   return (p & 15) == 0 && ((uintptr_t)g.w_dst16 & 7) == 0 && g.ldw % 4 == 0 && g.pstride % 4 == 0 && g.N % 4 == 0;
@@ -49,8 +56,12 @@ __device__ __forceinline__ void dw_epilogue_lds(const GemmArgs& g, int worker, i
     for (int v = 0; v < PER; ++v) {
       const int c = tid + NT * (pass * PER + v), row = c / (TB / 4), col = 4 * (c % (TB / 4));
       const int64_t el = wo + (int64_t)min(m0 + row, g.M - 1) * g.ldw + min(n0 + col, g.N - 4);
-      w[v] = *reinterpret_cast<const float4*>(g.w_src + el);
-      if (LAST) sn[v] = *reinterpret_cast<const float4*>(g.w_snap + el);
+      const epi_f32x4 t = __builtin_nontemporal_load(reinterpret_cast<const epi_f32x4*>(g.w_src + el));
+      w[v] = make_float4(t.x, t.y, t.z, t.w);
+      if (LAST) {
+        const epi_f32x4 u = __builtin_nontemporal_load(reinterpret_cast<const epi_f32x4*>(g.w_snap + el));
+        sn[v] = make_float4(u.x, u.y, u.z, u.w);
+      }
     }
     if (pass == 0) {
       // the accumulator tile to LDS while they are in flight
@@ -85,13 +96,14 @@ __device__ __forceinline__ void dw_epilogue_lds(const GemmArgs& g, int worker, i
       if (LAST) {
         nw = make_float4((nw.x - sn[v].x) / g.lam, (nw.y - sn[v].y) / g.lam, (nw.z - sn[v].z) / g.lam,
                          (nw.w - sn[v].w) / g.lam);
-        *reinterpret_cast<float4*>(g.w_dst + e) = nw;
+        const epi_f32x4 dv = {nw.x, nw.y, nw.z, nw.w};
+        __builtin_nontemporal_store(dv, reinterpret_cast<epi_f32x4*>(g.w_dst + e));
       } else {
-        *reinterpret_cast<float4*>(g.w_dst + e) = nw;
-        uint2 h;
-        h.x = f32_to_bf16_rne(nw.x) | ((uint32_t)f32_to_bf16_rne(nw.y) << 16);
-        h.y = f32_to_bf16_rne(nw.z) | ((uint32_t)f32_to_bf16_rne(nw.w) << 16);
-        *reinterpret_cast<uint2*>(g.w_dst16 + e) = h;
+        const epi_f32x4 nv = {nw.x, nw.y, nw.z, nw.w};
+        __builtin_nontemporal_store(nv, reinterpret_cast<epi_f32x4*>(g.w_dst + e));
+        const epi_u32x2 h = {f32_to_bf16_rne(nw.x) | ((uint32_t)f32_to_bf16_rne(nw.y) << 16),
+                             f32_to_bf16_rne(nw.z) | ((uint32_t)f32_to_bf16_rne(nw.w) << 16)};
+        __builtin_nontemporal_store(h, reinterpret_cast<epi_u32x2*>(g.w_dst16 + e));
       }
     }
   }
