@@ -193,7 +193,7 @@ def measure_eval(agn, g, wl, xh, yh, Xh, yh_host, reps=20, cpu=True):
 
 
 KERNEL_SOURCES = os.path.join(ROOT, "paper_1710_02368_amd", "csrc")
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_{}.json")
 
 
 def kernel_source_digest():
@@ -213,7 +213,7 @@ def stored_traffic(workload, kernel_class):
     FETCH_SIZE / WRITE_SIZE passes (scaled by the copy calibration), or None
     when they were taken on other kernel sources or another workload."""
     try:
-        with open(TRAFFIC_FILE) as fh:
+        with open(TRAFFIC_FILE.format(workload)) as fh:
             t = json.load(fh)
     except (OSError, ValueError):
         return None
@@ -279,7 +279,7 @@ def summarize_traffic(d, workload):
     """FETCH_SIZE / WRITE_SIZE counter passes (rocprofv3 --pmc, csv output,
     under d/{bench,copy}_{FETCH_SIZE,WRITE_SIZE}/) -> HBM bytes per launch
     of each kernel class, scaled by what the same counter reads for the
-    1 GiB copy of --copy-calibration; written to profiles/traffic.json with
+    1 GiB copy of --copy-calibration; written to profiles/traffic_<workload>.json with
     the digest of the kernel sources, and printed as a text summary."""
     import collections
     import csv
@@ -321,7 +321,7 @@ def summarize_traffic(d, workload):
         f = sum(fkern[k]) / len(fkern[k])
         w = sum(wkern.get(k, [0.0])) / max(1, len(wkern.get(k, [0.0])))
         lines.append(f"  {k[:80]:80s} fetch {f / 1e6:9.2f} MB write {w / 1e6:9.2f} MB")
-    with open(TRAFFIC_FILE, "w") as fh:
+    with open(TRAFFIC_FILE.format(workload), "w") as fh:
         json.dump(out, fh, indent=1)
     print("\n".join(lines))
 
@@ -426,7 +426,7 @@ def main():
                          "for --workload (no GPU needed)")
     ap.add_argument("--summarize-traffic", metavar="DIR",
                     help="turn the FETCH_SIZE / WRITE_SIZE counter passes under DIR into "
-                         "profiles/traffic.json for --workload (no GPU needed)")
+                         "profiles/traffic_<workload>.json (no GPU needed)")
     args = ap.parse_args()
     if args.copy_calibration:
         copy_calibration()

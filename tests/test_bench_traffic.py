@@ -20,8 +20,8 @@ def write_pass(d, sub, counter, rows):
 
 def test_summarize_traffic(tmp_path, monkeypatch):
     d = str(tmp_path / "pmc")
-    out = tmp_path / "traffic.json"
-    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(out))
+    out = tmp_path / "traffic_mlp1000_n8.json"
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(tmp_path / "traffic_{}.json"))
     # the copy reads 2^30 bytes and writes 2^30: FETCH reads half (factor 2), WRITE all (factor 1)
     copy = "void at::native::elementwise_kernel<copy>"
     write_pass(d, "copy_FETCH_SIZE", "FETCH_SIZE", [("fill", 3.0), (copy, (1 << 20) / 2)])
@@ -41,7 +41,6 @@ def test_summarize_traffic(tmp_path, monkeypatch):
     assert b["launches_sampled"] == 2
     assert t["classes"]["commit"]["hbm_bytes_per_launch"] == 50.0 * 1024 * 2 + 5.0 * 1024
     # stored values apply only to these sources and this workload
-    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(out))
     assert bench.stored_traffic("mlp1000_n8", "bwd") == b["hbm_bytes_per_launch"]
     assert bench.stored_traffic("wide_bf16", "bwd") is None
 
