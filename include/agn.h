@@ -338,7 +338,8 @@ int agn_debug_batch_indices(agn_ctx* ctx, int32_t worker, int64_t step_t,
  * plus the bf16 copies of the pulls in bf16 mode;
  * for the classes with the update: the parameters they update read and
  * written once per local step, plus their bf16 shadow written in bf16
- * mode and Adam's two moment estimates read and written; for the output
+ * mode (and, for the hidden layers' backward launches, read by the input
+ * gradient) and Adam's two moment estimates read and written; for the output
  * layer: its activations read and gradients written).  AGN_K_EVAL: the
  * work of the last agn_evaluate call instead (its rows' inputs and the
  * weights read once, the logits written once), zero before the first.

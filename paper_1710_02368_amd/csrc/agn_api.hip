@@ -1259,6 +1259,9 @@ int agn_kernel_class_work(agn_ctx* c, int32_t cls, double* flops, double* bytes)
       for (int l = 1; l < (c->use_head ? L - 1 : L); ++l) {
         f += 4.0 * mac(l) * rows;
         b += upd * (mac(l) + c->dims[l + 1]);
+        // bf16: the input gradient reads the weights' bf16 shadow, a stream of
+        // its own (in float32 it shares the update's read of the weights)
+        if (c->dtype == AGN_BF16) b += 2.0 * (double)c->n * c->lam * mac(l);
       }
       break;
     case AGN_K_DW_FIRST:
