@@ -26,6 +26,16 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int HEAD_WAVE_ROWS = 1;                  // rows a wave processes together
 constexpr int HEAD_DMAX = 2048;                     // hidden width limit
+// dynamic LDS a workgroup may use (160 KB per CU on gfx950, less the
+// kernel's static LDS)
+constexpr int HEAD_LDS_CAP = 160 * 1024 - 2048;
+
+// Rows of W in LDS trimmed to the width (instances whose padded rows would
+// take more than half of the cap), and the floats per row
+__host__ __device__ constexpr bool head_trim(int cmax, int q4) { return cmax * 256 * q4 * 4 > HEAD_LDS_CAP / 2; }
+__host__ __device__ constexpr int head_pitch(int cmax, int q4, int d) {
+  return head_trim(cmax, q4) ? (d + 3) & ~3 : 256 * q4;
+}
 
 // Argmax order of the evaluation: a NaN beats any number, a larger value a
 // smaller one, and among equals (or NaNs) the lower class index wins.
@@ -43,13 +53,17 @@ __host__ __device__ constexpr int head_rows(bool eval) { return 4 * (eval ? EVAL
 // one row per wave; the evaluation variant runs many rows per wave instead)
 __host__ __device__ constexpr int head_split(int q4, bool eval) { return !eval && q4 >= 2 ? 2 : 1; }
 
-// LDS: W padded to CMAX rows x 256*Q4 columns (zeros outside C x d), then b.
-// Lane l owns the columns 4l + 256q .. +3 of every row, for the groups q of
-// its wave's share (all Q4 of them, or half when SP = 2 waves share a row):
-// it keeps them of its wave's rows of H in registers (all loaded at once,
-// 16 bytes at a time when the rows allow it) and reads W and writes the
-// input gradient 16 bytes at a time.  Padding rows and columns are zero, so
-// the loops are static and branch-free.
+// LDS: W as CMAX rows (zeros outside C x d), then b.  Lane l owns the
+// columns 4l + 256q .. +3 of every row, for the groups q of its wave's share
+// (all Q4 of them, or half when SP = 2 waves share a row): it keeps them of
+// its wave's rows of H in registers (all loaded at once, 16 bytes at a time
+// when the rows allow it) and reads W and writes the input gradient 16 bytes
+// at a time.  A row holds the 256*Q4 columns the lanes span (padding zero),
+// so the loops are static and branch-free -- except where that would take
+// more than half of a compute unit's LDS (head_trim): there a row holds d
+// rounded up to 4 floats, and a group past the row's end reads the row's
+// last four columns instead (its H is zero and its outputs are not stored).
+// At d = 2000, C <= 10 that makes 80 KB, two workgroups per compute unit.
 template <int CMAX, int Q4, bool EVAL>
 __global__ __launch_bounds__(256 * head_split(Q4, EVAL)) void head_kernel(HeadArgs a) {
   extern __shared__ float smem[];
@@ -64,11 +78,12 @@ __global__ __launch_bounds__(256 * head_split(Q4, EVAL)) void head_kernel(HeadAr
   const int blocks_per_worker = (a.m + RB - 1) / RB;
   const int k = blockIdx.x / blocks_per_worker;
   const int r0 = (blockIdx.x % blocks_per_worker) * RB;
-  const int d = a.d, C = a.C;
+  constexpr bool TRIM = head_trim(CMAX, Q4);
+  const int d = a.d, C = a.C, pitch = head_pitch(CMAX, Q4, d);
   const float* W = a.w + (int64_t)k * a.pstride;
   const float* bias = a.b + (int64_t)k * a.pstride;
   float* Ws = smem;
-  float* bs = smem + CMAX * LW;
+  float* bs = smem + CMAX * pitch;
   const int64_t t = gather_step(a.g);
 
   // rows of this wave: issue every load of H (and the labels) before
@@ -99,25 +114,53 @@ __global__ __launch_bounds__(256 * head_split(Q4, EVAL)) void head_kernel(HeadAr
   // loads first, unconditionally (row and column clamped into the padded W:
   // rows are ldw >= d floats, ldw a multiple of 8), then the LDS writes with
   // the parts outside C x d zeroed: the loads are in flight together
-  constexpr int NW4 = CMAX * LW / 4, WIT = (NW4 + NTH - 1) / NTH;
-  float4 wv[WIT];
+  if constexpr (TRIM) {
+    // thread tid takes the chunks tid + NTH*u of every row (at most the
+    // pitch's: NTH*CPT >= LW/4)
+    constexpr int CPT = (LW / 4 + NTH - 1) / NTH;
+    float4 wv[CMAX][CPT];
 #pragma unroll
-  for (int it = 0; it < WIT; ++it) {
-    const int e4 = min(tid + NTH * it, NW4 - 1);
-    const int c = min(e4 / (LW / 4), C - 1), i = min(4 * (e4 % (LW / 4)), (int)a.ldw - 4);
-    wv[it] = *reinterpret_cast<const float4*>(W + (int64_t)c * a.ldw + i);
-  }
+    for (int c = 0; c < CMAX; ++c)
 #pragma unroll
-  for (int it = 0; it < WIT; ++it) {
-    const int e4 = tid + NTH * it;
-    if (NW4 % NTH != 0 && e4 >= NW4) break;
-    const int c = e4 / (LW / 4), i = 4 * (e4 % (LW / 4));
-    float4 v = wv[it];
-    if (c >= C || i >= d) v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (i + 1 >= d) v.y = 0.f;
-    if (i + 2 >= d) v.z = 0.f;
-    if (i + 3 >= d) v.w = 0.f;
-    *reinterpret_cast<float4*>(Ws + c * LW + i) = v;
+      for (int u = 0; u < CPT; ++u) {
+        const int i = min(4 * (tid + NTH * u), (int)a.ldw - 4);
+        wv[c][u] = *reinterpret_cast<const float4*>(W + (int64_t)min(c, C - 1) * a.ldw + i);
+      }
+#pragma unroll
+    for (int c = 0; c < CMAX; ++c)
+#pragma unroll
+      for (int u = 0; u < CPT; ++u) {
+        const int i = 4 * (tid + NTH * u);
+        if (i >= pitch) continue;
+        float4 v = wv[c][u];
+        if (c >= C || i >= d) v = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (i + 1 >= d) v.y = 0.f;
+        if (i + 2 >= d) v.z = 0.f;
+        if (i + 3 >= d) v.w = 0.f;
+        *reinterpret_cast<float4*>(Ws + c * pitch + i) = v;
+      }
+  } else {
+    // the padded CMAX x LW block in row-major chunks, spread over the threads
+    constexpr int NW4 = CMAX * LW / 4, WIT = (NW4 + NTH - 1) / NTH;
+    float4 wv[WIT];
+#pragma unroll
+    for (int it = 0; it < WIT; ++it) {
+      const int e4 = min(tid + NTH * it, NW4 - 1);
+      const int c = min(e4 / (LW / 4), C - 1), i = min(4 * (e4 % (LW / 4)), (int)a.ldw - 4);
+      wv[it] = *reinterpret_cast<const float4*>(W + (int64_t)c * a.ldw + i);
+    }
+#pragma unroll
+    for (int it = 0; it < WIT; ++it) {
+      const int e4 = tid + NTH * it;
+      if (NW4 % NTH != 0 && e4 >= NW4) break;
+      const int c = e4 / (LW / 4), i = 4 * (e4 % (LW / 4));
+      float4 v = wv[it];
+      if (c >= C || i >= d) v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (i + 1 >= d) v.y = 0.f;
+      if (i + 2 >= d) v.z = 0.f;
+      if (i + 3 >= d) v.w = 0.f;
+      *reinterpret_cast<float4*>(Ws + c * LW + i) = v;
+    }
   }
   {
     const float bv = bias[min(tid, C - 1)];  // (unconditional: clamped into the bias)
@@ -131,6 +174,12 @@ __global__ __launch_bounds__(256 * head_split(Q4, EVAL)) void head_kernel(HeadAr
       for (int e = 0; e < 4; ++e) hv[r][q][e] = 4 * lane + 256 * (qb + q) + e < d ? hv[r][q][e] : 0.f;
   __syncthreads();
 
+  // this lane's column group q in a row of W (clamped into a trimmed row)
+  const auto wcol = [&](int q) {
+    const int i = 4 * lane + 256 * (qb + q);
+    return TRIM ? min(i, pitch - 4) : i;
+  };
+
   // logits: lane-partial dot products, then one wave reduction per (row, class)
   float p[WR][CMAX];
 #pragma unroll
@@ -141,7 +190,7 @@ __global__ __launch_bounds__(256 * head_split(Q4, EVAL)) void head_kernel(HeadAr
   for (int q = 0; q < QH; ++q) {
 #pragma unroll
     for (int c = 0; c < CMAX; ++c) {
-      const f32x4 w = *reinterpret_cast<const f32x4*>(Ws + c * LW + 4 * lane + 256 * (qb + q));
+      const f32x4 w = *reinterpret_cast<const f32x4*>(Ws + c * pitch + wcol(q));
 #pragma unroll
       for (int r = 0; r < WR; ++r)
 #pragma unroll
@@ -253,6 +302,10 @@ __global__ __launch_bounds__(256 * head_split(Q4, EVAL)) void head_kernel(HeadAr
 
   // input gradient of the output layer, masked by the ReLU of H_{L-1}
   if (a.dprev) {
+    // a trimmed row's pitch made opaque, so that the logits' LDS addresses
+    // are recomputed here rather than held in registers across the softmax
+    int pitch2 = pitch;
+    if constexpr (TRIM) asm volatile("" : "+s"(pitch2));
 #pragma unroll
     for (int q = 0; q < QH; ++q) {
       const int i = 4 * lane + 256 * (qb + q);
@@ -261,7 +314,7 @@ __global__ __launch_bounds__(256 * head_split(Q4, EVAL)) void head_kernel(HeadAr
       for (int r = 0; r < WR; ++r) acc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int c = 0; c < CMAX; ++c) {
-        const f32x4 w = *reinterpret_cast<const f32x4*>(Ws + c * LW + i);
+        const f32x4 w = *reinterpret_cast<const f32x4*>(Ws + c * pitch2 + wcol(q));
 #pragma unroll
         for (int r = 0; r < WR; ++r)
 #pragma unroll
@@ -301,7 +354,7 @@ static int head_q4(int d) { return d <= 256 ? 1 : d <= 512 ? 2 : d <= 1024 ? 4 :
 
 size_t head_lds_bytes(int C, int d) {
   const int cm = head_cmax(C);
-  return ((size_t)cm * 256 * head_q4(d) + cm) * sizeof(float);
+  return ((size_t)cm * head_pitch(cm, head_q4(d), d) + cm) * sizeof(float);
 }
 
 // 16-byte accesses to the rows of H (and of the input gradient): d and the
@@ -315,10 +368,10 @@ static bool head_vec(const HeadArgs& a) {
 template <int CM, int QM, bool EVAL>
 static hipError_t head_go(const HeadArgs& a, hipStream_t s, bool prepare) {
   const size_t lds = head_lds_bytes(a.C, a.d);
-  if (prepare) {
+  if (prepare) {  // (the cap, not lds: contexts of other widths share the instance)
     if (lds <= 64 * 1024) return hipSuccess;
     return hipFuncSetAttribute((const void*)head_kernel<CM, QM, EVAL>,
-                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+                               hipFuncAttributeMaxDynamicSharedMemorySize, HEAD_LDS_CAP);
   }
   const int blocks = a.n * ((a.m + head_rows(EVAL) - 1) / head_rows(EVAL));
   HeadArgs v = a;
@@ -351,7 +404,7 @@ static hipError_t head_dispatch(const HeadArgs& a, hipStream_t s, bool prepare) 
 // on gfx950; beyond 64 KB the kernel's dynamic-LDS limit is raised first).
 bool head_prepare(int C, int d) {
   if (C > 32 || d > HEAD_DMAX) return false;
-  if (head_lds_bytes(C, d) > 160 * 1024 - 2048) return false;  // (+ the kernel's static LDS)
+  if (head_lds_bytes(C, d) > HEAD_LDS_CAP) return false;
   HeadArgs a{};
   a.C = C;
   a.d = d;

@@ -54,6 +54,9 @@ SMALL = [
     ("many_classes", (60, 50, 40), 3, 2, 24, 0.1, 2, 300, "gauss_linear", "permutation", "fp32"),
     ("wide_hidden", (30, 2100, 10), 2, 2, 8, 0.02, 2, 64, "gauss_linear", "permutation", "fp32"),
     ("big_head_lds", (50, 2000, 12), 2, 2, 16, 0.02, 2, 96, "gauss_linear", "permutation", "fp32"),
+    # 32-class fused kernel over a width whose LDS rows are trimmed to the
+    # width (1104 floats, not the 2048 its lanes span) to fit
+    ("head_32_classes_wide", (40, 1102, 30), 2, 2, 16, 0.05, 2, 96, "gauss_linear", "permutation", "fp32"),
     # the fused output layer with each row's columns split over two waves
     # (width > 256): rows that do not allow 16-byte accesses, and the output
     # layer fed by the gathered data rows directly (with and without them)
