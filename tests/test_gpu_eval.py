@@ -62,6 +62,8 @@ def check_rows(res, rl, rp, X, y, params, dims, dtype, tol):
 EVAL_CASES = [
     # name, dims, n, m, N rows, data, dtype
     ("head_ragged", (200, 130, 70, 10), 3, 40, 650, "gauss_linear", "fp32"),
+    # output weights in LDS rows trimmed to the width (1502, not a multiple of 4)
+    ("head_trimmed_rows", (40, 1502, 10), 2, 16, 300, "gauss_linear", "fp32"),
     ("unaligned_d0", (37, 29, 5), 4, 9, 101, "sparse_teacher2", "fp32"),
     ("many_classes", (60, 50, 40), 3, 24, 300, "gauss_linear", "fp32"),
     ("dl_shape", (100, 200, 136, 10), 3, 100, 1000, "sparse_teacher2", "fp32"),

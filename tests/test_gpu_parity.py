@@ -57,6 +57,7 @@ SMALL = [
     # 32-class fused kernel over a width whose LDS rows are trimmed to the
     # width (1104 floats, not the 2048 its lanes span) to fit
     ("head_32_classes_wide", (40, 1102, 30), 2, 2, 16, 0.05, 2, 96, "gauss_linear", "permutation", "fp32"),
+    ("head_trimmed_ragged", (50, 1502, 10), 3, 2, 16, 0.05, 2, 120, "gauss_linear", "permutation", "fp32"),
     # the fused output layer with each row's columns split over two waves
     # (width > 256): rows that do not allow 16-byte accesses, and the output
     # layer fed by the gathered data rows directly (with and without them)
