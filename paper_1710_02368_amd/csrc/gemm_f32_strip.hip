@@ -439,7 +439,7 @@ __device__ __forceinline__ const float* xblock_src(const float* x, int64_t ldx, 
   return x + (rowk + j) * ldx + gc;
 }
 
-template <bool LAST>
+template <bool LAST, bool ADAM>
 __global__ __launch_bounds__(512) void gemm_f32_strip_dw_kernel(GemmArgs dw) {
   __shared__ __attribute__((aligned(16))) float zs[Z_F];
   __shared__ __attribute__((aligned(16))) float xs0[H_F];
@@ -487,18 +487,26 @@ __global__ __launch_bounds__(512) void gemm_f32_strip_dw_kernel(GemmArgs dw) {
     rowo[r] = wo + (int64_t)min(i, dw.M - 1) * dw.ldw;
   }
   f32x4 aw[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
-  f32x2 wsrc[4], snap[4];
+  f32x2 wsrc[4], snap[4], mw[4], vw[4];
   float bsum = 0.f;
+  const AdamCoef ac = ADAM ? adam_coef(dw.g, dw.adam) : AdamCoef{1.f, 1.f};
 
   // the update of block t (columns j0 = 64t + 32wj + 2li, +1): its operands
-  // (UPL loads) and its stores (exactly 4, past an edge into the sink)
-  constexpr int UPL = LAST ? 8 : 4;
+  // (UPL loads: W_src, the snapshot on the last step, Adam's two moments)
+  // and its stores (UST: the weights and the moments, every lane storing,
+  // past an edge into the sink)
+  constexpr int UPL = 4 + (LAST ? 4 : 0) + (ADAM ? 8 : 0);
+  constexpr int UST = ADAM ? 12 : 4;
   auto load_update = [&](int t) {
     const int j = min(BLK * t + 32 * wj + 2 * li, dw.N - 2);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       wsrc[r] = *reinterpret_cast<const f32x2*>(dw.w_src + rowo[r] + j);
       if (LAST) snap[r] = *reinterpret_cast<const f32x2*>(dw.w_snap + rowo[r] + j);
+      if (ADAM) {
+        mw[r] = *reinterpret_cast<const f32x2*>(dw.adam.mw + rowo[r] + j);
+        vw[r] = *reinterpret_cast<const f32x2*>(dw.adam.vw + rowo[r] + j);
+      }
     }
   };
   auto store_update = [&](int t) {
@@ -506,23 +514,36 @@ __global__ __launch_bounds__(512) void gemm_f32_strip_dw_kernel(GemmArgs dw) {
     f32x2* sink = reinterpret_cast<f32x2*>(dw.sink) + (lane & 31);
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      f32x2 v = {wsrc[r].x - dw.eta * aw[0][r], wsrc[r].y - dw.eta * aw[1][r]};
+      f32x2 d = {aw[0][r], aw[1][r]};
+      if (ADAM) {
+        float mx = mw[r].x, my = mw[r].y, vx = vw[r].x, vy = vw[r].y;
+        d.x = adam_moments(d.x, mx, vx, dw.adam, ac);
+        d.y = adam_moments(d.y, my, vy, dw.adam, ac);
+        mw[r] = f32x2{mx, my};
+        vw[r] = f32x2{vx, vy};
+      }
+      f32x2 v = {wsrc[r].x - dw.eta * d.x, wsrc[r].y - dw.eta * d.y};
       if (LAST) {
         v.x = (v.x - snap[r].x) / dw.lam;
         v.y = (v.y - snap[r].y) / dw.lam;
       }
-      f32x2* dst = rin[r] && j < dw.N ? reinterpret_cast<f32x2*>(dw.w_dst + rowo[r] + j) : sink;
+      const bool in = rin[r] && j < dw.N;
+      f32x2* dst = in ? reinterpret_cast<f32x2*>(dw.w_dst + rowo[r] + j) : sink;
       if (LAST)
         *dst = v;
       else
         __builtin_nontemporal_store(v, dst);
+      if (ADAM) {
+        __builtin_nontemporal_store(mw[r], in ? reinterpret_cast<f32x2*>(dw.adam.mw + rowo[r] + j) : sink);
+        __builtin_nontemporal_store(vw[r], in ? reinterpret_cast<f32x2*>(dw.adam.vw + rowo[r] + j) : sink);
+      }
     }
   };
 
   // Per block t: wait for its loads; issue the loads of block t+1 (waves
   // 0-3); the product of block t from LDS; then its update's stores and the
   // update operands of block t+1.  Those two sets of memory operations
-  // (4 + UPL per wave) are younger than every direct load a wave waits for
+  // (UST + UPL per wave) are younger than every direct load a wave waits for
   // at the next block, so they stay in flight across the barrier; a store
   // or load issued at the start of a block waited behind that block's
   // direct loads.
@@ -533,7 +554,7 @@ __global__ __launch_bounds__(512) void gemm_f32_strip_dw_kernel(GemmArgs dw) {
     if (t == 0)
       wait_vm<UPL>();
     else
-      wait_vm<4 + UPL>();
+      wait_vm<UST + UPL>();
     barrier();
     if (t + 1 < T && wave < 4) fire_x(std::integral_constant<int, 4>{}, t + 1, (t & 1) ? xs0 : xs1);
     if (t == 0 && wj == 0) {
@@ -549,10 +570,16 @@ __global__ __launch_bounds__(512) void gemm_f32_strip_dw_kernel(GemmArgs dw) {
     // the bias of rows i0 + 16wi + li: lane groups 1..3 hold partial sums
     // of the same column of dZ_1 as group 0, added in a fixed order
     const float p1 = __shfl(bsum, li + 16), p2 = __shfl(bsum, li + 32), p3 = __shfl(bsum, li + 48);
-    const float tot = ((bsum + p1) + p2) + p3;
+    float tot = ((bsum + p1) + p2) + p3;
     const int i = i0 + 16 * wi + li;
     if (lg == 0 && i < dw.M) {
       const int64_t e = wo + i;
+      if (ADAM) {
+        float mb = dw.adam.mb[e], vb = dw.adam.vb[e];
+        tot = adam_moments(tot, mb, vb, dw.adam, ac);
+        dw.adam.mb[e] = mb;
+        dw.adam.vb[e] = vb;
+      }
       const float nb = dw.b_src[e] - dw.eta * tot;
       dw.b_dst[e] = LAST ? (nb - dw.b_snap[e]) / dw.lam : nb;
     }
@@ -606,11 +633,13 @@ hipError_t launch_gemm_f32_strip_bwd(const GemmArgs& dx, const GemmArgs& dw, hip
 }
 
 // The strip schedule of the first layer's weight gradient: gathered data
-// rows as B (a batch within a shard), dZ_1 as A, SGD as the local rule, a
-// mini-batch of at most 128 rows, 16-byte rows, and enough strips (workers x
-// 64-row strips of W_0) to give every compute unit several workgroups.
+// rows as B (a batch within a shard), dZ_1 as A, SGD or Adam as the local
+// rule, a mini-batch of at most 128 rows, 16-byte rows, and enough strips
+// (workers x 64-row strips of W_0) to give every compute unit several
+// workgroups.
 bool gemm_f32_strip_dw_ok(const GemmArgs& dw) {
-  if (dw.epi != EPI_DW_UPDATE || !dw.zero || !dw.sink || dw.adam.on || dw.w_dst16) return false;
+  if (dw.epi != EPI_DW_UPDATE || !dw.zero || !dw.sink || dw.w_dst16) return false;
+  if (dw.adam.on && (!aligned16(dw.adam.mw) || !aligned16(dw.adam.vw) || !dw.adam.mb || !dw.adam.vb)) return false;
   if (!dw.b.gather || dw.a.gather || dw.K < 1 || dw.K > ROWS || dw.K > dw.g.S) return false;
   if (dw.M % 4 || dw.N % 4 || dw.N < 2) return false;
   const void* ptrs[] = {dw.a.ptr, dw.b.ptr, dw.w_src, dw.w_dst, dw.zero, dw.sink};
@@ -625,10 +654,16 @@ bool gemm_f32_strip_dw_ok(const GemmArgs& dw) {
 hipError_t launch_gemm_f32_strip_dw(const GemmArgs& dw, hipStream_t s) {
   if (!gemm_f32_strip_dw_ok(dw)) return hipErrorInvalidValue;
   const dim3 grid((unsigned)(dw.batch * ((dw.M + STRIP - 1) / STRIP))), block(512);
-  if (dw.last)
-    AGN_LAUNCH((gemm_f32_strip_dw_kernel<true>), grid, block, 0, s, dw);
-  else
-    AGN_LAUNCH((gemm_f32_strip_dw_kernel<false>), grid, block, 0, s, dw);
+  if (dw.adam.on) {
+    if (dw.last)
+      AGN_LAUNCH((gemm_f32_strip_dw_kernel<true, true>), grid, block, 0, s, dw);
+    else
+      AGN_LAUNCH((gemm_f32_strip_dw_kernel<false, true>), grid, block, 0, s, dw);
+  } else if (dw.last) {
+    AGN_LAUNCH((gemm_f32_strip_dw_kernel<true, false>), grid, block, 0, s, dw);
+  } else {
+    AGN_LAUNCH((gemm_f32_strip_dw_kernel<false, false>), grid, block, 0, s, dw);
+  }
   return hipGetLastError();
 }
 

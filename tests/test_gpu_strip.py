@@ -1,8 +1,8 @@
 """The strip schedules against the oracle: the backward launch of a float32
 hidden layer (input gradient and weight gradient + update sharing each
-weight block in LDS) and, with SGD, the first layer's weight gradient +
-update as 64-row strips of W_0 (gathered data rows streamed past a dZ_1
-strip held in LDS).  The library takes them when workers x strips of 64
+weight block in LDS) and the first layer's weight gradient + update as
+64-row strips of W_0 (gathered data rows streamed past a dZ_1 strip held in
+LDS).  The library takes them when workers x strips of 64
 reach 1024 (one workgroup per compute unit at a time), so these shapes use
 many workers: 64 x 16 and 128 x 8 strips.
 
@@ -11,7 +11,8 @@ multiples of 64; 968 leaves 8 rows in the last block, so most of its MFMA
 groups are skipped), a row stride padded past the width (996 -> 1000), a
 mini-batch below the 128 rows the schedule holds (m = 100), several local
 steps (the round's last step stores the normalized displacement), two
-rounds, Adam as the local rule.  Gates as in the full-size tests
+rounds, Adam as the local rule (also on the first layer's strips, over
+several column blocks of W_0 with a ragged last one).  Gates as in the full-size tests
 (test_gpu_fullsize.py): round 1 against the live oracle on the whole central
 variable, every delta and every pulled copy, and the commit bit for bit;
 round 2 on the central variable and the pulled copies.  Adam: see
@@ -36,6 +37,7 @@ STRIP_CASES = [
     ("strip_short_tail", (96, 1000, 968, 12), 64, 2, 128, 0.02, 2, 64 * 300, "sparse_teacher2"),
     ("strip_two_hidden", (64, 512, 768, 512, 10), 128, 3, 128, 0.02, 2, 128 * 256, "sparse_teacher2"),
     ("strip_adam", (64, 516, 512, 10), 128, 3, 120, 0.002, 2, 128 * 256, "sparse_teacher2", ADAM),
+    ("strip_adam_first_layer", (200, 516, 10), 128, 3, 120, 0.002, 2, 128 * 256, "sparse_teacher2", ADAM),
 ]
 
 
